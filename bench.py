@@ -1,0 +1,227 @@
+"""Benchmark of one training step of an MLP workload on one MI355X.
+
+A step is one ``dlvm_gradient`` call (the forward recomputed from the original
+inputs, then the whole adjoint) followed, for workloads with an SGD update, by
+one ``dlvm_sgd_step`` call, over one batch of seeded synthetic inputs that are
+resident in device memory before the timed region starts.
+
+Prints one JSON line. ``value`` is steps per second of the whole job on one
+GPU. ``roofline`` describes the kernel that takes the most time in a step: its
+algorithmic flops (or bytes) per launch, divided by its average launch
+duration measured with HIP events on the launch stream during the timed steps.
+``cpu_baseline`` times the float64 oracle on the host cores on a bounded sample
+of the same workload.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c2]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+
+import workloads  # noqa: E402
+
+METRIC = "MLP fwd+grad steps/s, TFLOP/s (% MFMA peak); fused elementwise GB/s"
+# MI355X published peaks: dense MFMA per dtype, and HBM3E bandwidth.
+PEAK_TFLOPS = {"f32": 157.3, "bf16": 2500.0}
+PEAK_HBM_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=None)
+    ap.add_argument("--warmup", type=int, default=None)
+    ap.add_argument("--workload", default="c2", choices=sorted(workloads.WORKLOADS))
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="budget of the oracle CPU baseline (0 disables it)")
+    ap.add_argument("--traffic", default=None,
+                    help="JSON file with measured HBM bytes per launch of the dominant kernel")
+    return ap.parse_args()
+
+
+def default_steps(wl) -> tuple[int, int]:
+    flops = wl.flops()
+    if flops > 1e12:
+        return 30, 5
+    if flops > 1e10:
+        return 200, 20
+    return 2000, 100
+
+
+def cpu_baseline(wl, budget_s: float) -> dict | None:
+    """Time the oracle (as it stands) on the host on a bounded sample."""
+    if budget_s <= 0:
+        return None
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([d.get("num_threads", 1) for d in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover - threadpoolctl is optional
+        threads = os.cpu_count() or 1
+    # sample: the whole batch when one oracle step is short, else a slice of rows
+    rows = wl.batch
+    while rows > 16 and wl.flops(rows) > 6e10:
+        rows //= 2
+    x, params, y = workloads.make_inputs(wl, batch=rows)
+    spec = oracle.MlpSpec(wl.widths, wl.acts, wl.loss, wl.dtype)
+    n = 0
+    t_grad = t_sgd = 0.0
+    while True:
+        t0 = time.perf_counter()
+        loss, grads, _ = oracle.mlp_gradient(spec, x, params, y, wrt_x=wl.wrt_x)
+        t1 = time.perf_counter()
+        if wl.sgd:
+            for (W, b), (dW, db) in zip(params, grads):
+                oracle.sgd_f32(W, dW, wl.lr)
+                oracle.sgd_f32(b, db, wl.lr)
+        t2 = time.perf_counter()
+        t_grad += t1 - t0
+        t_sgd += t2 - t1
+        n += 1
+        el = t_grad + t_sgd
+        if el >= budget_s or el * (n + 1) / n > 2 * budget_s:
+            break
+    # the gradient's work is linear in the rows; the update's does not depend on them
+    per_step = (t_grad / n) * (wl.batch / rows) + t_sgd / n
+    sample = (f"{n} oracle steps (float64 gradient{' + SGD' if wl.sgd else ''}) on "
+              f"{rows} of {wl.batch} rows in {el:.1f} s")
+    if rows != wl.batch:
+        sample += (f"; gradient time scaled by {wl.batch}/{rows} rows (each of its terms is "
+                   "linear in the rows), update time taken as measured")
+    return {"value": 1.0 / per_step, "unit": "steps/s", "cores": int(threads),
+            "kind": "oracle", "sample": sample}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the workloads "
+              "here are single-GPU and no multi-GPU path is built", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    import paper_1711_03016_amd as dl
+
+    wl = workloads.WORKLOADS[args.workload]
+    steps, warmup = default_steps(wl)
+    steps = args.steps if args.steps is not None else steps
+    warmup = args.warmup if args.warmup is not None else warmup
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    tdt = torch.float32 if wl.dtype == "f32" else torch.bfloat16
+
+    # inputs, resident in device memory before timing
+    x, params, y = workloads.make_inputs(wl)
+    B = wl.batch
+    m = dl.Model(wl.widths, wl.acts, wl.dtype, wl.loss, wl.wrt_x, B)
+    P = m.pack(params, dev, tdt)
+    master = m.pack(params, dev, torch.float32) if wl.dtype == "bf16" and wl.sgd else None
+    del params
+    xd = torch.from_numpy(x).to(dev).to(tdt)
+    yd = None if y is None else torch.from_numpy(y).to(dev)
+    del x
+    ws = torch.empty(m.workspace_bytes(B), dtype=torch.uint8, device=dev)
+    loss = torch.empty(1, device=dev)
+    dP = torch.empty(m.param_count(), device=dev)
+    dx = torch.empty((B, wl.widths[0]), device=dev) if wl.wrt_x else None
+    stream = torch.cuda.current_stream()
+
+    def step():
+        m.gradient(P, xd, yd, B, loss, dP, dx, ws, stream)
+        if wl.sgd:
+            m.sgd_step(P, master, dP, wl.lr, stream)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    if m.check(ws) != dl.OK:
+        raise RuntimeError("device flags raised during warm-up")
+
+    # find the launch that takes the most time (outside the timed region)
+    plan = m.plan(B)
+    if not wl.sgd:
+        plan = plan[:-1]
+    probe_steps = 3
+    m.probe_arm(-1, probe_steps * len(plan) + 8)
+    for _ in range(probe_steps):
+        step()
+    torch.cuda.synchronize()
+    times = []
+    for e in plan:
+        n, ms = m.probe_read(e["index"])
+        times.append(ms / max(n, 1))
+    dom = plan[int(np.argmax(times))]
+    m.probe_disarm()
+
+    # timed region: the dominant launch is bracketed by HIP events on its stream
+    m.probe_arm(dom["index"], steps)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    n_dom, ms_dom = m.probe_read(dom["index"])
+    m.probe_disarm()
+    elapsed = t1 - t0
+    sps = steps / elapsed
+    avg_s = ms_dom / max(n_dom, 1) / 1e3
+
+    if dom["flops"] > 0:
+        achieved = dom["flops"] / avg_s / 1e12
+        peak = PEAK_TFLOPS[wl.dtype]
+        roof = {"bound": "mfma", "achieved": round(achieved, 3), "peak": peak,
+                "unit": "TFLOP/s", "frac": round(achieved / peak, 4)}
+    else:
+        achieved = dom["bytes"] / avg_s / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
+                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4)}
+    traffic = None
+    if args.traffic:
+        with open(args.traffic) as f:
+            t = json.load(f)
+        if t.get("kernel") == dom["name"] and t.get("workload") == wl.name:
+            traffic = t.get("bytes_per_launch")
+    roof["traffic"] = traffic
+    roof["kernel"] = (f"{dom['name']} M={dom['M']} N={dom['N']} K={dom['K']} "
+                      f"(launch {dom['index']} of {len(plan)}, {n_dom} timed launches, "
+                      f"avg {avg_s * 1e6:.2f} us)")
+
+    step_flops = wl.flops()
+    tflops = step_flops * sps / 1e12
+    out = {
+        "metric": METRIC,
+        "value": round(sps, 3),
+        "unit": "steps/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": warmup,
+        "ms_per_step": round(elapsed / steps * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": wl.dtype,
+        "data": "synthetic",
+        "config": {"workload": f"{wl.name}: {wl.title}", "global_batch": B,
+                   "widths": list(wl.widths), "loss": wl.loss, "parallelism": "none"},
+        "tflops": round(tflops, 3),
+        "mfma_frac": round(tflops / PEAK_TFLOPS[wl.dtype], 4),
+        "roofline": roof,
+    }
+    del P, master, xd, ws, dP, dx
+    out["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

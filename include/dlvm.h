@@ -1,0 +1,249 @@
+/*
+ * dlvm.h - C ABI of the MI355X (gfx950) hot path of a DLVM-compiled network:
+ * a differentiable linear-algebra function (dense layers plus element-wise
+ * chains) and its generated adjoint.
+ *
+ * Paper: R. Wei, L. Schwartz, V. Adve, "DLVM: A modern compiler infrastructure
+ * for deep learning systems", arXiv 1711.03016.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Tensors are row-major and dense. A layer maps K inputs to N outputs on a
+ *   batch of B rows: X is [B, K], W is [K, N], b is [N], H = act(X.W + b) is
+ *   [B, N] (the orientation of Fig. 3: x <1 x 784>, w <784 x 10>).
+ * - Every tensor argument is a DEVICE pointer owned by the caller; the
+ *   library never allocates, frees or keeps tensor memory. Device pointers must
+ *   be 16-byte aligned (else DLVM_ERR_MISALIGNED).
+ * - "dtype" is the storage type: DLVM_F32 (float32 storage and arithmetic) or
+ *   DLVM_BF16 (bfloat16 storage, float32 accumulation and epilogue arithmetic,
+ *   round-to-nearest-even on every float32 -> bf16 store). Losses, logits,
+ *   gradients of parameters and of x, and SGD master weights are float32.
+ * - Every call is asynchronous on the given stream (a hipStream_t passed as
+ *   void*; NULL is the default stream). Errors found on the host return at once
+ *   and enqueue nothing. A launch failure returns DLVM_ERR_HIP. Device-side
+ *   conditions (a label out of range, a non-finite loss) are latched in the
+ *   workspace and reported by dlvm_check.
+ * - No call allocates device memory or issues a memset, so the calls can be
+ *   captured into a HIP graph.
+ * - Results are deterministic: the same inputs give bitwise-identical outputs
+ *   (fixed reduction orders, no floating-point atomics).
+ * - No C++ exception crosses this interface. dlvm_last_error() returns a
+ *   thread-local message describing the last failure on the calling thread.
+ */
+#ifndef DLVM_H
+#define DLVM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t dlvm_status;
+enum {
+  DLVM_OK = 0,
+  DLVM_ERR_INVALID_ARG = -1,  /* null pointer, bad shape/dtype, batch > batch_max */
+  DLVM_ERR_MISALIGNED = -2,   /* a device pointer is not 16-byte aligned */
+  DLVM_ERR_WORKSPACE = -3,    /* workspace missing or smaller than required */
+  DLVM_ERR_UNSUPPORTED = -4,  /* a combination this library does not implement */
+  DLVM_ERR_HIP = -5,          /* a HIP launch or runtime call failed */
+  DLVM_ERR_LABEL_RANGE = -6,  /* dlvm_check: a label was outside [0, classes) */
+  DLVM_ERR_NONFINITE = -7     /* dlvm_check: the loss was NaN or infinite */
+};
+
+enum { DLVM_F32 = 0, DLVM_BF16 = 1 };
+enum { DLVM_ACT_NONE = 0, DLVM_ACT_SIGMOID = 1, DLVM_ACT_TANH = 2, DLVM_ACT_RELU = 3 };
+enum { DLVM_LOSS_SOFTMAX_CE = 0, DLVM_LOSS_CHAIN8 = 1 };
+
+/* Static description of a network: the shape-specialised function of the
+ * NNKit JIT (section 3.4) fixed once per handle. */
+typedef struct dlvm_mlp_desc {
+  int32_t n_layers;        /* L >= 1 */
+  const int32_t* widths;   /* L + 1 host ints: widths[0] = K0 (input), widths[L] = classes */
+  const int32_t* acts;     /* L host ints (DLVM_ACT_*); acts[L-1] must be DLVM_ACT_NONE */
+  int32_t dtype;           /* DLVM_F32 or DLVM_BF16 */
+  int32_t loss;            /* DLVM_LOSS_SOFTMAX_CE, or DLVM_LOSS_CHAIN8 (L == 1, widths[0] == widths[1]) */
+  int32_t wrt_x;           /* 1: dlvm_gradient also returns dL/dx (required for CHAIN8) */
+  int64_t batch_max;       /* largest batch any call will use */
+} dlvm_mlp_desc;
+
+typedef struct dlvm_model dlvm_model;
+
+/* ---------------------------------------------------------------------------
+ * Model-level entry points
+ * ------------------------------------------------------------------------- */
+
+/* Create a handle for a network (host only; touches no device). The handle
+ * owns the copied description and the launch plan, never tensor memory.
+ * Softmax cross-entropy networks (section 3.1.1: softmax composed from
+ * primitives): H_l = act_l(H_{l-1}.W_l + b_l), logits = H_L, loss = mean over
+ * rows of logsumexp(logits_i) - logits_i[y_i]. CHAIN8 networks: one dense
+ * layer z = x.W, then the element-wise chain e = sigmoid(0.5 tanh(z + b) + 1)
+ * * x, loss = mean(e * e) (x_skip = x). */
+dlvm_status dlvm_create(const dlvm_mlp_desc* desc, dlvm_model** out);
+void dlvm_destroy(dlvm_model* m);
+
+/* Number of elements of the flat parameter buffer (including padding). The
+ * flat buffer holds W_1, b_1, ..., W_L, b_L, each starting on a 256-byte
+ * boundary (linear-algebra fusion passes pre-concatenated parameters,
+ * section 3.1.2). The same element layout is used for params (storage dtype),
+ * master weights (float32) and dparams (float32). */
+int64_t dlvm_param_count(const dlvm_model* m);
+
+/* Element offsets of W_l and b_l: offsets[2l] = W_{l+1}, offsets[2l+1] = b_{l+1}
+ * for l in [0, L), and the row stride of each W: element (k, n) of W_{l+1} is
+ * at offsets[2l] + k * lds[l] + n. lds[l] is the layer width, except that the
+ * class dimension of a softmax network's last layer is rounded up to a
+ * multiple of 8 (16-byte rows, the padded tensors of section 3.1.2); its
+ * padding columns must be zero in params (they stay zero under dlvm_sgd_step)
+ * and are written as zero in dparams. `offsets` is a host array of 2L int64,
+ * `lds` (may be NULL) of L int64. */
+dlvm_status dlvm_param_layout(const dlvm_model* m, int64_t* offsets, int64_t* lds);
+
+/* Bytes of workspace a forward or gradient call at `batch` rows needs
+ * (0 if the batch is invalid). Holds saved activations, adjoints, loss
+ * partials and the device error flags. One workspace must not be used by two
+ * calls that may run concurrently. */
+size_t dlvm_workspace_bytes(const dlvm_model* m, int64_t batch);
+
+/* The original function (Fig. 3's @foo): writes `out`, float32 [batch, widths[L]]:
+ * the logits for SOFTMAX_CE, the chain value e for CHAIN8. Saves nothing (the
+ * forward of a function that is not differentiated keeps no activations). */
+dlvm_status dlvm_forward(const dlvm_model* m, const void* params, const void* x,
+                         int64_t batch, float* out, void* ws, size_t ws_bytes,
+                         void* stream);
+
+/* The gradient function (section 3.1.3; gradient declaration "wrt params
+ * [, x] keeping loss"): recomputes the forward from the original inputs,
+ * then runs the adjoint. Writes loss (one float32 on the device), dparams
+ * (float32, flat layout, padding set to zero) and, iff wrt_x, dx (float32
+ * [batch, widths[0]]). `labels` are int32 [batch] in [0, classes) for
+ * SOFTMAX_CE and NULL for CHAIN8. The input gradient of the first layer is
+ * not computed unless wrt_x (dead code elimination, section 3.1.3). */
+dlvm_status dlvm_gradient(const dlvm_model* m, const void* params, const void* x,
+                          const int32_t* labels, int64_t batch, float* loss,
+                          float* dparams, float* dx, void* ws, size_t ws_bytes,
+                          void* stream);
+
+/* Plain SGD over the whole flat buffer in one launch: params -= lr * dparams.
+ * F32 models update params in place and take master == NULL. BF16 models
+ * update the float32 `master` copy and write params = bf16(master). */
+dlvm_status dlvm_sgd_step(const dlvm_model* m, void* params, float* master,
+                          const float* dparams, float lr, void* stream);
+
+/* Synchronise `stream` and read the device flags that the last gradient call
+ * using `ws` wrote (every gradient call rewrites them): returns
+ * DLVM_ERR_LABEL_RANGE if a label was outside [0, classes) (that row's loss
+ * term is NaN), else DLVM_ERR_NONFINITE if the loss was NaN or infinite, else
+ * DLVM_OK. The step-level loss calls write the same flags at the start of
+ * their `ws`, so dlvm_check also reads those. */
+dlvm_status dlvm_check(const dlvm_model* m, void* ws, void* stream);
+
+/* Message describing the last failure on this thread ("" if none). */
+const char* dlvm_last_error(void);
+
+/* ---------------------------------------------------------------------------
+ * Launch plan and timing probe (instrumentation)
+ * ------------------------------------------------------------------------- */
+
+/* One kernel launch of a training step: a dlvm_gradient call followed by a
+ * dlvm_sgd_step call. `flops` counts 2*M*N*K for a matrix product (else 0);
+ * `bytes` is the algorithmic minimum of device-memory traffic: every operand
+ * read once and every result written once. */
+typedef struct dlvm_launch_info {
+  char name[48];
+  int64_t M, N, K;
+  double flops;
+  double bytes;
+} dlvm_launch_info;
+
+/* Number of launches in one step at `batch` rows (gradient launches, then
+ * the one SGD launch), or 0 if the batch is invalid. */
+int32_t dlvm_plan_size(const dlvm_model* m, int64_t batch);
+/* Description of launch `index` (0-based, in enqueue order) of a step. */
+dlvm_status dlvm_plan_entry(const dlvm_model* m, int64_t batch, int32_t index,
+                            dlvm_launch_info* info);
+
+/* Arm the probe: subsequent launches at position `index` of a step (-1: every
+ * position) made by this handle's dlvm_gradient / dlvm_sgd_step calls are
+ * bracketed by HIP events recorded on the call's stream, for the first
+ * `capacity` such launches. Arming creates the events (a runtime call, done
+ * before any timed region); recording them allocates nothing. Re-arming
+ * discards earlier records. */
+dlvm_status dlvm_probe_arm(dlvm_model* m, int32_t index, int32_t capacity);
+/* Synchronise on the recorded events and return how many launches at position
+ * `index` were recorded and their summed duration in milliseconds. */
+dlvm_status dlvm_probe_read(dlvm_model* m, int32_t index, int64_t* count, double* total_ms);
+/* Stop recording and release the events. */
+dlvm_status dlvm_probe_disarm(dlvm_model* m);
+
+/* ---------------------------------------------------------------------------
+ * Step-level entry points: the individual steps the model-level calls are
+ * made of, exported so each can be driven and checked on its own.
+ * ------------------------------------------------------------------------- */
+
+/* Dense layer forward with the bias add and activation fused into the matrix
+ * product (linear-algebra fusion, section 3.1.2; element-wise operator
+ * fusion, section 1): H[M,N] = act(alpha * X[M,K].W[K,N] + bias[N]).
+ * X, W, bias (may be NULL) are `dtype`; H is `out_dtype` (F32, or BF16 when
+ * dtype is BF16). */
+dlvm_status dlvm_dense_forward(int32_t dtype, int32_t out_dtype, int32_t act,
+                               int64_t M, int64_t N, int64_t K, float alpha,
+                               const void* X, const void* W, const void* bias,
+                               void* H, void* stream);
+
+/* Adjoint of the dense layer with respect to its input (adjoint of dot:
+ * dX = dY.W^T, transpose never materialised), fused with the adjoint of the
+ * previous layer's activation taken from its saved output Hprev, plus an
+ * optional second adjoint contribution R to the same value (a value used in
+ * two places receives the sum of both adjoints):
+ * dX[M,K] = (dY[M,N].W[K,N]^T) * act'(Hprev[M,K]) + R[M,K].
+ * act' is s(1-s) for sigmoid, 1-t^2 for tanh, [h > 0] for relu, 1 for none
+ * (Hprev may then be NULL). R (may be NULL) has dX's type. dY, W, Hprev are
+ * `dtype`; dX is `out_dtype`. dX may alias R (in-place accumulate). */
+dlvm_status dlvm_dense_backward_data(int32_t dtype, int32_t out_dtype,
+                                     int32_t act_prev, int64_t M, int64_t N,
+                                     int64_t K, const void* dY, const void* W,
+                                     const void* Hprev, const void* R, void* dX,
+                                     void* stream);
+
+/* Adjoint of the dense layer with respect to its parameters: dW[K,N] =
+ * X[M,K]^T.dY[M,N] and db[N] = sum over rows of dY (the padded product
+ * [X 1]^T.dY = [dW; db] of section 3.1.2). X, dY are `dtype`; dW, db are
+ * float32 (db may be NULL). */
+dlvm_status dlvm_dense_backward_params(int32_t dtype, int64_t M, int64_t N,
+                                       int64_t K, const void* X, const void* dY,
+                                       float* dW, float* db, void* stream);
+
+/* Softmax cross-entropy and its adjoint on float32 logits [rows, classes]
+ * (softmax composed of exp, reduce-add, log; section 3.1.1):
+ * loss = scale * sum_i (logsumexp(z_i) - z_i[y_i]),
+ * dlogits = scale * (softmax(z) - onehot(y)), stored as `dtype`.
+ * `ws` needs dlvm_softmax_xent_ws_bytes(rows) bytes; flags latch in it. */
+size_t dlvm_softmax_xent_ws_bytes(int64_t rows);
+dlvm_status dlvm_softmax_xent(int32_t dtype, int64_t rows, int64_t classes,
+                              const float* logits, const int32_t* labels,
+                              float scale, void* dlogits, float* loss, void* ws,
+                              size_t ws_bytes, void* stream);
+
+/* The eight-operator element-wise chain, forward and adjoint fused in one
+ * pass over float32 [rows, cols] tensors: a = tanh(z + b), s = sigmoid(0.5a + 1),
+ * e = s * x_skip, loss = mean(e^2) (x^2 simplified to x*x, section 3.1.2);
+ * zbar = dL/dz, xbar = dL/dx_skip. `ws` needs dlvm_chain8_ws_bytes(rows, cols). */
+size_t dlvm_chain8_ws_bytes(int64_t rows, int64_t cols);
+dlvm_status dlvm_chain8(int64_t rows, int64_t cols, const float* z,
+                        const float* bias, const float* x_skip, float* zbar,
+                        float* xbar, float* loss, void* ws, size_t ws_bytes,
+                        void* stream);
+
+/* Fused SGD over n elements: F32: params -= lr * grads (master NULL).
+ * BF16: master -= lr * grads, params = bf16(master). */
+dlvm_status dlvm_sgd(int32_t dtype, int64_t n, void* params, float* master,
+                     const float* grads, float lr, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DLVM_H */

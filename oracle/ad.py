@@ -21,6 +21,11 @@ The adjoint rules are the textbook ones for each primitive. Where an operand
 was broadcast (all element-wise binary operators broadcast, §3.1.1), its
 adjoint is summed over the broadcast axes.
 
+``cast`` (dataTypeCast to bf16) is differentiated as the identity: its adjoint
+is the incoming adjoint cast back to the operand's type, which in float64 is
+the incoming adjoint itself. (Rounding is piecewise constant; the convention
+used by every mixed-precision program is to pass the adjoint straight through.)
+
 ``reduce_max`` only ever appears as the shift inside log-sum-exp. Its adjoint
 is routed to the positions that attain the maximum (compare + select); in the
 shift-invariant composite the two contributions through the shift cancel, so
@@ -33,7 +38,7 @@ from .ir import BOOL, F64, Function, Instr
 # Instructions through which derivatives flow.
 _DIFFERENTIABLE = {
     "neg", "exp", "log", "tanh", "add", "sub", "mul", "div", "power",
-    "select", "dot", "transpose", "reduce_add", "reduce_max", "broadcast",
+    "select", "dot", "transpose", "reduce_add", "reduce_max", "broadcast", "cast",
 }
 
 
@@ -169,6 +174,8 @@ def differentiate(fn: Function, wrt, keeping=(), seedable: bool = False,
             acc(a[0], g.select(hit, g.broadcast(vb, g.shape(a[0])), g.const(0.0)))
         elif op == "broadcast":
             acc(a[0], _unbroadcast(g, vb, g.shape(a[0])))
+        elif op == "cast":
+            acc(a[0], vb)
         else:  # compare, iota, const: no adjoint flows through these
             raise AssertionError(f"active value from non-differentiable op {op}")
 

@@ -24,6 +24,10 @@ What it follows (DLVM, arXiv 1711.03016):
 * ``broadcast`` materialises a NumPy-style broadcast; it is the explicit form
   of the implicit broadcasting of element-wise binary operators and is what the
   adjoint of a reduction expands into.
+* ``cast`` is Table 1's ``dataTypeCast``. Only the cast to bf16 is used: the
+  value becomes the bf16 number nearest (round to nearest, ties to even) to the
+  float32 rounding of the operand, kept as a float64. A network stored in bf16
+  is the function with such a cast on every activation it stores.
 
 Every value is a NumPy array. Floating-point values are float64 throughout;
 ``bool`` values come from compare instructions and ``int64`` values are
@@ -125,10 +129,17 @@ class Function:
                                _broadcast_shape(self.shape(a), self.shape(b)))
         return self._add(Instr("select", (cond, a, b), shp, F64))
 
-    def dot(self, a: int, b: int) -> int:
+    def dot(self, a: int, b: int, acc: str = "f64") -> int:
+        """Matrix product; ``acc="f32"`` accumulates in float32 instead of float64.
+
+        The float32 form exists only to measure how much a network's results
+        depend on the accumulation order (see ``MlpSpec.accumulate``).
+        """
         (m, k1), (k2, n) = self.shape(a), self.shape(b)
         assert k1 == k2, (self.shape(a), self.shape(b))
-        return self._add(Instr("dot", (a, b), (m, n), F64))
+        assert acc in ("f64", "f32")
+        attrs = {"acc": acc} if acc == "f32" else {}
+        return self._add(Instr("dot", (a, b), (m, n), F64, attrs))
 
     def transpose(self, a: int) -> int:
         m, n = self.shape(a)
@@ -146,6 +157,11 @@ class Function:
         else:
             out = tuple(1 if i == axis else s for i, s in enumerate(shp))
         return self._add(Instr("reduce_" + kind, (a,), out, F64, {"axis": axis}))
+
+    def cast(self, a: int, to: str = "bf16") -> int:
+        """``dataTypeCast a to <to>`` (only bf16 is used)."""
+        assert to == "bf16" and self.dtype(a) == F64
+        return self._add(Instr("cast", (a,), self.shape(a), F64, {"to": to}))
 
     def broadcast(self, a: int, shape) -> int:
         shape = tuple(shape)
@@ -240,6 +256,8 @@ def _eval_instr(ins: Instr, vals: list, args: list):
     if op == "select":
         return np.where(a[0], a[1], a[2])
     if op == "dot":
+        if ins.attrs.get("acc") == "f32":
+            return (a[0].astype(np.float32) @ a[1].astype(np.float32)).astype(np.float64)
         return a[0] @ a[1]
     if op == "transpose":
         return a[0].T
@@ -251,6 +269,9 @@ def _eval_instr(ins: Instr, vals: list, args: list):
         return a[0].max() if ax is None else a[0].max(axis=ax, keepdims=True)
     if op == "broadcast":
         return np.broadcast_to(a[0], ins.shape).copy()
+    if op == "cast":
+        from .bf16 import round_to_bf16
+        return round_to_bf16(a[0].astype(np.float32))
     raise ValueError(f"unknown op {op}")
 
 

@@ -25,6 +25,24 @@ Functions written here:
 
 Activations are composites: sigmoid = 1 / (1 + exp(-v)); relu =
 select(v > 0, v, 0); tanh is a primitive.
+
+A bf16-storage network stores its inputs, parameters and hidden activations
+in bf16: x and the parameters are rounded on the way in, and each hidden
+activation goes through a dataTypeCast to bf16 (Table 1) before the next layer
+reads it. The logits stay float32 (their rounding to float32 is not modelled).
+``MlpSpec(storage_casts=False)`` gives the same network without the
+activation casts, i.e. the exact function of the rounded inputs.
+
+Order sensitivity. With storage casts the network is a discontinuous function
+of its pre-activations: a change far below float32 resolution can move a value
+across a bf16 rounding boundary, the resulting one-ulp change grows through
+later layers and can flip ReLU masks of pre-activations near zero, and a
+flipped mask switches a whole gradient path on or off. The gradient of a deep
+bf16 ReLU network is therefore only defined up to the accumulation order of
+its dot products. ``MlpSpec(accumulate="f32")`` evaluates the same network with
+float32 accumulation in the forward dots (what a bf16-storage, float32-
+accumulate evaluator does); the distance between the two oracle evaluations
+measures that intrinsic ambiguity.
 """
 from __future__ import annotations
 
@@ -48,7 +66,9 @@ class MlpSpec:
     widths: tuple
     acts: tuple          # one per layer; names from ACTS
     loss: str = "softmax_ce"
-    dtype: str = "f32"   # storage type of x and params: "f32" or "bf16"
+    dtype: str = "f32"   # storage type of x, params and hidden activations: "f32" or "bf16"
+    storage_casts: bool = True  # bf16: cast every stored hidden activation to bf16
+    accumulate: str = "f64"     # forward dots: "f64", or "f32" to measure order sensitivity
 
     @property
     def n_layers(self) -> int:
@@ -115,8 +135,10 @@ def build_mlp_loss(spec: MlpSpec, batch: int) -> Function:
     if spec.loss == "softmax_ce":
         y = f.arg((batch, 1), I64, name="y")
         h = x
-        for (W, b), act in zip(ws, spec.acts):
-            h = _act(f, act, f.add(f.dot(h, W), b))
+        for l, ((W, b), act) in enumerate(zip(ws, spec.acts)):
+            h = _act(f, act, f.add(f.dot(h, W, spec.accumulate), b))
+            if spec.dtype == "bf16" and spec.storage_casts and l < spec.n_layers - 1:
+                h = f.cast(h, "bf16")   # the hidden activation is stored as bf16
         loss = _softmax_xent_ir(f, h, y, batch, spec.widths[-1])
         f.ret(loss, h)
     else:
@@ -251,3 +273,85 @@ def sgd_bf16(master, grad, lr: float):
 def gemm(a, b) -> np.ndarray:
     """The ``dot`` instruction: a plain float64 matrix product."""
     return np.asarray(a, dtype=np.float64) @ np.asarray(b, dtype=np.float64)
+
+
+# ---------------------------------------------------------------------------
+# Single dense-layer steps (for checking each fused kernel on its own)
+# ---------------------------------------------------------------------------
+@lru_cache(maxsize=64)
+def _dense_fn(M: int, N: int, K: int, act: str, alpha: float) -> Function:
+    """dense(x, W, b) = act(alpha * x.W + b)."""
+    f = Function("dense")
+    x = f.arg((M, K), name="x")
+    W = f.arg((K, N), name="W")
+    b = f.arg((1, N), name="b")
+    f.ret(_act(f, act, f.add(f.mul(f.dot(x, W), f.const(alpha)), b)))
+    return f
+
+
+def dense_forward(x, W, b, act: str = "none", alpha: float = 1.0) -> np.ndarray:
+    """act(alpha * x.W + b) in float64 (b may be None for no bias)."""
+    x = np.asarray(x, np.float64)
+    W = np.asarray(W, np.float64)
+    M, K = x.shape
+    N = W.shape[1]
+    b = np.zeros((1, N)) if b is None else np.asarray(b, np.float64).reshape(1, N)
+    out, = evaluate(_dense_fn(M, N, K, act, float(alpha)), [x, W, b])
+    return out
+
+
+@lru_cache(maxsize=64)
+def _act_dot_vjp_fn(M: int, N: int, K: int, act: str) -> Function:
+    """[gradient @g wrt 0 seedable] for g(u, W) = dot(act(u), W).
+
+    g maps the previous layer's pre-activation u [M, K] through its activation
+    and the next layer's weights W [K, N]: g(u) = dot(act(u), W). Its
+    vector-Jacobian product with seed dY [M, N] is (dY.W^T) * act'(u).
+    """
+    f = Function("act_dot")
+    u = f.arg((M, K), name="u")
+    W = f.arg((K, N), name="W")
+    f.ret(f.dot(_act(f, act, u), W))
+    return differentiate(f, wrt=[0], seedable=True)
+
+
+def dense_vjp_input(u, W, dY, act_prev: str = "none") -> np.ndarray:
+    """Adjoint with respect to the previous pre-activation u: (dY.W^T) * act'(u)."""
+    u = np.asarray(u, np.float64)
+    W = np.asarray(W, np.float64)
+    M, K = u.shape
+    N = W.shape[1]
+    du, = evaluate(_act_dot_vjp_fn(M, N, K, act_prev), [u, W, np.asarray(dY, np.float64)])
+    return du
+
+
+@lru_cache(maxsize=64)
+def _linear_params_vjp_fn(M: int, N: int, K: int) -> Function:
+    """Fig. 3's declaration 'wrt 1, 2 seedable' of foo(x, W, b) = dot(x, W) + b."""
+    f = Function("foo")
+    x = f.arg((M, K), name="x")
+    W = f.arg((K, N), name="W")
+    b = f.arg((1, N), name="b")
+    f.ret(f.add(f.dot(x, W), b))
+    return differentiate(f, wrt=[1, 2], seedable=True)
+
+
+def dense_vjp_params(x, dY):
+    """(dW, db) = (x^T.dY, column sums of dY), via the seedable gradient of foo."""
+    x = np.asarray(x, np.float64)
+    dY = np.asarray(dY, np.float64)
+    M, K = x.shape
+    N = dY.shape[1]
+    dW, db = evaluate(_linear_params_vjp_fn(M, N, K),
+                      [x, np.zeros((K, N)), np.zeros((1, N)), dY])
+    return dW, db.reshape(-1)
+
+
+def apply_act(u, act: str) -> np.ndarray:
+    """act(u) in float64, through the same IR composites as the network."""
+    u = np.asarray(u, np.float64)
+    f = Function("act")
+    a = f.arg(u.shape)
+    f.ret(_act(f, act, a))
+    out, = evaluate(f, [u])
+    return out

@@ -1,0 +1,287 @@
+"""Python binding of ``libdlvm.so``, the gfx950 hot path of a DLVM-compiled network.
+
+Argument marshalling only: every step of the forward, the gradient and the
+update runs in the library's HIP kernels. PyTorch supplies device memory and
+streams; tensors are passed as raw device pointers. The library must have
+been built (``python -m paper_1711_03016_amd.build``); importing the binding
+on a machine without it raises at first use, there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libdlvm.so")
+HEADER_PATH = os.path.join(os.path.dirname(_HERE), "include", "dlvm.h")
+
+# Constants mirrored from include/dlvm.h.
+OK, ERR_INVALID_ARG, ERR_MISALIGNED, ERR_WORKSPACE = 0, -1, -2, -3
+ERR_UNSUPPORTED, ERR_HIP, ERR_LABEL_RANGE, ERR_NONFINITE = -4, -5, -6, -7
+F32, BF16 = 0, 1
+ACTS = {"none": 0, "sigmoid": 1, "tanh": 2, "relu": 3}
+DTYPES = {"f32": F32, "bf16": BF16}
+LOSSES = {"softmax_ce": 0, "chain8": 1}
+
+
+class DlvmError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"dlvm status {status}: {message}")
+        self.status = status
+
+
+class _Desc(ctypes.Structure):
+    _fields_ = [
+        ("n_layers", ctypes.c_int32),
+        ("widths", ctypes.POINTER(ctypes.c_int32)),
+        ("acts", ctypes.POINTER(ctypes.c_int32)),
+        ("dtype", ctypes.c_int32),
+        ("loss", ctypes.c_int32),
+        ("wrt_x", ctypes.c_int32),
+        ("batch_max", ctypes.c_int64),
+    ]
+
+
+class LaunchInfo(ctypes.Structure):
+    _fields_ = [
+        ("name", ctypes.c_char * 48),
+        ("M", ctypes.c_int64),
+        ("N", ctypes.c_int64),
+        ("K", ctypes.c_int64),
+        ("flops", ctypes.c_double),
+        ("bytes", ctypes.c_double),
+    ]
+
+
+_lib = None
+_P = ctypes.c_void_p
+_I32, _I64, _F = ctypes.c_int32, ctypes.c_int64, ctypes.c_float
+_SIGS = {
+    "dlvm_create": (_I32, [ctypes.POINTER(_Desc), ctypes.POINTER(_P)]),
+    "dlvm_destroy": (None, [_P]),
+    "dlvm_param_count": (_I64, [_P]),
+    "dlvm_param_layout": (_I32, [_P, ctypes.POINTER(_I64), ctypes.POINTER(_I64)]),
+    "dlvm_workspace_bytes": (ctypes.c_size_t, [_P, _I64]),
+    "dlvm_forward": (_I32, [_P, _P, _P, _I64, _P, _P, ctypes.c_size_t, _P]),
+    "dlvm_gradient": (_I32, [_P, _P, _P, _P, _I64, _P, _P, _P, _P, ctypes.c_size_t, _P]),
+    "dlvm_sgd_step": (_I32, [_P, _P, _P, _P, _F, _P]),
+    "dlvm_check": (_I32, [_P, _P, _P]),
+    "dlvm_last_error": (ctypes.c_char_p, []),
+    "dlvm_dense_forward": (_I32, [_I32, _I32, _I32, _I64, _I64, _I64, _F, _P, _P, _P, _P, _P]),
+    "dlvm_dense_backward_data": (_I32, [_I32, _I32, _I32, _I64, _I64, _I64, _P, _P, _P, _P, _P, _P]),
+    "dlvm_dense_backward_params": (_I32, [_I32, _I64, _I64, _I64, _P, _P, _P, _P, _P]),
+    "dlvm_softmax_xent_ws_bytes": (ctypes.c_size_t, [_I64]),
+    "dlvm_softmax_xent": (_I32, [_I32, _I64, _I64, _P, _P, _F, _P, _P, _P, ctypes.c_size_t, _P]),
+    "dlvm_chain8_ws_bytes": (ctypes.c_size_t, [_I64, _I64]),
+    "dlvm_chain8": (_I32, [_I64, _I64, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
+    "dlvm_sgd": (_I32, [_I32, _I64, _P, _P, _P, _F, _P]),
+    "dlvm_plan_size": (_I32, [_P, _I64]),
+    "dlvm_plan_entry": (_I32, [_P, _I64, _I32, ctypes.POINTER(LaunchInfo)]),
+    "dlvm_probe_arm": (_I32, [_P, _I32, _I32]),
+    "dlvm_probe_read": (_I32, [_P, _I32, ctypes.POINTER(_I64), ctypes.POINTER(ctypes.c_double)]),
+    "dlvm_probe_disarm": (_I32, [_P]),
+}
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded library (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -m paper_1711_03016_amd.build`")
+        h = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGS.items():
+            fn = getattr(h, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = h
+    return _lib
+
+
+def header_functions() -> list[str]:
+    """Names of every function the C header declares."""
+    text = open(HEADER_PATH).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(dlvm_[a-z0-9_]+)\s*\(", text)))
+
+
+def _check(status: int) -> None:
+    if status != OK:
+        msg = lib().dlvm_last_error()
+        raise DlvmError(status, msg.decode() if msg else "")
+
+
+def _ptr(t) -> int | None:
+    """Device address of a tensor (or an int address, or None)."""
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream(stream) -> int | None:
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+class Model:
+    """A handle on one shape-specialised network (see ``dlvm_create``)."""
+
+    def __init__(self, widths, acts, dtype: str = "f32", loss: str = "softmax_ce",
+                 wrt_x: bool = False, batch_max: int = 1):
+        self.widths = tuple(int(w) for w in widths)
+        self.acts = tuple(acts)
+        self.dtype = dtype
+        self.loss = loss
+        self.wrt_x = bool(wrt_x)
+        self.batch_max = int(batch_max)
+        L = len(self.widths) - 1
+        self._w = (ctypes.c_int32 * (L + 1))(*self.widths)
+        self._a = (ctypes.c_int32 * max(L, 1))(*[ACTS[a] for a in self.acts])
+        desc = _Desc(L, self._w, self._a, DTYPES[dtype], LOSSES[loss], int(self.wrt_x),
+                     self.batch_max)
+        h = _P()
+        _check(lib().dlvm_create(ctypes.byref(desc), ctypes.byref(h)))
+        self._h = h
+
+    def __del__(self):
+        h = getattr(self, "_h", None)
+        if h is not None and h.value and _lib is not None:
+            _lib.dlvm_destroy(h)
+            self._h = None
+
+    @property
+    def n_layers(self) -> int:
+        return len(self.widths) - 1
+
+    def param_count(self) -> int:
+        return int(lib().dlvm_param_count(self._h))
+
+    def param_layout(self) -> list[int]:
+        """Element offsets [W_1, b_1, ..., W_L, b_L] of the flat buffer."""
+        return self.param_layout_lds()[0]
+
+    def param_layout_lds(self) -> tuple[list[int], list[int]]:
+        """(offsets, row stride of each W) of the flat buffer."""
+        arr = (_I64 * (2 * self.n_layers))()
+        lds = (_I64 * self.n_layers)()
+        _check(lib().dlvm_param_layout(self._h, arr, lds))
+        return list(arr), list(lds)
+
+    def pack(self, params, device, torch_dtype):
+        """A flat parameter tensor (zero padding) holding [(W [K,N], b [N]), ...]."""
+        import torch
+        flat = torch.zeros(self.param_count(), dtype=torch_dtype, device=device)
+        for (Wv, bv), (W, b) in zip(self.unpack(flat), params):
+            Wv.copy_(torch.as_tensor(W).to(device=device, dtype=torch_dtype))
+            bv.copy_(torch.as_tensor(b).reshape(-1).to(device=device, dtype=torch_dtype))
+        return flat
+
+    def unpack(self, flat, padded: bool = False):
+        """Views [(W [K,N], b [N]), ...] into a flat parameter or gradient tensor.
+
+        With padded=True the weight views include the padding columns [K, ld].
+        """
+        offs, lds = self.param_layout_lds()
+        out = []
+        for l in range(self.n_layers):
+            K, N, ld = self.widths[l], self.widths[l + 1], lds[l]
+            Wp = flat[offs[2 * l]:offs[2 * l] + K * ld].view(K, ld)
+            out.append((Wp if padded else Wp[:, :N], flat[offs[2 * l + 1]:offs[2 * l + 1] + N]))
+        return out
+
+    def workspace_bytes(self, batch: int) -> int:
+        return int(lib().dlvm_workspace_bytes(self._h, int(batch)))
+
+    def forward(self, params, x, batch, out, ws, stream=None) -> None:
+        _check(lib().dlvm_forward(self._h, _ptr(params), _ptr(x), int(batch), _ptr(out),
+                                  _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
+
+    def gradient(self, params, x, labels, batch, loss, dparams, dx, ws, stream=None) -> None:
+        _check(lib().dlvm_gradient(self._h, _ptr(params), _ptr(x), _ptr(labels), int(batch),
+                                   _ptr(loss), _ptr(dparams), _ptr(dx), _ptr(ws),
+                                   ws.numel() * ws.element_size(), _stream(stream)))
+
+    def sgd_step(self, params, master, dparams, lr: float, stream=None) -> None:
+        _check(lib().dlvm_sgd_step(self._h, _ptr(params), _ptr(master), _ptr(dparams),
+                                   float(lr), _stream(stream)))
+
+    def plan(self, batch: int) -> list[dict]:
+        """The launches of one training step (gradient call, then SGD call)."""
+        n = int(lib().dlvm_plan_size(self._h, int(batch)))
+        out = []
+        for i in range(n):
+            info = LaunchInfo()
+            _check(lib().dlvm_plan_entry(self._h, int(batch), i, ctypes.byref(info)))
+            out.append({"index": i, "name": info.name.decode(), "M": info.M, "N": info.N,
+                        "K": info.K, "flops": info.flops, "bytes": info.bytes})
+        return out
+
+    def probe_arm(self, index: int, capacity: int) -> None:
+        _check(lib().dlvm_probe_arm(self._h, int(index), int(capacity)))
+
+    def probe_read(self, index: int) -> tuple[int, float]:
+        """(launches recorded at position `index`, their summed milliseconds)."""
+        n = _I64()
+        ms = ctypes.c_double()
+        _check(lib().dlvm_probe_read(self._h, int(index), ctypes.byref(n), ctypes.byref(ms)))
+        return int(n.value), float(ms.value)
+
+    def probe_disarm(self) -> None:
+        _check(lib().dlvm_probe_disarm(self._h))
+
+    def check(self, ws, stream=None) -> int:
+        """Status of the device flags (0, ERR_LABEL_RANGE or ERR_NONFINITE)."""
+        return int(lib().dlvm_check(self._h, _ptr(ws), _stream(stream)))
+
+
+# ---------------------------------------------------------------------------
+# step-level entry points
+# ---------------------------------------------------------------------------
+def dense_forward(dtype, out_dtype, act, M, N, K, alpha, X, W, bias, H, stream=None):
+    _check(lib().dlvm_dense_forward(DTYPES[dtype], DTYPES[out_dtype], ACTS[act], M, N, K,
+                                    float(alpha), _ptr(X), _ptr(W), _ptr(bias), _ptr(H),
+                                    _stream(stream)))
+
+
+def dense_backward_data(dtype, out_dtype, act_prev, M, N, K, dY, W, Hprev, R, dX, stream=None):
+    _check(lib().dlvm_dense_backward_data(DTYPES[dtype], DTYPES[out_dtype], ACTS[act_prev],
+                                          M, N, K, _ptr(dY), _ptr(W), _ptr(Hprev), _ptr(R),
+                                          _ptr(dX), _stream(stream)))
+
+
+def dense_backward_params(dtype, M, N, K, X, dY, dW, db, stream=None):
+    _check(lib().dlvm_dense_backward_params(DTYPES[dtype], M, N, K, _ptr(X), _ptr(dY),
+                                            _ptr(dW), _ptr(db), _stream(stream)))
+
+
+def softmax_xent_ws_bytes(rows: int) -> int:
+    return int(lib().dlvm_softmax_xent_ws_bytes(int(rows)))
+
+
+def softmax_xent(dtype, rows, classes, logits, labels, scale, dlogits, loss, ws, stream=None):
+    _check(lib().dlvm_softmax_xent(DTYPES[dtype], rows, classes, _ptr(logits), _ptr(labels),
+                                   float(scale), _ptr(dlogits), _ptr(loss), _ptr(ws),
+                                   ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def chain8_ws_bytes(rows: int, cols: int) -> int:
+    return int(lib().dlvm_chain8_ws_bytes(int(rows), int(cols)))
+
+
+def chain8(rows, cols, z, bias, x_skip, zbar, xbar, loss, ws, stream=None):
+    _check(lib().dlvm_chain8(rows, cols, _ptr(z), _ptr(bias), _ptr(x_skip), _ptr(zbar),
+                             _ptr(xbar), _ptr(loss), _ptr(ws), ws.numel() * ws.element_size(),
+                             _stream(stream)))
+
+
+def sgd(dtype, n, params, master, grads, lr, stream=None):
+    _check(lib().dlvm_sgd(DTYPES[dtype], int(n), _ptr(params), _ptr(master), _ptr(grads),
+                          float(lr), _stream(stream)))

@@ -1,0 +1,764 @@
+// C ABI of the hot path: argument validation, the flat parameter layout, the
+// workspace layout, and the launch plans of the forward and gradient functions.
+//
+// The gradient function follows DLVM's adjoint code generation (section
+// 3.1.3): it takes the original inputs, recomputes the forward keeping every
+// layer output, then walks the layers backwards emitting the adjoint of each
+// dot (two products, transposes never materialised) fused with the adjoint of
+// the element-wise operators around it. The input gradient of the first layer
+// is dead unless x is differentiated, and is not computed (aggressive dead
+// code elimination, section 3.1.4).
+#include <hip/hip_runtime.h>
+
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "../../include/dlvm.h"
+#include "common.hpp"
+#include "kernels.hpp"
+
+using dlvm::GemmDesc;
+using dlvm::Layout;
+
+// Events of the timing probe (see dlvm_probe_arm).
+struct ProbeState {
+  bool armed = false;
+  int32_t index = -1;
+  int32_t capacity = 0;
+  int32_t used = 0;
+  std::vector<hipEvent_t> start, stop;
+  std::vector<int32_t> pos;
+};
+
+struct dlvm_model {
+  int L = 0;
+  std::vector<int32_t> widths;
+  std::vector<int32_t> acts;
+  int32_t dtype = DLVM_F32;
+  int32_t loss = DLVM_LOSS_SOFTMAX_CE;
+  int32_t wrt_x = 0;
+  int64_t batch_max = 0;
+  std::vector<int64_t> offsets;  // element offsets: W_l, b_l interleaved
+  std::vector<int64_t> ldw;      // row stride of W_l (N_l, or N_L rounded up to 8)
+  int64_t param_count = 0;
+  dlvm::ZeroGaps gaps{};         // padding ranges of the flat buffer
+  int32_t n_grad_launches = 0;   // launches of one gradient call
+  mutable ProbeState probe;
+};
+
+namespace {
+
+thread_local std::string g_last_error;
+
+dlvm_status fail(dlvm_status code, const std::string& msg) {
+  g_last_error = msg;
+  return code;
+}
+
+dlvm_status hip_fail(hipError_t e, const char* where) {
+  return fail(DLVM_ERR_HIP, std::string(where) + ": " + hipGetErrorString(e));
+}
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+size_t elem_size(int dtype) { return dtype == DLVM_BF16 ? 2 : 4; }
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+bool valid_dtype(int32_t d) { return d == DLVM_F32 || d == DLVM_BF16; }
+bool valid_act(int32_t a) { return a >= DLVM_ACT_NONE && a <= DLVM_ACT_RELU; }
+
+// Workspace layout for a given batch. Offsets in bytes from the base.
+struct WsLayout {
+  size_t flags = 0;         // int32[4]: [0] label out of range, [1] non-finite loss
+  size_t partials = 0;      // float32 loss partials
+  size_t bad = 0;           // int32 bad-label counts, one per loss partial
+  std::vector<size_t> H;    // H[l], l = 1 .. L-1: saved layer outputs (storage dtype)
+  size_t logits = 0;        // float32 [B, widths[L]] (logits, or z for the chain)
+  size_t dz[2] = {0, 0};    // adjoint ping-pong buffers (storage dtype; float32 for the chain)
+  size_t total = 0;
+};
+
+WsLayout ws_layout(const dlvm_model* m, int64_t B) {
+  WsLayout w;
+  size_t off = 0;
+  w.flags = off;
+  off = align_up(off + 16);
+  const int64_t np = std::max<int64_t>(dlvm::softmax_xent_partials(B),
+                                       dlvm::chain8_partials(B, m->widths[m->L]));
+  w.partials = off;
+  off = align_up(off + static_cast<size_t>(np) * 4);
+  w.bad = off;
+  off = align_up(off + static_cast<size_t>(np) * 4);
+  const size_t es = elem_size(m->dtype);
+  w.H.assign(m->L + 1, 0);
+  for (int l = 1; l < m->L; ++l) {
+    w.H[l] = off;
+    off = align_up(off + static_cast<size_t>(B) * m->widths[l] * es);
+  }
+  w.logits = off;
+  off = align_up(off + static_cast<size_t>(B) * m->widths[m->L] * 4);
+  int64_t maxw = 0;
+  for (int l = 0; l <= m->L; ++l) maxw = std::max<int64_t>(maxw, m->widths[l]);
+  for (int l = 0; l < m->L; ++l) maxw = std::max<int64_t>(maxw, m->ldw[l]);
+  const size_t dz_es = m->loss == DLVM_LOSS_CHAIN8 ? 4 : es;
+  for (int i = 0; i < 2; ++i) {
+    w.dz[i] = off;
+    off = align_up(off + static_cast<size_t>(B) * maxw * dz_es);
+  }
+  w.total = off;
+  return w;
+}
+
+// Address arithmetic on integers: a dry run (plan description) uses null bases.
+template <typename T> T* at(const void* base, size_t off) {
+  return reinterpret_cast<T*>(reinterpret_cast<uintptr_t>(base) + off);
+}
+
+const void* param_ptr(const dlvm_model* m, const void* params, int64_t elem_off) {
+  return at<const void>(params, static_cast<size_t>(elem_off) * elem_size(m->dtype));
+}
+
+dlvm_status check_batch(const dlvm_model* m, int64_t batch) {
+  if (batch < 1 || batch > m->batch_max)
+    return fail(DLVM_ERR_INVALID_ARG, "batch must be in [1, batch_max]");
+  return DLVM_OK;
+}
+
+dlvm_status check_ws(const dlvm_model* m, int64_t batch, const void* ws, size_t ws_bytes) {
+  if (ws == nullptr) return fail(DLVM_ERR_WORKSPACE, "workspace is null");
+  if (!aligned16(ws)) return fail(DLVM_ERR_MISALIGNED, "workspace is not 16-byte aligned");
+  if (ws_bytes < ws_layout(m, batch).total)
+    return fail(DLVM_ERR_WORKSPACE, "workspace is smaller than dlvm_workspace_bytes");
+  return DLVM_OK;
+}
+
+dlvm_status run_gemm(const GemmDesc& d, hipStream_t s) {
+  const hipError_t e = dlvm::launch_gemm(d, dlvm::plan_gemm(d), s);
+  if (e != hipSuccess) return hip_fail(e, "gemm launch");
+  return DLVM_OK;
+}
+
+// H[M,N] (row stride ldh) = act(alpha * X[M,K] . W[K,N] (row stride ldw) + bias[N])
+GemmDesc gemm_nn(int dtype, int out_dtype, int act, int64_t M, int64_t N, int64_t K, float alpha,
+                 const void* X, const void* W, int64_t ldw, const void* bias, void* H,
+                 int64_t ldh) {
+  GemmDesc d{};
+  d.layout = Layout::NN; d.dtype = dtype; d.out_dtype = out_dtype; d.act = act;
+  d.M = M; d.N = N; d.K = K;
+  d.A = X; d.lda = K; d.B = W; d.ldb = ldw; d.C = H; d.ldc = ldh;
+  d.bias = bias; d.alpha = alpha; d.nvec = N;
+  return d;
+}
+
+// dX[M,K] = (dY[M,N] (stride ldy) . W[K,N]^T (stride ldw)) * act'(Hprev) + R
+GemmDesc gemm_nt(int dtype, int out_dtype, int act_prev, int64_t M, int64_t N, int64_t K,
+                 const void* dY, int64_t ldy, const void* W, int64_t ldw, const void* Hprev,
+                 const void* R, void* dX) {
+  GemmDesc d{};
+  d.layout = Layout::NT; d.dtype = dtype; d.out_dtype = out_dtype; d.act = act_prev;
+  d.M = M; d.N = K; d.K = N;
+  d.A = dY; d.lda = ldy; d.B = W; d.ldb = ldw; d.C = dX; d.ldc = K;
+  d.aux = Hprev; d.residual = R; d.alpha = 1.0f; d.nvec = K;
+  return d;
+}
+
+// dW[K,N] (stride ldw) = X[M,K]^T . dY[M,N] (stride ldy); db = column sums of
+// the first nvec columns of dY
+GemmDesc gemm_tn(int dtype, int64_t M, int64_t N, int64_t K, const void* X, const void* dY,
+                 int64_t ldy, float* dW, int64_t ldw, float* db, int64_t nvec) {
+  GemmDesc d{};
+  d.layout = Layout::TN; d.dtype = dtype; d.out_dtype = DLVM_F32; d.act = DLVM_ACT_NONE;
+  d.M = K; d.N = N; d.K = M;
+  d.A = X; d.lda = K; d.B = dY; d.ldb = ldy; d.C = dW; d.ldc = ldw;
+  d.colsum = db; d.alpha = 1.0f; d.nvec = nvec;
+  return d;
+}
+
+// Description of one launch (name, sizes, algorithmic work).
+struct LaunchInfo {
+  std::string name;
+  int64_t M = 0, N = 0, K = 0;
+  double flops = 0.0, bytes = 0.0;
+};
+
+LaunchInfo gemm_info(const GemmDesc& d) {
+  static const char* lay[] = {"nn", "nt", "tn"};
+  LaunchInfo i;
+  i.name = std::string("gemm_") + lay[static_cast<int>(d.layout)] + (d.dtype == DLVM_F32 ? "_f32" : "_bf16");
+  i.M = d.M; i.N = d.N; i.K = d.K;
+  i.flops = 2.0 * double(d.M) * double(d.N) * double(d.K);
+  const double es = double(elem_size(d.dtype)), eo = double(elem_size(d.out_dtype));
+  double b = (double(d.M) * d.K + double(d.K) * d.N) * es + double(d.M) * d.N * eo;
+  if (d.bias) b += double(d.N) * es;
+  if (d.layout == Layout::NT && d.act != DLVM_ACT_NONE) b += double(d.M) * d.N * es;
+  if (d.residual) b += double(d.M) * d.N * eo;
+  if (d.colsum) b += double(d.N) * 4.0;
+  i.bytes = b;
+  return i;
+}
+
+LaunchInfo elementwise_info(const char* name, int64_t rows, int64_t cols, double bytes) {
+  LaunchInfo i;
+  i.name = name;
+  i.M = rows; i.N = cols; i.K = 0;
+  i.bytes = bytes;
+  return i;
+}
+
+// Every launch of the model-level calls goes through one Launcher. With a
+// plan vector it only records what it would launch (no pointer is touched);
+// otherwise it enqueues the launch, bracketed by the probe's events when the
+// probe is armed for this position.
+class Launcher {
+ public:
+  Launcher(const dlvm_model* m, hipStream_t s, std::vector<LaunchInfo>* plan, int32_t first)
+      : m_(m), s_(s), plan_(plan), index_(first) {}
+
+  template <class F>
+  dlvm_status run(LaunchInfo info, F&& launch, const char* what) {
+    const int32_t idx = index_++;
+    if (plan_ != nullptr) {
+      plan_->push_back(std::move(info));
+      return DLVM_OK;
+    }
+    ProbeState& p = m_->probe;
+    const bool rec = p.armed && (p.index < 0 || p.index == idx) && p.used < p.capacity;
+    if (rec) (void)hipEventRecord(p.start[p.used], s_);
+    const hipError_t e = launch();
+    if (rec) {
+      (void)hipEventRecord(p.stop[p.used], s_);
+      p.pos[p.used] = idx;
+      ++p.used;
+    }
+    if (e != hipSuccess) return hip_fail(e, what);
+    return DLVM_OK;
+  }
+
+  dlvm_status gemm(const GemmDesc& d) {
+    const dlvm::GemmPlan pl = dlvm::plan_gemm(d);
+    LaunchInfo info = gemm_info(d);
+    info.name += "_" + std::to_string(pl.bm) + "x" + std::to_string(pl.bn) + "c" + std::to_string(pl.cfg);
+    return run(std::move(info), [&] { return dlvm::launch_gemm(d, pl, s_); }, "gemm launch");
+  }
+
+  hipStream_t stream() const { return s_; }
+  bool dry() const { return plan_ != nullptr; }
+
+ private:
+  const dlvm_model* m_;
+  hipStream_t s_;
+  std::vector<LaunchInfo>* plan_;
+  int32_t index_;
+};
+
+// The launches of one gradient call (section 3.1.3): forward keeping every
+// layer output, the loss adjoint, then the adjoint of each layer, last first.
+dlvm_status plan_gradient(const dlvm_model* m, const void* params, const void* x,
+                          const int32_t* labels, int64_t batch, float* loss, float* dparams,
+                          float* dx, void* ws, Launcher& run) {
+  const WsLayout w = ws_layout(m, batch);
+  const int L = m->L;
+  const int dt = m->dtype;
+  const double es = double(elem_size(dt));
+  float* partials = at<float>(ws, w.partials);
+  int32_t* bad = at<int32_t>(ws, w.bad);
+  int32_t* flags = at<int32_t>(ws, w.flags);
+  auto P = [&](int idx) { return param_ptr(m, params, m->offsets[idx]); };
+  auto G = [&](int idx) { return at<float>(dparams, static_cast<size_t>(m->offsets[idx]) * 4); };
+  hipStream_t s = run.stream();
+  dlvm_status st = DLVM_OK;
+  int np = 0;
+  float scale = 1.0f;
+
+  if (m->loss == DLVM_LOSS_CHAIN8) {
+    const int64_t N = m->widths[1], K = m->widths[0];
+    float* z = at<float>(ws, w.logits);
+    float* zbar = at<float>(ws, w.dz[0]);
+    if ((st = run.gemm(gemm_nn(dt, DLVM_F32, DLVM_ACT_NONE, batch, N, K, 1.0f, x, P(0), N, nullptr,
+                               z, N))) != DLVM_OK)
+      return st;
+    np = dlvm::chain8_partials(batch, N);
+    st = run.run(elementwise_info("chain8", batch, N, 16.0 * double(batch) * N + 4.0 * N),
+                 [&] {
+                   int n = 0;
+                   return dlvm::launch_chain8(batch, N, z, static_cast<const float*>(P(1)),
+                                              static_cast<const float*>(x), zbar, dx, partials,
+                                              false, &n, s);
+                 },
+                 "chain launch");
+    if (st != DLVM_OK) return st;
+    if ((st = run.gemm(gemm_tn(dt, batch, N, K, x, zbar, N, G(0), N, G(1), N))) != DLVM_OK) return st;
+    // dx = zbar . W^T + xbar (xbar already in dx: in-place accumulate)
+    if ((st = run.gemm(gemm_nt(dt, DLVM_F32, DLVM_ACT_NONE, batch, N, K, zbar, N, P(0), N, nullptr,
+                               dx, dx))) != DLVM_OK)
+      return st;
+    scale = static_cast<float>(1.0 / (static_cast<double>(batch) * static_cast<double>(N)));
+  } else {
+    // Forward, keeping every layer output.
+    const void* h = x;
+    for (int l = 0; l < L; ++l) {
+      const bool last = l == L - 1;
+      const int64_t N = m->widths[l + 1];
+      void* dst = last ? at<void>(ws, w.logits) : at<void>(ws, w.H[l + 1]);
+      if ((st = run.gemm(gemm_nn(dt, last ? DLVM_F32 : dt, m->acts[l], batch, N, m->widths[l], 1.0f,
+                                 h, P(2 * l), m->ldw[l], P(2 * l + 1), dst, N))) != DLVM_OK)
+        return st;
+      h = dst;
+    }
+    const int64_t C = m->widths[L];
+    const int64_t ldc = m->ldw[L - 1];  // dZ_L rows are padded like W_L's
+    scale = static_cast<float>(1.0 / static_cast<double>(batch));
+    void* dz = at<void>(ws, w.dz[0]);
+    np = dlvm::softmax_xent_partials(batch);
+    st = run.run(elementwise_info("softmax_xent", batch, C,
+                                  double(batch) * C * (4.0 + es) + 4.0 * batch),
+                 [&] {
+                   int n = 0;
+                   return dlvm::launch_softmax_xent(dt, batch, C, at<float>(ws, w.logits), labels,
+                                                    scale, dz, ldc, partials, bad, &n, s);
+                 },
+                 "softmax cross-entropy launch");
+    if (st != DLVM_OK) return st;
+    // Adjoint sweep, last layer first.
+    int cur = 0;
+    // On the padded class columns dZ_L and W_L are zero, so the products run
+    // over the padded width and the padding columns of dW_L come out zero.
+    for (int l = L - 1; l >= 0; --l) {
+      const void* hin = l == 0 ? x : at<void>(ws, w.H[l]);
+      const int64_t K = m->widths[l], N = m->widths[l + 1];
+      const int64_t Np = m->ldw[l];  // padded width (== N except the last layer)
+      void* dzl = at<void>(ws, w.dz[cur]);
+      if ((st = run.gemm(gemm_tn(dt, batch, Np, K, hin, dzl, Np, G(2 * l), Np, G(2 * l + 1), N))) !=
+          DLVM_OK)
+        return st;
+      if (l > 0) {
+        void* dzp = at<void>(ws, w.dz[cur ^ 1]);
+        if ((st = run.gemm(gemm_nt(dt, dt, m->acts[l - 1], batch, Np, K, dzl, Np, P(2 * l), Np,
+                                   at<void>(ws, w.H[l]), nullptr, dzp))) != DLVM_OK)
+          return st;
+        cur ^= 1;
+      } else if (m->wrt_x) {
+        if ((st = run.gemm(gemm_nt(dt, DLVM_F32, DLVM_ACT_NONE, batch, Np, K, dzl, Np, P(0), Np,
+                                   nullptr, nullptr, dx))) != DLVM_OK)
+          return st;
+      }
+    }
+  }
+  const int32_t* badp = m->loss == DLVM_LOSS_CHAIN8 ? nullptr : bad;
+  return run.run(elementwise_info("finalize", np, 1, 8.0 * np + 4.0),
+                 [&] {
+                   return dlvm::launch_finalize(partials, badp, np, scale, loss, flags, dparams,
+                                                m->gaps, s);
+                 },
+                 "loss finalisation launch");
+}
+
+// The launches of one forward call: nothing is kept, two ping-pong buffers
+// hold the layer outputs.
+dlvm_status plan_forward(const dlvm_model* m, const void* params, const void* x, int64_t batch,
+                         float* out, void* ws, Launcher& run) {
+  const WsLayout w = ws_layout(m, batch);
+  dlvm_status st = DLVM_OK;
+  const int L = m->L;
+  const int dt = m->dtype;
+  hipStream_t s = run.stream();
+  if (m->loss == DLVM_LOSS_CHAIN8) {
+    const int64_t N = m->widths[1];
+    float* z = at<float>(ws, w.logits);
+    if ((st = run.gemm(gemm_nn(dt, DLVM_F32, DLVM_ACT_NONE, batch, N, m->widths[0], 1.0f, x,
+                               param_ptr(m, params, m->offsets[0]), N, nullptr, z, N))) != DLVM_OK)
+      return st;
+    const float* bias = static_cast<const float*>(param_ptr(m, params, m->offsets[1]));
+    return run.run(elementwise_info("chain8_forward", batch, N, 12.0 * double(batch) * N + 4.0 * N),
+                   [&] {
+                     int n = 0;
+                     return dlvm::launch_chain8(batch, N, z, bias, static_cast<const float*>(x),
+                                                out, nullptr, at<float>(ws, w.partials), true, &n, s);
+                   },
+                   "chain launch");
+  }
+  const void* h = x;
+  for (int l = 0; l < L; ++l) {
+    const bool last = l == L - 1;
+    void* dst = last ? static_cast<void*>(out) : at<void>(ws, w.dz[l & 1]);
+    if ((st = run.gemm(gemm_nn(dt, last ? DLVM_F32 : dt, m->acts[l], batch, m->widths[l + 1],
+                               m->widths[l], 1.0f, h, param_ptr(m, params, m->offsets[2 * l]),
+                               m->ldw[l], param_ptr(m, params, m->offsets[2 * l + 1]), dst,
+                               m->widths[l + 1]))) != DLVM_OK)
+      return st;
+    h = dst;
+  }
+  return DLVM_OK;
+}
+
+LaunchInfo sgd_info(const dlvm_model* m) {
+  const double per = m->dtype == DLVM_BF16 ? 14.0 : 12.0;  // master/params, grads, (shadow)
+  return elementwise_info(m->dtype == DLVM_BF16 ? "sgd_bf16" : "sgd_f32", m->param_count, 1,
+                          per * double(m->param_count));
+}
+
+void probe_release(ProbeState& p) {
+  for (hipEvent_t e : p.start)
+    if (e) (void)hipEventDestroy(e);
+  for (hipEvent_t e : p.stop)
+    if (e) (void)hipEventDestroy(e);
+  p = ProbeState();
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* dlvm_last_error(void) { return g_last_error.c_str(); }
+
+dlvm_status dlvm_create(const dlvm_mlp_desc* desc, dlvm_model** out) {
+  if (out == nullptr || desc == nullptr) return fail(DLVM_ERR_INVALID_ARG, "null argument");
+  *out = nullptr;
+  const int L = desc->n_layers;
+  if (L < 1 || L > 30) return fail(DLVM_ERR_INVALID_ARG, "n_layers must be in [1, 30]");
+  if (desc->widths == nullptr || desc->acts == nullptr)
+    return fail(DLVM_ERR_INVALID_ARG, "widths and acts must be given");
+  if (!valid_dtype(desc->dtype)) return fail(DLVM_ERR_INVALID_ARG, "unknown dtype");
+  if (desc->loss != DLVM_LOSS_SOFTMAX_CE && desc->loss != DLVM_LOSS_CHAIN8)
+    return fail(DLVM_ERR_INVALID_ARG, "unknown loss");
+  if (desc->batch_max < 1 || desc->batch_max > (int64_t(1) << 24))
+    return fail(DLVM_ERR_INVALID_ARG, "batch_max must be in [1, 2^24]");
+  for (int l = 0; l <= L; ++l)
+    if (desc->widths[l] < 1 || desc->widths[l] > (1 << 20))
+      return fail(DLVM_ERR_INVALID_ARG, "every width must be in [1, 2^20]");
+  for (int l = 0; l < L; ++l)
+    if (!valid_act(desc->acts[l])) return fail(DLVM_ERR_INVALID_ARG, "unknown activation");
+  if (desc->acts[L - 1] != DLVM_ACT_NONE)
+    return fail(DLVM_ERR_INVALID_ARG, "the last layer must have no activation");
+  if (desc->loss == DLVM_LOSS_CHAIN8) {
+    if (L != 1 || desc->widths[0] != desc->widths[1])
+      return fail(DLVM_ERR_UNSUPPORTED, "the chain loss needs one layer with in == out");
+    if (desc->dtype != DLVM_F32) return fail(DLVM_ERR_UNSUPPORTED, "the chain loss is float32");
+    if (!desc->wrt_x) return fail(DLVM_ERR_UNSUPPORTED, "the chain loss differentiates x too");
+  }
+  for (int l = 0; l < L; ++l) {
+    const int64_t es = static_cast<int64_t>(elem_size(desc->dtype));
+    const int64_t bytes = static_cast<int64_t>(desc->widths[l]) * desc->widths[l + 1] * es;
+    if (bytes > (int64_t(1) << 34)) return fail(DLVM_ERR_INVALID_ARG, "a weight matrix is too large");
+  }
+  dlvm_model* m = new (std::nothrow) dlvm_model();
+  if (m == nullptr) return fail(DLVM_ERR_INVALID_ARG, "out of host memory");
+  m->L = L;
+  m->widths.assign(desc->widths, desc->widths + L + 1);
+  m->acts.assign(desc->acts, desc->acts + L);
+  m->dtype = desc->dtype;
+  m->loss = desc->loss;
+  m->wrt_x = desc->wrt_x ? 1 : 0;
+  m->batch_max = desc->batch_max;
+  // Flat layout: every tensor starts on a 256-byte boundary in every view
+  // (storage dtype and float32 share element offsets: 128 elements is 256
+  // bytes of bf16 and 512 bytes of float32).
+  const int64_t step = 128;
+  int64_t off = 0;
+  m->gaps.n = 0;
+  // The class dimension of a softmax network's last weight matrix is padded
+  // to a multiple of 8 (zero columns), so every row is 16-byte aligned.
+  for (int l = 0; l < L; ++l) {
+    const int64_t n = m->widths[l + 1];
+    m->ldw.push_back(m->loss == DLVM_LOSS_SOFTMAX_CE && l == L - 1 ? (n + 7) / 8 * 8 : n);
+  }
+  for (int l = 0; l < L; ++l) {
+    for (int t = 0; t < 2; ++t) {
+      const int64_t n = t == 0 ? int64_t(m->widths[l]) * m->ldw[l] : m->widths[l + 1];
+      m->offsets.push_back(off);
+      const int64_t end = off + n;
+      const int64_t next = (end + step - 1) / step * step;
+      if (next > end) {
+        m->gaps.off[m->gaps.n] = end;
+        m->gaps.len[m->gaps.n] = static_cast<int32_t>(next - end);
+        ++m->gaps.n;
+      }
+      off = next;
+    }
+  }
+  m->param_count = off;
+  std::vector<LaunchInfo> plan;
+  Launcher dry(m, nullptr, &plan, 0);
+  plan_gradient(m, nullptr, nullptr, nullptr, 1, nullptr, nullptr, nullptr, nullptr, dry);
+  m->n_grad_launches = static_cast<int32_t>(plan.size());
+  *out = m;
+  return DLVM_OK;
+}
+
+void dlvm_destroy(dlvm_model* m) {
+  if (m == nullptr) return;
+  probe_release(m->probe);
+  delete m;
+}
+
+int64_t dlvm_param_count(const dlvm_model* m) { return m ? m->param_count : 0; }
+
+dlvm_status dlvm_param_layout(const dlvm_model* m, int64_t* offsets, int64_t* lds) {
+  if (m == nullptr || offsets == nullptr) return fail(DLVM_ERR_INVALID_ARG, "null argument");
+  std::memcpy(offsets, m->offsets.data(), m->offsets.size() * sizeof(int64_t));
+  if (lds != nullptr) std::memcpy(lds, m->ldw.data(), m->ldw.size() * sizeof(int64_t));
+  return DLVM_OK;
+}
+
+size_t dlvm_workspace_bytes(const dlvm_model* m, int64_t batch) {
+  if (m == nullptr || batch < 1 || batch > m->batch_max) return 0;
+  return ws_layout(m, batch).total;
+}
+
+dlvm_status dlvm_forward(const dlvm_model* m, const void* params, const void* x, int64_t batch,
+                         float* out, void* ws, size_t ws_bytes, void* stream) {
+  if (m == nullptr || params == nullptr || x == nullptr || out == nullptr)
+    return fail(DLVM_ERR_INVALID_ARG, "null argument");
+  if (!aligned16(params) || !aligned16(x) || !aligned16(out))
+    return fail(DLVM_ERR_MISALIGNED, "device pointers must be 16-byte aligned");
+  dlvm_status st = check_batch(m, batch);
+  if (st != DLVM_OK) return st;
+  if ((st = check_ws(m, batch, ws, ws_bytes)) != DLVM_OK) return st;
+  Launcher run(m, static_cast<hipStream_t>(stream), nullptr, 0);
+  return plan_forward(m, params, x, batch, out, ws, run);
+}
+
+dlvm_status dlvm_gradient(const dlvm_model* m, const void* params, const void* x,
+                          const int32_t* labels, int64_t batch, float* loss, float* dparams,
+                          float* dx, void* ws, size_t ws_bytes, void* stream) {
+  if (m == nullptr || params == nullptr || x == nullptr || loss == nullptr || dparams == nullptr)
+    return fail(DLVM_ERR_INVALID_ARG, "null argument");
+  if (m->loss == DLVM_LOSS_SOFTMAX_CE && labels == nullptr)
+    return fail(DLVM_ERR_INVALID_ARG, "labels are required for the softmax cross-entropy loss");
+  if (m->wrt_x && dx == nullptr) return fail(DLVM_ERR_INVALID_ARG, "dx is required when wrt_x");
+  if (!aligned16(params) || !aligned16(x) || !aligned16(dparams) ||
+      (labels && !aligned16(labels)) || (dx && !aligned16(dx)))
+    return fail(DLVM_ERR_MISALIGNED, "device pointers must be 16-byte aligned");
+  dlvm_status st = check_batch(m, batch);
+  if (st != DLVM_OK) return st;
+  if ((st = check_ws(m, batch, ws, ws_bytes)) != DLVM_OK) return st;
+  Launcher run(m, static_cast<hipStream_t>(stream), nullptr, 0);
+  return plan_gradient(m, params, x, labels, batch, loss, dparams, dx, ws, run);
+}
+
+dlvm_status dlvm_sgd_step(const dlvm_model* m, void* params, float* master, const float* dparams,
+                          float lr, void* stream) {
+  if (m == nullptr || params == nullptr || dparams == nullptr)
+    return fail(DLVM_ERR_INVALID_ARG, "null argument");
+  if (m->dtype == DLVM_BF16 && master == nullptr)
+    return fail(DLVM_ERR_INVALID_ARG, "bf16 models need float32 master weights");
+  if (!aligned16(params) || !aligned16(dparams) || (master && !aligned16(master)))
+    return fail(DLVM_ERR_MISALIGNED, "device pointers must be 16-byte aligned");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  Launcher run(m, s, nullptr, m->n_grad_launches);
+  float* mst = m->dtype == DLVM_BF16 ? master : nullptr;
+  return run.run(sgd_info(m),
+                 [&] { return dlvm::launch_sgd(m->dtype, m->param_count, params, mst, dparams, lr, s); },
+                 "sgd launch");
+}
+
+int32_t dlvm_plan_size(const dlvm_model* m, int64_t batch) {
+  if (m == nullptr || batch < 1 || batch > m->batch_max) return 0;
+  return m->n_grad_launches + 1;
+}
+
+dlvm_status dlvm_plan_entry(const dlvm_model* m, int64_t batch, int32_t index,
+                            dlvm_launch_info* info) {
+  if (m == nullptr || info == nullptr) return fail(DLVM_ERR_INVALID_ARG, "null argument");
+  dlvm_status st = check_batch(m, batch);
+  if (st != DLVM_OK) return st;
+  std::vector<LaunchInfo> plan;
+  Launcher dry(m, nullptr, &plan, 0);
+  plan_gradient(m, nullptr, nullptr, nullptr, batch, nullptr, nullptr, nullptr, nullptr, dry);
+  plan.push_back(sgd_info(m));
+  if (index < 0 || index >= static_cast<int32_t>(plan.size()))
+    return fail(DLVM_ERR_INVALID_ARG, "launch index out of range");
+  const LaunchInfo& li = plan[index];
+  std::memset(info, 0, sizeof(*info));
+  std::strncpy(info->name, li.name.c_str(), sizeof(info->name) - 1);
+  info->M = li.M; info->N = li.N; info->K = li.K;
+  info->flops = li.flops;
+  info->bytes = li.bytes;
+  return DLVM_OK;
+}
+
+dlvm_status dlvm_probe_arm(dlvm_model* m, int32_t index, int32_t capacity) {
+  if (m == nullptr || capacity < 1 || capacity > (1 << 20) || index < -1)
+    return fail(DLVM_ERR_INVALID_ARG, "bad probe arguments");
+  probe_release(m->probe);
+  ProbeState& p = m->probe;
+  p.start.assign(capacity, nullptr);
+  p.stop.assign(capacity, nullptr);
+  p.pos.assign(capacity, -1);
+  for (int32_t i = 0; i < capacity; ++i) {
+    hipError_t e = hipEventCreate(&p.start[i]);
+    if (e == hipSuccess) e = hipEventCreate(&p.stop[i]);
+    if (e != hipSuccess) {
+      probe_release(p);
+      return hip_fail(e, "creating probe events");
+    }
+  }
+  p.index = index;
+  p.capacity = capacity;
+  p.used = 0;
+  p.armed = true;
+  return DLVM_OK;
+}
+
+dlvm_status dlvm_probe_read(dlvm_model* m, int32_t index, int64_t* count, double* total_ms) {
+  if (m == nullptr || count == nullptr || total_ms == nullptr)
+    return fail(DLVM_ERR_INVALID_ARG, "null argument");
+  ProbeState& p = m->probe;
+  *count = 0;
+  *total_ms = 0.0;
+  for (int32_t i = 0; i < p.used; ++i) {
+    if (index >= 0 && p.pos[i] != index) continue;
+    hipError_t e = hipEventSynchronize(p.stop[i]);
+    float ms = 0.0f;
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, p.start[i], p.stop[i]);
+    if (e != hipSuccess) return hip_fail(e, "reading probe events");
+    *count += 1;
+    *total_ms += ms;
+  }
+  return DLVM_OK;
+}
+
+dlvm_status dlvm_probe_disarm(dlvm_model* m) {
+  if (m == nullptr) return fail(DLVM_ERR_INVALID_ARG, "null argument");
+  probe_release(m->probe);
+  return DLVM_OK;
+}
+
+dlvm_status dlvm_check(const dlvm_model* m, void* ws, void* stream) {
+  if (m == nullptr || ws == nullptr) return fail(DLVM_ERR_INVALID_ARG, "null argument");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int32_t flags[4] = {0, 0, 0, 0};
+  hipError_t e = hipMemcpyAsync(flags, ws, 2 * sizeof(int32_t), hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return hip_fail(e, "reading the workspace flags");
+  if (flags[0]) return fail(DLVM_ERR_LABEL_RANGE, "a label was outside [0, classes)");
+  if (flags[1]) return fail(DLVM_ERR_NONFINITE, "the loss was not finite");
+  return DLVM_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Step-level entry points
+// ---------------------------------------------------------------------------
+dlvm_status dlvm_dense_forward(int32_t dtype, int32_t out_dtype, int32_t act, int64_t M, int64_t N,
+                               int64_t K, float alpha, const void* X, const void* W,
+                               const void* bias, void* H, void* stream) {
+  if (!valid_dtype(dtype) || !valid_dtype(out_dtype) || !valid_act(act))
+    return fail(DLVM_ERR_INVALID_ARG, "bad dtype or activation");
+  if (dtype == DLVM_F32 && out_dtype != DLVM_F32)
+    return fail(DLVM_ERR_UNSUPPORTED, "float32 operands give float32 outputs");
+  if (M < 1 || N < 1 || K < 1) return fail(DLVM_ERR_INVALID_ARG, "sizes must be positive");
+  if (X == nullptr || W == nullptr || H == nullptr) return fail(DLVM_ERR_INVALID_ARG, "null argument");
+  if (!aligned16(X) || !aligned16(W) || !aligned16(H) || (bias && !aligned16(bias)))
+    return fail(DLVM_ERR_MISALIGNED, "device pointers must be 16-byte aligned");
+  return run_gemm(gemm_nn(dtype, out_dtype, act, M, N, K, alpha, X, W, N, bias, H, N),
+                  static_cast<hipStream_t>(stream));
+}
+
+dlvm_status dlvm_dense_backward_data(int32_t dtype, int32_t out_dtype, int32_t act_prev, int64_t M,
+                                     int64_t N, int64_t K, const void* dY, const void* W,
+                                     const void* Hprev, const void* R, void* dX, void* stream) {
+  if (!valid_dtype(dtype) || !valid_dtype(out_dtype) || !valid_act(act_prev))
+    return fail(DLVM_ERR_INVALID_ARG, "bad dtype or activation");
+  if (dtype == DLVM_F32 && out_dtype != DLVM_F32)
+    return fail(DLVM_ERR_UNSUPPORTED, "float32 operands give float32 outputs");
+  if (M < 1 || N < 1 || K < 1) return fail(DLVM_ERR_INVALID_ARG, "sizes must be positive");
+  if (dY == nullptr || W == nullptr || dX == nullptr) return fail(DLVM_ERR_INVALID_ARG, "null argument");
+  if (act_prev != DLVM_ACT_NONE && Hprev == nullptr)
+    return fail(DLVM_ERR_INVALID_ARG, "Hprev is required for an activation derivative");
+  if (!aligned16(dY) || !aligned16(W) || !aligned16(dX) || (Hprev && !aligned16(Hprev)) ||
+      (R && !aligned16(R)))
+    return fail(DLVM_ERR_MISALIGNED, "device pointers must be 16-byte aligned");
+  return run_gemm(gemm_nt(dtype, out_dtype, act_prev, M, N, K, dY, N, W, N, Hprev, R, dX),
+                  static_cast<hipStream_t>(stream));
+}
+
+dlvm_status dlvm_dense_backward_params(int32_t dtype, int64_t M, int64_t N, int64_t K,
+                                       const void* X, const void* dY, float* dW, float* db,
+                                       void* stream) {
+  if (!valid_dtype(dtype)) return fail(DLVM_ERR_INVALID_ARG, "bad dtype");
+  if (M < 1 || N < 1 || K < 1) return fail(DLVM_ERR_INVALID_ARG, "sizes must be positive");
+  if (X == nullptr || dY == nullptr || dW == nullptr) return fail(DLVM_ERR_INVALID_ARG, "null argument");
+  if (!aligned16(X) || !aligned16(dY) || !aligned16(dW) || (db && !aligned16(db)))
+    return fail(DLVM_ERR_MISALIGNED, "device pointers must be 16-byte aligned");
+  return run_gemm(gemm_tn(dtype, M, N, K, X, dY, N, dW, N, db, N), static_cast<hipStream_t>(stream));
+}
+
+size_t dlvm_softmax_xent_ws_bytes(int64_t rows) {
+  if (rows < 1) return 0;
+  return align_up(16) + 2 * align_up(static_cast<size_t>(dlvm::softmax_xent_partials(rows)) * 4);
+}
+
+dlvm_status dlvm_softmax_xent(int32_t dtype, int64_t rows, int64_t classes, const float* logits,
+                              const int32_t* labels, float scale, void* dlogits, float* loss,
+                              void* ws, size_t ws_bytes, void* stream) {
+  if (!valid_dtype(dtype)) return fail(DLVM_ERR_INVALID_ARG, "bad dtype");
+  if (rows < 1 || classes < 1) return fail(DLVM_ERR_INVALID_ARG, "sizes must be positive");
+  if (logits == nullptr || labels == nullptr || dlogits == nullptr || loss == nullptr)
+    return fail(DLVM_ERR_INVALID_ARG, "null argument");
+  if (ws == nullptr || ws_bytes < dlvm_softmax_xent_ws_bytes(rows))
+    return fail(DLVM_ERR_WORKSPACE, "workspace missing or too small");
+  if (!aligned16(logits) || !aligned16(labels) || !aligned16(dlogits) || !aligned16(loss) ||
+      !aligned16(ws))
+    return fail(DLVM_ERR_MISALIGNED, "device pointers must be 16-byte aligned");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int32_t* flags = at<int32_t>(ws, 0);
+  float* partials = at<float>(ws, align_up(16));
+  int32_t* bad = at<int32_t>(ws, align_up(16) +
+                                     align_up(static_cast<size_t>(dlvm::softmax_xent_partials(rows)) * 4));
+  int np = 0;
+  hipError_t e = dlvm::launch_softmax_xent(dtype, rows, classes, logits, labels, scale, dlogits,
+                                           classes, partials, bad, &np, s);
+  if (e != hipSuccess) return hip_fail(e, "softmax cross-entropy launch");
+  dlvm::ZeroGaps none{};
+  e = dlvm::launch_finalize(partials, bad, np, scale, loss, flags, nullptr, none, s);
+  if (e != hipSuccess) return hip_fail(e, "loss finalisation launch");
+  return DLVM_OK;
+}
+
+size_t dlvm_chain8_ws_bytes(int64_t rows, int64_t cols) {
+  if (rows < 1 || cols < 1) return 0;
+  return align_up(16) + align_up(static_cast<size_t>(dlvm::chain8_partials(rows, cols)) * 4);
+}
+
+dlvm_status dlvm_chain8(int64_t rows, int64_t cols, const float* z, const float* bias,
+                        const float* x_skip, float* zbar, float* xbar, float* loss, void* ws,
+                        size_t ws_bytes, void* stream) {
+  if (rows < 1 || cols < 1) return fail(DLVM_ERR_INVALID_ARG, "sizes must be positive");
+  if (z == nullptr || bias == nullptr || x_skip == nullptr || zbar == nullptr || xbar == nullptr ||
+      loss == nullptr)
+    return fail(DLVM_ERR_INVALID_ARG, "null argument");
+  if (ws == nullptr || ws_bytes < dlvm_chain8_ws_bytes(rows, cols))
+    return fail(DLVM_ERR_WORKSPACE, "workspace missing or too small");
+  if (!aligned16(z) || !aligned16(bias) || !aligned16(x_skip) || !aligned16(zbar) ||
+      !aligned16(xbar) || !aligned16(loss) || !aligned16(ws))
+    return fail(DLVM_ERR_MISALIGNED, "device pointers must be 16-byte aligned");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int32_t* flags = at<int32_t>(ws, 0);
+  float* partials = at<float>(ws, align_up(16));
+  int np = 0;
+  hipError_t e = dlvm::launch_chain8(rows, cols, z, bias, x_skip, zbar, xbar, partials, false, &np, s);
+  if (e != hipSuccess) return hip_fail(e, "chain launch");
+  dlvm::ZeroGaps none{};
+  const float scale = static_cast<float>(1.0 / (static_cast<double>(rows) * static_cast<double>(cols)));
+  e = dlvm::launch_finalize(partials, nullptr, np, scale, loss, flags, nullptr, none, s);
+  if (e != hipSuccess) return hip_fail(e, "loss finalisation launch");
+  return DLVM_OK;
+}
+
+dlvm_status dlvm_sgd(int32_t dtype, int64_t n, void* params, float* master, const float* grads,
+                     float lr, void* stream) {
+  if (!valid_dtype(dtype)) return fail(DLVM_ERR_INVALID_ARG, "bad dtype");
+  if (n < 1) return fail(DLVM_ERR_INVALID_ARG, "n must be positive");
+  if (params == nullptr || grads == nullptr || (dtype == DLVM_BF16 && master == nullptr))
+    return fail(DLVM_ERR_INVALID_ARG, "null argument");
+  if (!aligned16(params) || !aligned16(grads) || (master && !aligned16(master)))
+    return fail(DLVM_ERR_MISALIGNED, "device pointers must be 16-byte aligned");
+  const hipError_t e = dlvm::launch_sgd(dtype, n, params, master, grads, lr,
+                                        static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "sgd launch");
+  return DLVM_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,63 @@
+// Device helpers shared by the gfx950 kernels: storage types, bf16 rounding,
+// activations and their derivatives from saved outputs.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace dlvm {
+
+typedef uint16_t bf16_t;  // raw bfloat16 bits in memory
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+enum Dtype { F32 = 0, BF16 = 1 };
+enum Act { ACT_NONE = 0, ACT_SIGMOID = 1, ACT_TANH = 2, ACT_RELU = 3 };
+
+__device__ __forceinline__ float bf16_to_f32(bf16_t h) {
+  return __uint_as_float(static_cast<uint32_t>(h) << 16);
+}
+
+// float32 -> bfloat16, round to nearest, ties to even; NaN stays a quiet NaN.
+__device__ __forceinline__ bf16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<bf16_t>(0x7fc0u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return static_cast<bf16_t>(u >> 16);
+}
+
+template <typename T> __device__ __forceinline__ float load_as_f32(const T* p);
+template <> __device__ __forceinline__ float load_as_f32<float>(const float* p) { return *p; }
+template <> __device__ __forceinline__ float load_as_f32<bf16_t>(const bf16_t* p) {
+  return bf16_to_f32(*p);
+}
+
+template <typename T> __device__ __forceinline__ T store_cast(float v);
+template <> __device__ __forceinline__ float store_cast<float>(float v) { return v; }
+template <> __device__ __forceinline__ bf16_t store_cast<bf16_t>(float v) { return f32_to_bf16(v); }
+
+// sigmoid(v) = 1 / (1 + exp(-v)); exp overflow gives exactly 0 for v -> -inf.
+__device__ __forceinline__ float sigmoidf_(float v) { return 1.0f / (1.0f + __expf(-v)); }
+
+__device__ __forceinline__ float apply_act(int act, float v) {
+  switch (act) {
+    case ACT_SIGMOID: return sigmoidf_(v);
+    case ACT_TANH: return tanhf(v);
+    case ACT_RELU: return v > 0.0f ? v : 0.0f;
+    default: return v;
+  }
+}
+
+// Derivative of the activation expressed through its saved output h
+// (common subexpression reuse: no exp/tanh is recomputed in the adjoint).
+__device__ __forceinline__ float act_grad_from_output(int act, float h) {
+  switch (act) {
+    case ACT_SIGMOID: return h * (1.0f - h);
+    case ACT_TANH: return 1.0f - h * h;
+    case ACT_RELU: return h > 0.0f ? 1.0f : 0.0f;
+    default: return 1.0f;
+  }
+}
+
+}  // namespace dlvm

@@ -1,0 +1,476 @@
+// Dense-layer matrix products on gfx950 matrix cores, with fused epilogues.
+//
+// The one kernel template computes C[M,N] = sum_k A(m,k) B(k,n) for the three
+// operand layouts a dense layer and its adjoint need (the adjoint of dot,
+// dA = dC.B^T and dB = A^T.dC, never materialises a transpose):
+//   NN  forward               A = X [M,K] (k contiguous), B = W [K,N] (n contiguous)
+//   NT  adjoint wrt input     A = dY [M,N'] (k contiguous), B = W [K',N'] read as W^T (k contiguous)
+//   TN  adjoint wrt weights   A = X [K,M] read as X^T (m contiguous), B = dY [K,N] (n contiguous)
+// and fuses the element-wise work around the product into the same kernel
+// (linear-algebra and element-wise fusion, DLVM sections 1 and 3.1.2):
+//   NN  H = act(alpha * acc + bias[n])                         (bias + activation)
+//   NT  dX = acc * act'(Hprev) + R, act' from the saved output (adjoint of act;
+//       R is another adjoint contribution to the same value, accumulated)
+//   TN  dW = acc (float32); db[n] = sum_k B(k,n) by the first row of tiles
+//       (the padded ones-row of [X 1]^T.dY, without materialising it)
+//
+// Data movement. Every operand tile is staged in LDS as rows of 128 bytes of
+// the reduction dimension (32 float32 or 64 bf16), one row per m (or n)
+// index, padded to a 144-byte stride. Global loads are 16 bytes per lane when
+// the operand's contiguous extent allows it (per operand), else element by
+// element with bounds checks. An operand whose reduction dimension is strided
+// in memory (the TN layout, and W in the NN layout) is transposed in registers
+// on its way to LDS (4x4 float32 blocks are a register renaming; 8x8 bf16
+// blocks use byte permutes), so the MFMA fragment of every lane is one
+// 16-byte LDS read in all layouts. The lane-to-chunk assignment (chunk index
+// fastest) together with the 144-byte stride keeps both those stores and the
+// fragment reads free of LDS bank conflicts. The next k-tile is prefetched into
+// registers while the current one is multiplied from LDS; LDS is
+// double-buffered so one barrier per k-tile suffices.
+//
+// Matrix cores: float32 uses v_mfma_f32_32x32x2_f32 (one 16-byte fragment =
+// 4 consecutive k per lane feeds 4 instructions), bf16 uses
+// v_mfma_f32_32x32x16_bf16 (8 consecutive k per lane feed one instruction).
+// Inside one fragment the assignment of k values to instruction slots is a
+// permutation applied identically to both operands, which leaves the sum
+// unchanged.
+//
+// Splitting the reduction inside a workgroup. For small products a workgroup
+// of WK groups of waves covers one output tile: every group multiplies the
+// same LDS tiles but takes every WK-th k-step of them, and at the end the
+// groups' accumulators are added through LDS in increasing group order before
+// the epilogue. This keeps all four SIMDs of a compute unit busy on a small
+// tile without any cross-workgroup communication, and the sum order is fixed.
+#pragma once
+
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace dlvm {
+namespace gemm {
+
+constexpr int kRowStride = 144;  // bytes per LDS row: 128 bytes of k plus 16 of padding
+constexpr int kChunks = 8;       // 16-byte chunks of k per LDS row
+
+enum Epi { EPI_STORE = 0, EPI_DACT = 1, EPI_DW = 2 };
+
+template <typename T> struct Elem;
+template <> struct Elem<float> { static constexpr int VW = 4; static constexpr int BK = 32; };
+template <> struct Elem<bf16_t> { static constexpr int VW = 8; static constexpr int BK = 64; };
+
+struct Params {
+  int64_t M, N, K;
+  const void* A; int64_t lda;
+  const void* B; int64_t ldb;
+  void* C; int64_t ldc;
+  const void* bias;
+  const void* aux;
+  const void* residual;
+  float* colsum;
+  float alpha;
+  int act;
+  int tiles_m, tiles_n;
+  int64_t nvec;  // entries of bias / colsum (columns n >= nvec have none)
+};
+
+__device__ __forceinline__ uint32_t perm_b32(uint32_t hi, uint32_t lo, uint32_t sel) {
+  return __builtin_amdgcn_perm(hi, lo, sel);
+}
+
+// One operand tile of ROWS x (KSEG * BK): element (r, k) of the operand is
+//   KMAJ:  P[r * ld + k]   (k contiguous)
+//   !KMAJ: P[k * ld + r]   (r contiguous)
+// and lands in LDS segment (k / BK) % KSEG, row r, byte (k % BK) * sizeof(T).
+// A segment holds SEG_ROWS rows (the A and B tiles of one stage share it).
+template <typename T, bool KMAJ, int ROWS, int THREADS, bool VEC, int KSEG>
+struct TileLoader {
+  static constexpr int VW = Elem<T>::VW;
+  static constexpr int CH = kChunks * KSEG;  // 16-byte chunks of k per row and stage
+  static constexpr int TASKS = KMAJ ? ROWS * CH : (ROWS / VW) * CH;
+  static constexpr int PER_THREAD = (TASKS + THREADS - 1) / THREADS;
+  static constexpr int NREG = KMAJ ? PER_THREAD : PER_THREAD * VW;
+  uint32_t v[NREG][4];
+
+  // Task q -> (row or row block, chunk). K-contiguous operands put the chunk
+  // index fastest (consecutive lanes read consecutive 16 bytes of a row);
+  // r-contiguous operands put the 8 chunks of a segment fastest, then the row
+  // blocks, then the segment (each k row is read in 128-byte runs).
+  __device__ __forceinline__ static void task(int q, int& rowblk, int& c) {
+    if constexpr (KMAJ) {
+      rowblk = q / CH;
+      c = q % CH;
+    } else {
+      constexpr int RB = ROWS / VW;
+      const int c8 = q % kChunks;
+      rowblk = (q / kChunks) % RB;
+      c = (q / (kChunks * RB)) * kChunks + c8;
+    }
+  }
+
+  __device__ __forceinline__ void load(const T* __restrict__ P, int64_t ld, int64_t r0,
+                                       int64_t rlim, int64_t k0, int64_t klim, int tid) {
+#pragma unroll
+    for (int i = 0; i < PER_THREAD; ++i) {
+      const int q = tid + i * THREADS;
+      if (TASKS % THREADS != 0 && q >= TASKS) break;
+      int rb, c;
+      task(q, rb, c);
+      if constexpr (KMAJ) {
+        const int64_t gr = r0 + rb;
+        const int64_t gk = k0 + c * VW;
+        if constexpr (VEC) {
+          if (gr < rlim && gk < klim) {
+            const uint4 x = *reinterpret_cast<const uint4*>(P + gr * ld + gk);
+            v[i][0] = x.x; v[i][1] = x.y; v[i][2] = x.z; v[i][3] = x.w;
+          } else {
+            v[i][0] = v[i][1] = v[i][2] = v[i][3] = 0u;
+          }
+        } else {
+          T e[VW];
+#pragma unroll
+          for (int j = 0; j < VW; ++j)
+            e[j] = (gr < rlim && gk + j < klim) ? P[gr * ld + gk + j] : T(0);
+          const uint32_t* w = reinterpret_cast<const uint32_t*>(e);
+          v[i][0] = w[0]; v[i][1] = w[1]; v[i][2] = w[2]; v[i][3] = w[3];
+        }
+      } else {
+        const int64_t gr = r0 + rb * VW;
+        const int64_t gk = k0 + c * VW;
+        uint32_t raw[VW][4];  // raw[kk] = elements (gk + kk, gr .. gr + VW - 1)
+#pragma unroll
+        for (int kk = 0; kk < VW; ++kk) {
+          if constexpr (VEC) {
+            // The whole 16-byte run lies inside row gk+kk (ld is a multiple of
+            // the vector width); elements past rlim reach only outputs that
+            // are not stored.
+            if (gr < rlim && gk + kk < klim) {
+              const uint4 x = *reinterpret_cast<const uint4*>(P + (gk + kk) * ld + gr);
+              raw[kk][0] = x.x; raw[kk][1] = x.y; raw[kk][2] = x.z; raw[kk][3] = x.w;
+            } else {
+              raw[kk][0] = raw[kk][1] = raw[kk][2] = raw[kk][3] = 0u;
+            }
+          } else {
+            T e[VW];
+#pragma unroll
+            for (int j = 0; j < VW; ++j)
+              e[j] = (gr + j < rlim && gk + kk < klim) ? P[(gk + kk) * ld + gr + j] : T(0);
+            const uint32_t* w = reinterpret_cast<const uint32_t*>(e);
+            raw[kk][0] = w[0]; raw[kk][1] = w[1]; raw[kk][2] = w[2]; raw[kk][3] = w[3];
+          }
+        }
+        if constexpr (sizeof(T) == 4) {
+          // 4x4 float32 transpose: output row j holds k = gk .. gk+3 of r = gr + j.
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int kk = 0; kk < 4; ++kk) v[i * 4 + j][kk] = raw[kk][j];
+        } else {
+          // 8x8 bf16 transpose: output row j, dword p = (k = 2p, k = 2p+1) of r = gr + j.
+#pragma unroll
+          for (int j = 0; j < 8; ++j)
+#pragma unroll
+            for (int p = 0; p < 4; ++p)
+              v[i * 8 + j][p] = perm_b32(raw[2 * p + 1][j >> 1], raw[2 * p][j >> 1],
+                                         (j & 1) ? 0x07060302u : 0x05040100u);
+        }
+      }
+    }
+  }
+
+  // `lds` is this operand's row 0 in segment 0; segments are SEG_BYTES apart.
+  template <int SEG_BYTES>
+  __device__ __forceinline__ void store(char* lds, int tid) const {
+#pragma unroll
+    for (int i = 0; i < PER_THREAD; ++i) {
+      const int q = tid + i * THREADS;
+      if (TASKS % THREADS != 0 && q >= TASKS) break;
+      int rb, c;
+      task(q, rb, c);
+      char* base = lds + (c / kChunks) * SEG_BYTES + (c % kChunks) * 16;
+      if constexpr (KMAJ) {
+        *reinterpret_cast<uint4*>(base + rb * kRowStride) =
+            make_uint4(v[i][0], v[i][1], v[i][2], v[i][3]);
+      } else {
+#pragma unroll
+        for (int j = 0; j < VW; ++j)
+          *reinterpret_cast<uint4*>(base + (rb * VW + j) * kRowStride) =
+              make_uint4(v[i * VW + j][0], v[i * VW + j][1], v[i * VW + j][2],
+                         v[i * VW + j][3]);
+      }
+    }
+  }
+};
+
+template <typename T>
+__device__ __forceinline__ void mfma_frag(f32x16& acc, const uint4& a, const uint4& b);
+
+template <>
+__device__ __forceinline__ void mfma_frag<float>(f32x16& acc, const uint4& a, const uint4& b) {
+  acc = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.x), __uint_as_float(b.x), acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.y), __uint_as_float(b.y), acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.z), __uint_as_float(b.z), acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.w), __uint_as_float(b.w), acc, 0, 0, 0);
+}
+
+template <>
+__device__ __forceinline__ void mfma_frag<bf16_t>(f32x16& acc, const uint4& a, const uint4& b) {
+  acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
+                                                 __builtin_bit_cast(bf16x8, b), acc, 0, 0, 0);
+}
+
+template <typename T, typename TO, bool AK, bool BKM, int BM, int BN, int WM, int WN, int WK,
+          int KSEG, bool VA, bool VB, int EPI>
+__global__ __launch_bounds__(64 * WM * WN * WK) void dlvm_gemm_kernel(Params p) {
+  constexpr int THREADS = 64 * WM * WN * WK;
+  constexpr int BK = Elem<T>::BK;
+  constexpr int WTM = BM / WM, WTN = BN / WN;
+  constexpr int TM = WTM / 32, TN = WTN / 32;
+  static_assert(TM >= 1 && TN >= 1 && WTM % 32 == 0 && WTN % 32 == 0, "wave tile");
+  static_assert(WK == 1 || WK == 2 || WK == 4, "k-step groups");
+  constexpr int SEG = (BM + BN) * kRowStride;        // one k-segment of A and B rows
+  constexpr int STAGE = KSEG * SEG;                   // one pipeline stage
+  constexpr int KSTAGE = KSEG * BK;                   // k elements per stage
+  constexpr int RED_BYTES = (WK - 1) * BM * BN * 4;  // accumulators of groups 1..WK-1
+  constexpr int SMEM = 2 * STAGE > RED_BYTES ? 2 * STAGE : RED_BYTES;
+  __shared__ __attribute__((aligned(16))) char smem[SMEM];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wk = wave / (WM * WN);          // k-step group
+  const int wmn = wave % (WM * WN);
+  const int wm = wmn / WN, wn = wmn % WN;
+
+  // Consecutive workgroups walk down a column of tiles, so they share the
+  // B tile (the weights in the forward) through L2.
+  const int tile = static_cast<int>(blockIdx.x);
+  const int tm = tile % p.tiles_m;
+  const int tn = tile / p.tiles_m;
+  const int64_t m0 = static_cast<int64_t>(tm) * BM;
+  const int64_t n0 = static_cast<int64_t>(tn) * BN;
+
+  const T* __restrict__ A = static_cast<const T*>(p.A);
+  const T* __restrict__ B = static_cast<const T*>(p.B);
+
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+  // Bias-gradient column sums (TN): the first row of tiles sums its B tiles.
+  constexpr int CS_PER = (BN + THREADS - 1) / THREADS;
+  float csum[CS_PER];
+#pragma unroll
+  for (int i = 0; i < CS_PER; ++i) csum[i] = 0.0f;
+  const bool do_colsum = (EPI == EPI_DW) && (p.colsum != nullptr) && (tm == 0);
+
+  TileLoader<T, AK, BM, THREADS, VA, KSEG> la;
+  TileLoader<T, BKM, BN, THREADS, VB, KSEG> lb;
+  const int64_t nk = (p.K + KSTAGE - 1) / KSTAGE;
+
+  la.load(A, p.lda, m0, p.M, 0, p.K, tid);
+  lb.load(B, p.ldb, n0, p.N, 0, p.K, tid);
+  la.template store<SEG>(smem, tid);
+  lb.template store<SEG>(smem + BM * kRowStride, tid);
+  __syncthreads();
+
+  const int frag_row = lane & 31;
+  const int frag_half = lane >> 5;
+
+  for (int64_t kt = 0; kt < nk; ++kt) {
+    const int buf = static_cast<int>(kt & 1);
+    char* stage = smem + buf * STAGE;
+    const bool more = kt + 1 < nk;
+    if (more) {
+      la.load(A, p.lda, m0, p.M, (kt + 1) * KSTAGE, p.K, tid);
+      lb.load(B, p.ldb, n0, p.N, (kt + 1) * KSTAGE, p.K, tid);
+    }
+#pragma unroll
+    for (int g = 0; g < 4 * KSEG; ++g) {
+      if (g % WK != wk) continue;  // this group's k-steps
+      const char* As = stage + (g / 4) * SEG;
+      const char* Bs = As + BM * kRowStride;
+      const int cofs = (2 * (g % 4) + frag_half) * 16;
+      uint4 af[TM], bfr[TN];
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+        af[i] = *reinterpret_cast<const uint4*>(As + (wm * WTM + i * 32 + frag_row) * kRowStride + cofs);
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+        bfr[j] = *reinterpret_cast<const uint4*>(Bs + (wn * WTN + j * 32 + frag_row) * kRowStride + cofs);
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) mfma_frag<T>(acc[i][j], af[i], bfr[j]);
+    }
+    if constexpr (EPI == EPI_DW) {
+      if (do_colsum) {
+#pragma unroll
+        for (int ci = 0; ci < CS_PER; ++ci) {
+          const int r = tid + ci * THREADS;
+          if (r < BN) {
+#pragma unroll
+            for (int c = 0; c < kChunks * KSEG; ++c) {
+              const uint4 x = *reinterpret_cast<const uint4*>(
+                  stage + (c / kChunks) * SEG + BM * kRowStride + r * kRowStride + (c % kChunks) * 16);
+              const uint32_t w[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                if constexpr (sizeof(T) == 4) {
+                  csum[ci] += __uint_as_float(w[e]);
+                } else {
+                  csum[ci] += __uint_as_float(w[e] << 16);
+                  csum[ci] += __uint_as_float(w[e] & 0xffff0000u);
+                }
+              }
+            }
+          }
+        }
+      }
+    }
+    if (more) {
+      char* next = smem + (buf ^ 1) * STAGE;
+      la.template store<SEG>(next, tid);
+      lb.template store<SEG>(next + BM * kRowStride, tid);
+    }
+    __syncthreads();
+  }
+
+  if constexpr (WK > 1) {
+    // Add the k-step groups' accumulators through LDS, group 1 first.
+    constexpr int WAVE_F = TM * TN * 16 * 64;  // accumulator floats of one wave
+    float* red = reinterpret_cast<float*>(smem);
+    if (wk > 0) {
+      float* dst = red + ((wk - 1) * (WM * WN) + wmn) * WAVE_F;
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) dst[((i * TN + j) * 16 + r) * 64 + lane] = acc[i][j][r];
+    }
+    __syncthreads();
+    if (wk > 0) {
+      // Only the first group runs the epilogue; the column sums (kept by
+      // every thread of the workgroup) are written by their owners below.
+      if constexpr (EPI == EPI_DW) {
+        if (do_colsum) {
+#pragma unroll
+          for (int ci = 0; ci < CS_PER; ++ci) {
+            const int r = tid + ci * THREADS;
+            if (r < BN && n0 + r < p.nvec) p.colsum[n0 + r] = csum[ci];
+          }
+        }
+      }
+      return;
+    }
+#pragma unroll
+    for (int q = 1; q < WK; ++q) {
+      const float* src = red + ((q - 1) * (WM * WN) + wmn) * WAVE_F;
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) acc[i][j][r] += src[((i * TN + j) * 16 + r) * 64 + lane];
+    }
+  }
+
+  // Epilogue. Accumulator register r of a 32x32 block holds row
+  // 8*(r/4) + 4*(lane/32) + r%4 and column lane%32 of the block.
+  TO* __restrict__ C = static_cast<TO*>(p.C);
+#pragma unroll
+  for (int j = 0; j < TN; ++j) {
+    const int64_t col = n0 + wn * WTN + j * 32 + (lane & 31);
+    const bool col_ok = col < p.N;
+    float bias_v = 0.0f;
+    if constexpr (EPI == EPI_STORE) {
+      if (p.bias != nullptr && col < p.nvec) bias_v = load_as_f32<T>(static_cast<const T*>(p.bias) + col);
+    }
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int64_t row = m0 + wm * WTM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        if (!col_ok || row >= p.M) continue;
+        float v = acc[i][j][r];
+        const int64_t idx = row * p.ldc + col;
+        if constexpr (EPI == EPI_STORE) {
+          v = apply_act(p.act, p.alpha * v + bias_v);
+        } else if constexpr (EPI == EPI_DACT) {
+          if (p.act != ACT_NONE)
+            v *= act_grad_from_output(p.act, load_as_f32<T>(static_cast<const T*>(p.aux) + idx));
+          if (p.residual != nullptr) v += load_as_f32<TO>(static_cast<const TO*>(p.residual) + idx);
+        }
+        C[idx] = store_cast<TO>(v);
+      }
+    }
+  }
+  if constexpr (EPI == EPI_DW) {
+    if (do_colsum) {
+#pragma unroll
+      for (int ci = 0; ci < CS_PER; ++ci) {
+        const int r = tid + ci * THREADS;
+        if (r < BN && n0 + r < p.nvec) p.colsum[n0 + r] = csum[ci];
+      }
+    }
+  }
+}
+
+// Tile configurations: (BM, BN, waves along M, waves along N, k-step groups,
+// k-segments per stage). A stage is KSEG * 128 bytes of k per row.
+//   0: 128 x 128, 2 x 2 waves,             1 segment    large products
+//   1:  64 x  64, 2 x 2 waves,             2 segments   medium products
+//   2: 128 x  32, 4 x 1 waves,             2 segments   narrow outputs (N <= 32)
+//   3:  32 x  32, 1 wave x 4 k-groups,     4 segments   small products (latency-bound)
+//   4:  64 x  64, 2 x 2 waves x 2 k-groups, 2 segments  (512 threads) medium-small products
+template <typename T, typename TO, bool AK, bool BKM, bool VA, bool VB, int EPI>
+hipError_t launch_cfg(const Params& p, int cfg, unsigned grid, hipStream_t s) {
+  switch (cfg) {
+    case 0:
+      hipLaunchKernelGGL((dlvm_gemm_kernel<T, TO, AK, BKM, 128, 128, 2, 2, 1, 1, VA, VB, EPI>),
+                         dim3(grid), dim3(256), 0, s, p);
+      break;
+    case 1:
+      hipLaunchKernelGGL((dlvm_gemm_kernel<T, TO, AK, BKM, 64, 64, 2, 2, 1, 2, VA, VB, EPI>),
+                         dim3(grid), dim3(256), 0, s, p);
+      break;
+    case 2:
+      hipLaunchKernelGGL((dlvm_gemm_kernel<T, TO, AK, BKM, 128, 32, 4, 1, 1, 2, VA, VB, EPI>),
+                         dim3(grid), dim3(256), 0, s, p);
+      break;
+    case 3:
+      hipLaunchKernelGGL((dlvm_gemm_kernel<T, TO, AK, BKM, 32, 32, 1, 1, 4, 4, VA, VB, EPI>),
+                         dim3(grid), dim3(256), 0, s, p);
+      break;
+    default:
+      hipLaunchKernelGGL((dlvm_gemm_kernel<T, TO, AK, BKM, 64, 64, 2, 2, 2, 2, VA, VB, EPI>),
+                         dim3(grid), dim3(512), 0, s, p);
+      break;
+  }
+  return hipGetLastError();
+}
+
+template <typename T, typename TO, bool AK, bool BKM, int EPI>
+hipError_t launch_vec(const Params& p, int cfg, unsigned grid, bool va, bool vb, hipStream_t s) {
+  if (va) {
+    return vb ? launch_cfg<T, TO, AK, BKM, true, true, EPI>(p, cfg, grid, s)
+              : launch_cfg<T, TO, AK, BKM, true, false, EPI>(p, cfg, grid, s);
+  }
+  return vb ? launch_cfg<T, TO, AK, BKM, false, true, EPI>(p, cfg, grid, s)
+            : launch_cfg<T, TO, AK, BKM, false, false, EPI>(p, cfg, grid, s);
+}
+
+// Per-layout entry points (one translation unit each).
+hipError_t launch_nn(const Params& p, int dtype, int out_dtype, int cfg, unsigned grid, bool va,
+                     bool vb, hipStream_t s);
+hipError_t launch_nt(const Params& p, int dtype, int out_dtype, int cfg, unsigned grid, bool va,
+                     bool vb, hipStream_t s);
+hipError_t launch_tn(const Params& p, int dtype, int cfg, unsigned grid, bool va, bool vb,
+                     hipStream_t s);
+
+}  // namespace gemm
+}  // namespace dlvm

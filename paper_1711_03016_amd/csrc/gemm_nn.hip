@@ -1,0 +1,16 @@
+// Instantiations of the dense-layer product for the NN layout (forward products: bias + activation
+// epilogue).
+#include "gemm_kernel.hpp"
+
+namespace dlvm {
+namespace gemm {
+
+hipError_t launch_nn(const Params& p, int dtype, int out_dtype, int cfg, unsigned grid, bool va,
+                     bool vb, hipStream_t s) {
+  if (dtype == F32) return launch_vec<float, float, true, false, EPI_STORE>(p, cfg, grid, va, vb, s);
+  if (out_dtype == F32) return launch_vec<bf16_t, float, true, false, EPI_STORE>(p, cfg, grid, va, vb, s);
+  return launch_vec<bf16_t, bf16_t, true, false, EPI_STORE>(p, cfg, grid, va, vb, s);
+}
+
+}  // namespace gemm
+}  // namespace dlvm

@@ -1,0 +1,81 @@
+// Host-side launch interface of the gfx950 kernels (internal to the library).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace dlvm {
+
+enum class Layout : int {
+  NN = 0,  // C = A.B        A [M,K] K-contiguous, B [K,N] N-contiguous (forward)
+  NT = 1,  // C = A.B^T      A [M,K] K-contiguous, B [N,K] K-contiguous (adjoint wrt input)
+  TN = 2,  // C = A^T.B      A [K,M] M-contiguous, B [K,N] N-contiguous (adjoint wrt weights)
+};
+
+struct GemmDesc {
+  Layout layout;
+  int dtype;       // operand storage: F32 or BF16
+  int out_dtype;   // C storage: F32 or BF16
+  int act;         // NN: activation applied; NT: activation whose derivative is applied
+  int64_t M, N, K;
+  const void* A; int64_t lda;
+  const void* B; int64_t ldb;
+  void* C; int64_t ldc;
+  const void* bias;      // NN: [N] in operand dtype, or null
+  const void* aux;       // NT: saved activation [M, ldc] in operand dtype, or null
+  const void* residual;  // NT: [M, ldc] in out dtype added after act', or null
+  float* colsum;         // TN: [nvec] float32 sum over k of B(k, n), or null
+  float alpha;           // NN: scale of the product
+  int64_t nvec;          // entries of bias / colsum (0 means N). Columns n >= nvec
+                         // have none; with a padded operand they are zero.
+};
+
+// How one product is launched: tile configuration and grid.
+struct GemmPlan {
+  int cfg;               // tile configuration index
+  int bm, bn;            // tile shape
+  int tiles_m, tiles_n;
+};
+
+// Choose the launch of a product.
+GemmPlan plan_gemm(const GemmDesc& d);
+
+// Enqueue one GEMM with its fused epilogue as planned. Returns hipSuccess or
+// the launch error. The caller has validated shapes and pointers.
+hipError_t launch_gemm(const GemmDesc& d, const GemmPlan& plan, hipStream_t s);
+
+// Softmax cross-entropy rows: one partial loss per row block into `partials`.
+// Returns the number of partials written through *n_partials.
+// `bad` receives, per row block, the number of labels outside [0, classes).
+// dlogits rows have stride ld_dlogits >= classes; columns [classes, ld) are written as 0.
+hipError_t launch_softmax_xent(int dtype, int64_t rows, int64_t classes, const float* logits,
+                               const int32_t* labels, float scale, void* dlogits,
+                               int64_t ld_dlogits, float* partials, int32_t* bad, int* n_partials,
+                               hipStream_t s);
+int softmax_xent_partials(int64_t rows);
+
+// Fused chain; `fwd_only` writes e into zbar and skips the adjoint.
+hipError_t launch_chain8(int64_t rows, int64_t cols, const float* z, const float* bias,
+                         const float* x_skip, float* zbar, float* xbar, float* partials,
+                         bool fwd_only, int* n_partials, hipStream_t s);
+int chain8_partials(int64_t rows, int64_t cols);
+
+// Sum `n` partials in a fixed order, multiply by `scale`, write *out. Writes
+// flags[0] = (any bad label counted in `bad`, which may be null) and
+// flags[1] = (loss not finite) on every call. Zeroes the `gaps` ranges of
+// `zero_base` (may be null).
+struct ZeroGaps {
+  static constexpr int kMax = 64;
+  int n;
+  int64_t off[kMax];
+  int32_t len[kMax];
+};
+hipError_t launch_finalize(const float* partials, const int32_t* bad, int n, float scale,
+                           float* out, int32_t* flags, float* zero_base, const ZeroGaps& gaps,
+                           hipStream_t s);
+
+hipError_t launch_sgd(int dtype, int64_t n, void* params, float* master, const float* grads,
+                      float lr, hipStream_t s);
+
+}  // namespace dlvm

@@ -1,0 +1,277 @@
+"""End-to-end GPU parity of the forward, gradient and SGD calls on the five workloads.
+
+Small workloads are compared at full size, element by element. The two large
+ones are compared (a) at a reduced batch, element by element, and (b) at their
+full batch in the launch configuration the benchmark times, using a batch made
+of a few base rows repeated in a seeded order: the mean loss and its gradient
+over such a batch equal those over the base rows, and every row's forward value
+and input gradient equal those of its base row.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import paper_1711_03016_amd as dl
+import workloads
+from helpers import TOL, device, rel_l2, to_dev, to_np, torch_dtype
+
+pytestmark = pytest.mark.gpu
+
+
+def _run(wl, x, params, y, wrt_x=None, forward=True):
+    """Run forward and gradient on the GPU; return host results."""
+    import torch
+    B = x.shape[0]
+    wrt_x = wl.wrt_x if wrt_x is None else wrt_x
+    m = dl.Model(wl.widths, wl.acts, wl.dtype, wl.loss, wrt_x, B)
+    dev = device()
+    P = m.pack(params, dev, torch_dtype(wl.dtype))
+    xd = to_dev(x, wl.dtype)
+    yd = None if y is None else torch.from_numpy(np.asarray(y, np.int32)).to(dev)
+    ws = torch.empty(m.workspace_bytes(B), dtype=torch.uint8, device=dev)
+    out = {}
+    if forward:
+        o = torch.empty((B, wl.widths[-1]), device=dev)
+        m.forward(P, xd, B, o, ws)
+        out["forward"] = to_np(o)
+    loss = torch.empty(1, device=dev)
+    dP = torch.full((m.param_count(),), float("nan"), device=dev)
+    dx = torch.empty((B, wl.widths[0]), device=dev) if wrt_x else None
+    m.gradient(P, xd, yd, B, loss, dP, dx, ws)
+    torch.cuda.synchronize()
+    out["loss"] = loss.item()
+    out["grads"] = [(to_np(a), to_np(b)) for a, b in m.unpack(dP)]
+    out["dparams"] = dP
+    out["dx"] = None if dx is None else to_np(dx)
+    out["status"] = m.check(ws)
+    out["model"], out["P"], out["ws"] = m, P, ws
+    return out
+
+
+def _spec(wl):
+    return oracle.MlpSpec(wl.widths, wl.acts, wl.loss, wl.dtype)
+
+
+def _order_tolerances(wl, x, params, y, ref_grads):
+    """Per-layer bounds for bf16 networks: max(2e-2, 2 x the oracle's own spread).
+
+    The spread is the distance between the oracle's float64-accumulate and
+    float32-accumulate evaluations of the same bf16-storage network: the part
+    of the gradient that the accumulation order does not determine (ReLU mask
+    flips behind bf16 rounding boundaries). Only oracle runs enter it.
+    """
+    from dataclasses import replace
+    if wl.dtype != "bf16":
+        return None
+    alt = replace(_spec(wl), accumulate="f32")
+    _, g32, _ = oracle.mlp_gradient(alt, x, params, y)
+    tol = TOL["bf16"]
+    return [(max(tol, 2 * rel_l2(a32, a)), max(tol, 2 * rel_l2(b32, b)))
+            for (a32, b32), (a, b) in zip(g32, ref_grads)]
+
+
+def _compare(wl, got, ref_loss, ref_grads, ref_dx=None, ref_out=None, tol=None,
+             layer_tols=None):
+    tol = TOL[wl.dtype] if tol is None else tol
+    assert got["status"] == dl.OK
+    assert abs(got["loss"] - ref_loss) <= tol * abs(ref_loss), (got["loss"], ref_loss)
+    for l, ((gw, gb), (rw, rb)) in enumerate(zip(got["grads"], ref_grads)):
+        tw, tb = (tol, tol) if layer_tols is None else layer_tols[l]
+        ew, eb = rel_l2(gw, rw), rel_l2(gb, rb)
+        assert ew <= tw, (l, "dW", ew, tw)
+        assert eb <= tb, (l, "db", eb, tb)
+    if ref_dx is not None:
+        assert rel_l2(got["dx"], ref_dx) <= tol
+    if ref_out is not None:
+        assert rel_l2(got["forward"], ref_out) <= tol
+
+
+@pytest.mark.parametrize("name", ["c1", "c2", "c3"])
+def test_workload_full_size(name):
+    wl = workloads.WORKLOADS[name]
+    x, params, y = workloads.make_inputs(wl, bias_scale=0.1)
+    got = _run(wl, x, params, y, wrt_x=True)
+    rl, rg, rdx = oracle.mlp_gradient(_spec(wl), x, params, y, wrt_x=True)
+    _, rout = oracle.mlp_forward(_spec(wl), x, params, y)
+    _compare(wl, got, rl, rg, rdx, rout)
+
+
+def test_c2_gradient_then_sgd():
+    import torch
+    wl = workloads.WORKLOADS["c2"]
+    x, params, y = workloads.make_inputs(wl)
+    got = _run(wl, x, params, y, forward=False)
+    m, P = got["model"], got["P"]
+    m.sgd_step(P, None, got["dparams"], wl.lr)
+    torch.cuda.synchronize()
+    _, rg, _ = oracle.mlp_gradient(_spec(wl), x, params, y)
+    for (gW, gb), (W, b), (dW, db) in zip(m.unpack(P), params, rg):
+        assert rel_l2(to_np(gW), oracle.sgd_f32(W, dW, wl.lr)) <= 1e-6
+        # the biases start at zero, so their new value is the step -lr*db itself
+        assert rel_l2(to_np(gb), oracle.sgd_f32(b, db, wl.lr)) <= TOL["f32"]
+
+
+def test_gradient_is_deterministic():
+    import torch
+    wl = workloads.WORKLOADS["c2"]
+    x, params, y = workloads.make_inputs(wl, bias_scale=0.1)
+    a = _run(wl, x, params, y, wrt_x=True)
+    m, P, ws = a["model"], a["P"], a["ws"]
+    dev = device()
+    xd = to_dev(x)
+    yd = torch.from_numpy(y).to(dev)
+    for _ in range(3):
+        loss = torch.empty(1, device=dev)
+        dP = torch.empty(m.param_count(), device=dev)
+        dx = torch.empty((x.shape[0], wl.widths[0]), device=dev)
+        m.gradient(P, xd, yd, x.shape[0], loss, dP, dx, ws)
+        torch.cuda.synchronize()
+        assert torch.equal(dP, a["dparams"])
+        assert loss.item() == a["loss"]
+        assert np.array_equal(to_np(dx), a["dx"])
+
+
+def test_dparams_padding_is_zero():
+    wl = workloads.WORKLOADS["c1"]
+    x, params, y = workloads.make_inputs(wl)
+    got = _run(wl, x, params, y, forward=False)
+    dP = to_np(got["dparams"])
+    offs, lds = got["model"].param_layout_lds()
+    assert lds[-1] == 16 and lds[0] == wl.widths[1]   # 10 classes padded to 16
+    live = np.zeros(dP.size, bool)
+    for l in range(wl.n_layers):
+        K, N, ld = wl.widths[l], wl.widths[l + 1], lds[l]
+        for k in range(K):
+            live[offs[2 * l] + k * ld:offs[2 * l] + k * ld + N] = True
+        live[offs[2 * l + 1]:offs[2 * l + 1] + N] = True
+    assert not np.isnan(dP).any()
+    assert (dP[~live] == 0).all()     # gaps between tensors and W padding columns
+
+
+def test_fig3_single_row():
+    """Fig. 3's shapes: x <1 x 784>, w <784 x 10>, b <1 x 10>, gradient wrt all."""
+    from dataclasses import replace
+    wl = replace(workloads.WORKLOADS["c1"], widths=(784, 10), acts=("none",), batch=1)
+    x, params, y = workloads.make_inputs(wl, bias_scale=0.1)
+    got = _run(wl, x, params, y, wrt_x=True)
+    rl, rg, rdx = oracle.mlp_gradient(_spec(wl), x, params, y, wrt_x=True)
+    _, rout = oracle.mlp_forward(_spec(wl), x, params, y)
+    _compare(wl, got, rl, rg, rdx, rout)
+
+
+@pytest.mark.parametrize("batch", [1, 37, 300])
+def test_ragged_batches(batch):
+    wl = workloads.WORKLOADS["c3"]
+    x, params, y = workloads.make_inputs(wl, batch=batch, bias_scale=0.1)
+    got = _run(wl, x, params, y, wrt_x=True)
+    rl, rg, rdx = oracle.mlp_gradient(_spec(wl), x, params, y, wrt_x=True)
+    _compare(wl, got, rl, rg, rdx, layer_tols=_order_tolerances(wl, x, params, y, rg))
+
+
+def test_label_out_of_range_is_reported():
+    wl = workloads.WORKLOADS["c1"]
+    x, params, y = workloads.make_inputs(wl)
+    y = y.copy()
+    y[3] = 10
+    got = _run(wl, x, params, y, forward=False)
+    assert got["status"] == dl.ERR_LABEL_RANGE
+    assert np.isnan(got["loss"])
+    y[3] = 2
+    good = _run(wl, x, params, y, forward=False)
+    assert good["status"] == dl.OK
+
+
+def test_non_default_stream():
+    import torch
+    wl = workloads.WORKLOADS["c2"]
+    x, params, y = workloads.make_inputs(wl)
+    ref = _run(wl, x, params, y, forward=False)
+    m, P, ws = ref["model"], ref["P"], ref["ws"]
+    dev = device()
+    s = torch.cuda.Stream()
+    xd, yd = to_dev(x), torch.from_numpy(y).to(dev)
+    loss = torch.empty(1, device=dev)
+    dP = torch.empty(m.param_count(), device=dev)
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s):
+        m.gradient(P, xd, yd, x.shape[0], loss, dP, None, ws, stream=s)
+        ev = torch.cuda.Event()
+        ev.record(s)
+    ev.synchronize()
+    assert torch.equal(dP, ref["dparams"])
+
+
+# ---------------------------------------------------------------------------
+# the two large workloads
+# ---------------------------------------------------------------------------
+def test_c4_reduced_batch():
+    wl = workloads.WORKLOADS["c4"]
+    x, params, _ = workloads.make_inputs(wl, batch=256, bias_scale=0.05)
+    got = _run(wl, x, params, None)
+    rl, rg, rdx = oracle.mlp_gradient(_spec(wl), x, params, None, wrt_x=True)
+    _, rout = oracle.mlp_forward(_spec(wl), x, params)
+    _compare(wl, got, rl, rg, rdx, rout)
+
+
+def test_c4_full_batch_repeated_rows():
+    wl = workloads.WORKLOADS["c4"]
+    base = 128
+    xb, params, _ = workloads.make_inputs(wl, batch=base, bias_scale=0.05)
+    x, _, idx = workloads.repeat_rows(xb, None, wl.batch)
+    got = _run(wl, x, params, None)
+    rl, rg, rdx = oracle.mlp_gradient(_spec(wl), xb, params, None, wrt_x=True)
+    _, rout = oracle.mlp_forward(_spec(wl), xb, params)
+    _compare(wl, got, rl, rg, rdx[idx] * (base / wl.batch), rout[idx])
+
+
+def test_c5_reduced_batch():
+    wl = workloads.WORKLOADS["c5"]
+    x, params, y = workloads.make_inputs(wl, batch=64, bias_scale=0.05)
+    got = _run(wl, x, params, y)
+    rl, rg, _ = oracle.mlp_gradient(_spec(wl), x, params, y)
+    _, rout = oracle.mlp_forward(_spec(wl), x, params, y)
+    _compare(wl, got, rl, rg, None, rout, layer_tols=_order_tolerances(wl, x, params, y, rg))
+
+
+def test_c5_full_batch_repeated_rows_and_sgd():
+    import torch
+    wl = workloads.WORKLOADS["c5"]
+    base = 64
+    xb, params, yb = workloads.make_inputs(wl, batch=base, bias_scale=0.05)
+    x, y, idx = workloads.repeat_rows(xb, yb, wl.batch)
+    got = _run(wl, x, params, y)
+    rl, rg, _ = oracle.mlp_gradient(_spec(wl), xb, params, yb)
+    _, rout = oracle.mlp_forward(_spec(wl), xb, params, yb)
+    _compare(wl, got, rl, rg, None, rout[idx],
+             layer_tols=_order_tolerances(wl, xb, params, yb, rg))
+    # the fused update over the whole 138M-parameter buffer: master and bf16 shadow
+    m, P = got["model"], got["P"]
+    master = m.pack(params, device(), torch.float32)
+    m.sgd_step(P, master, got["dparams"], wl.lr)
+    torch.cuda.synchronize()
+    for l, ((gW, gb), (mW, mb)) in enumerate(zip(m.unpack(P), m.unpack(master))):
+        (W0, b0), (rdW, rdb) = params[l], rg[l]
+        assert rel_l2(to_np(mW), oracle.sgd_f32(W0, rdW, wl.lr)) <= 1e-4
+        assert rel_l2(to_np(mb), oracle.sgd_f32(b0, rdb, wl.lr)) <= 1e-3
+        # the shadow is the round-to-nearest-even bf16 of the new master
+        assert torch.equal(gW, mW.to(torch.bfloat16))
+        assert torch.equal(gb, mb.to(torch.bfloat16))
+
+
+def test_bf16_storage_effect_against_exact_math():
+    """bf16 storage of the hidden activations changes the function itself.
+
+    The gate above compares against the network with those storage casts. Here
+    the same GPU gradient is compared with the exact function of the rounded
+    inputs (no activation casts): the difference is the effect of bf16 storage
+    and stays within a few percent on this network.
+    """
+    wl = workloads.WORKLOADS["c3"]
+    x, params, y = workloads.make_inputs(wl, bias_scale=0.1)
+    got = _run(wl, x, params, y, forward=False)
+    exact = oracle.MlpSpec(wl.widths, wl.acts, wl.loss, wl.dtype, storage_casts=False)
+    rl, rg, _ = oracle.mlp_gradient(exact, x, params, y)
+    assert abs(got["loss"] - rl) <= 1e-2 * abs(rl)
+    for l, ((gw, gb), (rw, rb)) in enumerate(zip(got["grads"], rg)):
+        assert rel_l2(gw, rw) <= 0.06, l
+        assert rel_l2(gb, rb) <= 0.06, l

@@ -531,10 +531,102 @@ def test_sgd_f32_is_correctly_rounded():
 def test_bf16_storage_quantises_inputs():
     wl = workloads.scaled(workloads.WORKLOADS["c3"], 64, batch=8)
     x, params, y = workloads.make_inputs(wl)
-    spec = MlpSpec(wl.widths, wl.acts, wl.loss, "bf16")
+    spec = MlpSpec(wl.widths, wl.acts, wl.loss, "bf16", storage_casts=False)
     spec32 = MlpSpec(wl.widths, wl.acts, wl.loss, "f32")
     xq = oracle.round_to_bf16(x)
     pq = [(oracle.round_to_bf16(W), oracle.round_to_bf16(b)) for W, b in params]
     l_bf, _ = oracle.mlp_forward(spec, x, params, y)
     l_q, _ = oracle.mlp_forward(spec32, xq.astype(np.float32), [(W.astype(np.float32), b.astype(np.float32)) for W, b in pq], y)
     assert l_bf == l_q
+
+
+# --------------------------------------------------------------------------
+# dataTypeCast to bf16 (Table 1): value rounding and straight-through adjoint
+# --------------------------------------------------------------------------
+def test_cast_value_matches_library_rounding():
+    import torch
+    v = np.random.default_rng(20).standard_normal((7, 9)) * 100
+    f = Function("c"); a = f.arg((7, 9)); f.ret(f.cast(a, "bf16"))
+    got, = evaluate(f, [v])
+    ref = torch.from_numpy(v.astype(np.float32)).to(torch.bfloat16).double().numpy()
+    np.testing.assert_array_equal(got, ref)
+
+
+def test_cast_adjoint_passes_straight_through():
+    rng = np.random.default_rng(21)
+    a0 = rng.standard_normal((4, 5)); w = rng.standard_normal((4, 5))
+    f = Function("c"); a = f.arg((4, 5)); wa = f.arg((4, 5))
+    f.ret(f.reduce("add", f.mul(f.cast(a, "bf16"), wa), None))
+    da, = evaluate(differentiate(f, [0]), [a0, w])
+    np.testing.assert_array_equal(da, w)
+
+
+def test_casts_vanish_on_bf16_representable_networks():
+    """Integer-valued ReLU network: every activation is exact in bf16, so the
+    network with storage casts and the one without compute the same values and
+    the same gradients, bit for bit."""
+    rng = np.random.default_rng(22)
+    spec_c = MlpSpec((6, 5, 4, 3), ("relu", "relu", "none"), "softmax_ce", "bf16")
+    spec_n = MlpSpec((6, 5, 4, 3), ("relu", "relu", "none"), "softmax_ce", "bf16",
+                     storage_casts=False)
+    x = rng.integers(-3, 4, (5, 6)).astype(np.float32)
+    params = [(rng.integers(-2, 3, (6, 5)).astype(np.float32), rng.integers(-1, 2, 5).astype(np.float32)),
+              (rng.integers(-2, 3, (5, 4)).astype(np.float32), rng.integers(-1, 2, 4).astype(np.float32)),
+              (rng.integers(-1, 2, (4, 3)).astype(np.float32) / 4, np.zeros(3, np.float32))]
+    y = np.array([0, 1, 2, 1, 0])
+    lc, gc, dxc = oracle.mlp_gradient(spec_c, x, params, y, wrt_x=True)
+    ln, gn, dxn = oracle.mlp_gradient(spec_n, x, params, y, wrt_x=True)
+    assert lc == ln
+    np.testing.assert_array_equal(dxc, dxn)
+    for (a, b), (c, d) in zip(gc, gn):
+        np.testing.assert_array_equal(a, c)
+        np.testing.assert_array_equal(b, d)
+
+
+def test_bf16_storage_network_against_torch_straight_through():
+    """torch float64 autograd with a straight-through bf16 rounding of each
+    hidden activation (h + (round(h) - h).detach()) computes the same function."""
+    import torch
+    wl = workloads.scaled(workloads.WORKLOADS["c5"], 64, batch=12)
+    x, params, y = workloads.make_inputs(wl, bias_scale=0.1)
+    spec = MlpSpec(wl.widths, wl.acts, wl.loss, "bf16")
+    loss, grads, dx = oracle.mlp_gradient(spec, x, params, y, wrt_x=True)
+
+    def q(a):
+        return torch.from_numpy(oracle.round_to_bf16(np.asarray(a, np.float32)))
+    xt = q(x).requires_grad_(True)
+    ps = [(q(W).requires_grad_(True), q(b).requires_grad_(True)) for W, b in params]
+    h = xt
+    for l, (W, b) in enumerate(ps):
+        h = h @ W + b
+        if l < len(ps) - 1:
+            h = torch.relu(h)
+            hr = h.detach().float().to(torch.bfloat16).double()
+            h = h + (hr - h).detach()
+    tl = torch.nn.functional.cross_entropy(h, torch.from_numpy(y.astype(np.int64)))
+    tl.backward()
+    assert abs(loss - tl.item()) < 1e-12 * abs(loss)
+    np.testing.assert_allclose(dx, xt.grad.numpy(), rtol=1e-9, atol=1e-15)
+    for (a, b), (W, bb) in zip(grads, ps):
+        np.testing.assert_allclose(a, W.grad.numpy(), rtol=1e-9, atol=1e-15)
+        np.testing.assert_allclose(b, bb.grad.numpy(), rtol=1e-9, atol=1e-15)
+
+
+def test_float32_accumulation_mode():
+    """accumulate="f32" changes only the accumulation precision of the forward dots:
+    on a float32 network (no casts) the two evaluations agree to float32 accuracy,
+    and the float32 dot equals a float32 library product."""
+    from dataclasses import replace
+    wl = workloads.scaled(workloads.WORKLOADS["c2"], 8, batch=16)
+    x, params, y = workloads.make_inputs(wl, bias_scale=0.1)
+    s64 = MlpSpec(wl.widths, wl.acts, wl.loss, "f32")
+    l64, g64, _ = oracle.mlp_gradient(s64, x, params, y)
+    l32, g32, _ = oracle.mlp_gradient(replace(s64, accumulate="f32"), x, params, y)
+    assert abs(l64 - l32) < 1e-5 * l64
+    for (a, b), (c, d) in zip(g64, g32):
+        assert np.linalg.norm(a - c) <= 1e-5 * np.linalg.norm(a)
+    f = Function("d"); A = f.arg((5, 7)); B = f.arg((7, 3)); f.ret(f.dot(A, B, "f32"))
+    rng = np.random.default_rng(23)
+    a, b = rng.standard_normal((5, 7)), rng.standard_normal((7, 3))
+    got, = evaluate(f, [a, b])
+    np.testing.assert_array_equal(got, (a.astype(np.float32) @ b.astype(np.float32)).astype(np.float64))
