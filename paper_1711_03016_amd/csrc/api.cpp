@@ -16,7 +16,7 @@
 #include <string>
 #include <vector>
 
-#include "../../include/dlvm.h"
+#include "dlvm.h"
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -187,14 +187,19 @@ LaunchInfo gemm_info(const GemmDesc& d) {
   static const char* lay[] = {"nn", "nt", "tn"};
   LaunchInfo i;
   i.name = std::string("gemm_") + lay[static_cast<int>(d.layout)] + (d.dtype == DLVM_F32 ? "_f32" : "_bf16");
-  i.M = d.M; i.N = d.N; i.K = d.K;
-  i.flops = 2.0 * double(d.M) * double(d.N) * double(d.K);
+  // Work of the unpadded problem: padding columns and padded contraction
+  // entries are zeros that the algorithm does not need.
+  const double M = double(d.M);
+  const double N = double(d.nvec > 0 && d.nvec < d.N ? d.nvec : d.N);
+  const double K = double(d.kvalid > 0 ? d.kvalid : d.K);
+  i.M = d.M; i.N = static_cast<int64_t>(N); i.K = static_cast<int64_t>(K);
+  i.flops = 2.0 * M * N * K;
   const double es = double(elem_size(d.dtype)), eo = double(elem_size(d.out_dtype));
-  double b = (double(d.M) * d.K + double(d.K) * d.N) * es + double(d.M) * d.N * eo;
-  if (d.bias) b += double(d.N) * es;
-  if (d.layout == Layout::NT && d.act != DLVM_ACT_NONE) b += double(d.M) * d.N * es;
-  if (d.residual) b += double(d.M) * d.N * eo;
-  if (d.colsum) b += double(d.N) * 4.0;
+  double b = (M * K + K * N) * es + M * N * eo;
+  if (d.bias) b += N * es;
+  if (d.layout == Layout::NT && d.act != DLVM_ACT_NONE) b += M * N * es;
+  if (d.residual) b += M * N * eo;
+  if (d.colsum) b += N * 4.0;
   i.bytes = b;
   return i;
 }
@@ -335,14 +340,16 @@ dlvm_status plan_gradient(const dlvm_model* m, const void* params, const void* x
         return st;
       if (l > 0) {
         void* dzp = at<void>(ws, w.dz[cur ^ 1]);
-        if ((st = run.gemm(gemm_nt(dt, dt, m->acts[l - 1], batch, Np, K, dzl, Np, P(2 * l), Np,
-                                   at<void>(ws, w.H[l]), nullptr, dzp))) != DLVM_OK)
-          return st;
+        GemmDesc d = gemm_nt(dt, dt, m->acts[l - 1], batch, Np, K, dzl, Np, P(2 * l), Np,
+                             at<void>(ws, w.H[l]), nullptr, dzp);
+        d.kvalid = N;
+        if ((st = run.gemm(d)) != DLVM_OK) return st;
         cur ^= 1;
       } else if (m->wrt_x) {
-        if ((st = run.gemm(gemm_nt(dt, DLVM_F32, DLVM_ACT_NONE, batch, Np, K, dzl, Np, P(0), Np,
-                                   nullptr, nullptr, dx))) != DLVM_OK)
-          return st;
+        GemmDesc d = gemm_nt(dt, DLVM_F32, DLVM_ACT_NONE, batch, Np, K, dzl, Np, P(0), Np, nullptr,
+                             nullptr, dx);
+        d.kvalid = N;
+        if ((st = run.gemm(d)) != DLVM_OK) return st;
       }
     }
   }

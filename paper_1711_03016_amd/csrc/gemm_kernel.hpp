@@ -81,15 +81,23 @@ __device__ __forceinline__ uint32_t perm_b32(uint32_t hi, uint32_t lo, uint32_t 
 //   KMAJ:  P[r * ld + k]   (k contiguous)
 //   !KMAJ: P[k * ld + r]   (r contiguous)
 // and lands in LDS segment (k / BK) % KSEG, row r, byte (k % BK) * sizeof(T).
-// A segment holds SEG_ROWS rows (the A and B tiles of one stage share it).
+//
+// load() only issues the global loads of the next stage; store() (after the
+// current stage has been multiplied) zeroes out-of-range chunks, transposes
+// r-contiguous blocks and writes LDS. With 16-byte loads every load is issued
+// unconditionally from a clamped, always valid address and its validity is
+// kept aside, so no branch and no consumer of the loaded registers sits
+// between the loads and the matrix-core work that hides their latency.
 template <typename T, bool KMAJ, int ROWS, int THREADS, bool VEC, int KSEG>
 struct TileLoader {
   static constexpr int VW = Elem<T>::VW;
   static constexpr int CH = kChunks * KSEG;  // 16-byte chunks of k per row and stage
   static constexpr int TASKS = KMAJ ? ROWS * CH : (ROWS / VW) * CH;
   static constexpr int PER_THREAD = (TASKS + THREADS - 1) / THREADS;
-  static constexpr int NREG = KMAJ ? PER_THREAD : PER_THREAD * VW;
-  uint32_t v[NREG][4];
+  static constexpr int NLOAD = KMAJ ? PER_THREAD : PER_THREAD * VW;  // 16-byte loads per thread
+  static_assert(NLOAD <= 32, "validity mask");
+  uint32_t raw[NLOAD][4];
+  uint32_t ok = 0;  // bit i: load i lies inside the operand
 
   // Task q -> (row or row block, chunk). K-contiguous operands put the chunk
   // index fastest (consecutive lanes read consecutive 16 bytes of a row);
@@ -107,8 +115,13 @@ struct TileLoader {
     }
   }
 
+  __device__ __forceinline__ void put(int i, const uint4& x) {
+    raw[i][0] = x.x; raw[i][1] = x.y; raw[i][2] = x.z; raw[i][3] = x.w;
+  }
+
   __device__ __forceinline__ void load(const T* __restrict__ P, int64_t ld, int64_t r0,
                                        int64_t rlim, int64_t k0, int64_t klim, int tid) {
+    ok = 0;
 #pragma unroll
     for (int i = 0; i < PER_THREAD; ++i) {
       const int q = tid + i * THREADS;
@@ -119,59 +132,40 @@ struct TileLoader {
         const int64_t gr = r0 + rb;
         const int64_t gk = k0 + c * VW;
         if constexpr (VEC) {
-          if (gr < rlim && gk < klim) {
-            const uint4 x = *reinterpret_cast<const uint4*>(P + gr * ld + gk);
-            v[i][0] = x.x; v[i][1] = x.y; v[i][2] = x.z; v[i][3] = x.w;
-          } else {
-            v[i][0] = v[i][1] = v[i][2] = v[i][3] = 0u;
-          }
+          const bool in = gr < rlim && gk < klim;
+          ok |= in ? (1u << i) : 0u;
+          put(i, *reinterpret_cast<const uint4*>(in ? P + gr * ld + gk : P));
         } else {
           T e[VW];
 #pragma unroll
           for (int j = 0; j < VW; ++j)
             e[j] = (gr < rlim && gk + j < klim) ? P[gr * ld + gk + j] : T(0);
           const uint32_t* w = reinterpret_cast<const uint32_t*>(e);
-          v[i][0] = w[0]; v[i][1] = w[1]; v[i][2] = w[2]; v[i][3] = w[3];
+          raw[i][0] = w[0]; raw[i][1] = w[1]; raw[i][2] = w[2]; raw[i][3] = w[3];
+          ok |= 1u << i;
         }
       } else {
         const int64_t gr = r0 + rb * VW;
         const int64_t gk = k0 + c * VW;
-        uint32_t raw[VW][4];  // raw[kk] = elements (gk + kk, gr .. gr + VW - 1)
 #pragma unroll
         for (int kk = 0; kk < VW; ++kk) {
           if constexpr (VEC) {
             // The whole 16-byte run lies inside row gk+kk (ld is a multiple of
             // the vector width); elements past rlim reach only outputs that
             // are not stored.
-            if (gr < rlim && gk + kk < klim) {
-              const uint4 x = *reinterpret_cast<const uint4*>(P + (gk + kk) * ld + gr);
-              raw[kk][0] = x.x; raw[kk][1] = x.y; raw[kk][2] = x.z; raw[kk][3] = x.w;
-            } else {
-              raw[kk][0] = raw[kk][1] = raw[kk][2] = raw[kk][3] = 0u;
-            }
+            const bool in = gr < rlim && gk + kk < klim;
+            ok |= in ? (1u << (i * VW + kk)) : 0u;
+            put(i * VW + kk, *reinterpret_cast<const uint4*>(in ? P + (gk + kk) * ld + gr : P));
           } else {
             T e[VW];
 #pragma unroll
             for (int j = 0; j < VW; ++j)
               e[j] = (gr + j < rlim && gk + kk < klim) ? P[(gk + kk) * ld + gr + j] : T(0);
             const uint32_t* w = reinterpret_cast<const uint32_t*>(e);
-            raw[kk][0] = w[0]; raw[kk][1] = w[1]; raw[kk][2] = w[2]; raw[kk][3] = w[3];
+            const int n = i * VW + kk;
+            raw[n][0] = w[0]; raw[n][1] = w[1]; raw[n][2] = w[2]; raw[n][3] = w[3];
+            ok |= 1u << n;
           }
-        }
-        if constexpr (sizeof(T) == 4) {
-          // 4x4 float32 transpose: output row j holds k = gk .. gk+3 of r = gr + j.
-#pragma unroll
-          for (int j = 0; j < 4; ++j)
-#pragma unroll
-            for (int kk = 0; kk < 4; ++kk) v[i * 4 + j][kk] = raw[kk][j];
-        } else {
-          // 8x8 bf16 transpose: output row j, dword p = (k = 2p, k = 2p+1) of r = gr + j.
-#pragma unroll
-          for (int j = 0; j < 8; ++j)
-#pragma unroll
-            for (int p = 0; p < 4; ++p)
-              v[i * 8 + j][p] = perm_b32(raw[2 * p + 1][j >> 1], raw[2 * p][j >> 1],
-                                         (j & 1) ? 0x07060302u : 0x05040100u);
         }
       }
     }
@@ -188,14 +182,39 @@ struct TileLoader {
       task(q, rb, c);
       char* base = lds + (c / kChunks) * SEG_BYTES + (c % kChunks) * 16;
       if constexpr (KMAJ) {
+        const bool o = (ok >> i) & 1u;
         *reinterpret_cast<uint4*>(base + rb * kRowStride) =
-            make_uint4(v[i][0], v[i][1], v[i][2], v[i][3]);
+            make_uint4(o ? raw[i][0] : 0u, o ? raw[i][1] : 0u, o ? raw[i][2] : 0u,
+                       o ? raw[i][3] : 0u);
       } else {
+        uint32_t w[VW][4];  // w[kk] = elements (k = kk, r = 0 .. VW-1) of the block
+#pragma unroll
+        for (int kk = 0; kk < VW; ++kk) {
+          const int n = i * VW + kk;
+          const bool o = (ok >> n) & 1u;
+          w[kk][0] = o ? raw[n][0] : 0u; w[kk][1] = o ? raw[n][1] : 0u;
+          w[kk][2] = o ? raw[n][2] : 0u; w[kk][3] = o ? raw[n][3] : 0u;
+        }
+        uint32_t t[VW][4];  // t[j] = row r = j of the block, its VW k values
+        if constexpr (sizeof(T) == 4) {
+          // 4x4 float32 transpose: a register renaming.
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int kk = 0; kk < 4; ++kk) t[j][kk] = w[kk][j];
+        } else {
+          // 8x8 bf16 transpose: row j, dword p = (k = 2p, k = 2p+1), by byte permutes.
+#pragma unroll
+          for (int j = 0; j < 8; ++j)
+#pragma unroll
+            for (int p = 0; p < 4; ++p)
+              t[j][p] = perm_b32(w[2 * p + 1][j >> 1], w[2 * p][j >> 1],
+                                 (j & 1) ? 0x07060302u : 0x05040100u);
+        }
 #pragma unroll
         for (int j = 0; j < VW; ++j)
           *reinterpret_cast<uint4*>(base + (rb * VW + j) * kRowStride) =
-              make_uint4(v[i * VW + j][0], v[i * VW + j][1], v[i * VW + j][2],
-                         v[i * VW + j][3]);
+              make_uint4(t[j][0], t[j][1], t[j][2], t[j][3]);
       }
     }
   }
@@ -290,7 +309,9 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void dlvm_gemm_kernel(Params p) 
     }
 #pragma unroll
     for (int g = 0; g < 4 * KSEG; ++g) {
-      if (g % WK != wk) continue;  // this group's k-steps
+      if constexpr (WK > 1) {
+        if (g % WK != wk) continue;  // this group's k-steps
+      }
       const char* As = stage + (g / 4) * SEG;
       const char* Bs = As + BM * kRowStride;
       const int cofs = (2 * (g % 4) + frag_half) * 16;

@@ -29,6 +29,7 @@ struct GemmDesc {
   float alpha;           // NN: scale of the product
   int64_t nvec;          // entries of bias / colsum (0 means N). Columns n >= nvec
                          // have none; with a padded operand they are zero.
+  int64_t kvalid;        // unpadded contraction extent, for work accounting (0 means K)
 };
 
 // How one product is launched: tile configuration and grid.

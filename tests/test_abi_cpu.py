@@ -1,0 +1,160 @@
+"""The C-ABI library on the host: it loads, exports every declared symbol, and
+its host-side logic (validation, layouts, plans, error paths) works without a
+device. No call here launches a kernel: every call either only computes on the
+host or fails validation before any HIP call.
+"""
+import ctypes
+import os
+
+import pytest
+
+import paper_1711_03016_amd as dl
+import workloads
+
+
+@pytest.fixture(scope="module", autouse=True)
+def built_library():
+    if not os.path.exists(dl.LIB_PATH):
+        from paper_1711_03016_amd import build
+        build.build()
+    dl.lib()
+
+
+def test_every_declared_function_is_exported():
+    names = dl.header_functions()
+    assert len(names) >= 20
+    missing = [n for n in names if not hasattr(dl.lib(), n)]
+    assert missing == []
+    for n in ("dlvm_forward", "dlvm_gradient", "dlvm_sgd_step"):
+        assert n in names
+
+
+def _desc(widths, acts, dtype=0, loss=0, wrt_x=0, batch_max=8):
+    L = len(widths) - 1
+    w = (ctypes.c_int32 * len(widths))(*widths)
+    a = (ctypes.c_int32 * max(L, 1))(*acts)
+    return dl._Desc(L, w, a, dtype, loss, wrt_x, batch_max), (w, a)
+
+
+@pytest.mark.parametrize("widths,acts,dtype,loss,wrt_x,batch_max,status", [
+    ((4, 3), (0,), 0, 0, 0, 8, dl.OK),
+    ((4, 3), (3,), 0, 0, 0, 8, dl.ERR_INVALID_ARG),        # last layer has an activation
+    ((4,), (), 0, 0, 0, 8, dl.ERR_INVALID_ARG),            # no layer
+    ((4, 0), (0,), 0, 0, 0, 8, dl.ERR_INVALID_ARG),        # zero width
+    ((4, 3), (0,), 7, 0, 0, 8, dl.ERR_INVALID_ARG),        # unknown dtype
+    ((4, 3), (0,), 0, 5, 0, 8, dl.ERR_INVALID_ARG),        # unknown loss
+    ((4, 3), (9,), 0, 0, 0, 8, dl.ERR_INVALID_ARG),        # unknown activation
+    ((4, 3), (0,), 0, 0, 0, 0, dl.ERR_INVALID_ARG),        # batch_max 0
+    ((4, 3), (0,), 0, 1, 1, 8, dl.ERR_UNSUPPORTED),        # chain needs in == out
+    ((4, 4), (0,), 1, 1, 1, 8, dl.ERR_UNSUPPORTED),        # chain is float32
+    ((4, 4), (0,), 0, 1, 0, 8, dl.ERR_UNSUPPORTED),        # chain differentiates x
+    ((4, 4, 4), (0, 0), 0, 1, 1, 8, dl.ERR_UNSUPPORTED),   # chain is one layer
+    ((4, 4), (0,), 0, 1, 1, 8, dl.OK),
+])
+def test_create_validates(widths, acts, dtype, loss, wrt_x, batch_max, status):
+    d, keep = _desc(widths, acts, dtype, loss, wrt_x, batch_max)
+    h = ctypes.c_void_p()
+    assert dl.lib().dlvm_create(ctypes.byref(d), ctypes.byref(h)) == status
+    if status == dl.OK:
+        dl.lib().dlvm_destroy(h)
+    else:
+        assert h.value is None
+        assert dl.lib().dlvm_last_error()
+
+
+@pytest.mark.parametrize("name", sorted(workloads.WORKLOADS))
+def test_layout_and_plan(name):
+    wl = workloads.WORKLOADS[name]
+    m = dl.Model(wl.widths, wl.acts, wl.dtype, wl.loss, wl.wrt_x, wl.batch)
+    offs, lds = m.param_layout_lds()
+    total = m.param_count()
+    es = 2 if wl.dtype == "bf16" else 4
+    prev_end = 0
+    for l in range(wl.n_layers):
+        K, N = wl.widths[l], wl.widths[l + 1]
+        ld = lds[l]
+        if wl.loss == "softmax_ce" and l == wl.n_layers - 1:
+            assert ld == (N + 7) // 8 * 8
+        else:
+            assert ld == N
+        for off, size in ((offs[2 * l], K * ld), (offs[2 * l + 1], N)):
+            assert off % 128 == 0 and (off * es) % 256 == 0   # 256-byte aligned tensors
+            assert off >= prev_end
+            prev_end = off + size
+    assert prev_end <= total
+    assert total - sum(wl.widths[l] * lds[l] + wl.widths[l + 1] for l in range(wl.n_layers)) < 128 * 2 * wl.n_layers
+    assert m.workspace_bytes(wl.batch) > 0
+    assert m.workspace_bytes(0) == 0
+    assert m.workspace_bytes(wl.batch + 1) == 0
+    plan = m.plan(wl.batch)
+    assert plan[-1]["name"].startswith("sgd")
+    # the launch plan's matrix work is exactly the workload's algorithmic flops
+    assert sum(p["flops"] for p in plan) == wl.flops()
+    # dead-code elimination: no input-gradient product for layer 1 unless x is differentiated
+    nt = [p for p in plan if p["name"].startswith("gemm_nt")]
+    assert len(nt) == wl.n_layers - 1 + (1 if wl.wrt_x else 0)
+
+
+def test_gradient_argument_errors_are_host_side():
+    L = dl.lib()
+    m = dl.Model((64, 32, 10), ("sigmoid", "none"), batch_max=16)
+    h = m._h
+    ws = m.workspace_bytes(16)
+    A = 0x100000  # never dereferenced: validation fails before any HIP call
+    # null pointers
+    assert L.dlvm_gradient(h, None, A, A, 16, A, A, None, A, ws, None) == dl.ERR_INVALID_ARG
+    assert L.dlvm_gradient(h, A, A, None, 16, A, A, None, A, ws, None) == dl.ERR_INVALID_ARG
+    # misaligned
+    assert L.dlvm_gradient(h, A + 4, A, A, 16, A, A, None, A, ws, None) == dl.ERR_MISALIGNED
+    # batch out of range
+    assert L.dlvm_gradient(h, A, A, A, 17, A, A, None, A, ws, None) == dl.ERR_INVALID_ARG
+    assert L.dlvm_gradient(h, A, A, A, 0, A, A, None, A, ws, None) == dl.ERR_INVALID_ARG
+    # workspace
+    assert L.dlvm_gradient(h, A, A, A, 16, A, A, None, A, ws - 1, None) == dl.ERR_WORKSPACE
+    assert L.dlvm_gradient(h, A, A, A, 16, A, A, None, None, ws, None) == dl.ERR_WORKSPACE
+    assert b"workspace" in L.dlvm_last_error()
+    # forward
+    assert L.dlvm_forward(h, A, A, 16, None, A, ws, None) == dl.ERR_INVALID_ARG
+    assert L.dlvm_forward(h, A, A, 16, A, A, 0, None) == dl.ERR_WORKSPACE
+    # sgd
+    assert L.dlvm_sgd_step(h, None, None, A, 0.1, None) == dl.ERR_INVALID_ARG
+    assert L.dlvm_sgd_step(h, A + 2, None, A, 0.1, None) == dl.ERR_MISALIGNED
+    mb = dl.Model((8, 8), ("none",), "bf16", batch_max=4)
+    assert L.dlvm_sgd_step(mb._h, A, None, A, 0.1, None) == dl.ERR_INVALID_ARG  # master needed
+    # wrt_x requires dx; the chain requires no labels but dx
+    mx = dl.Model((8, 8), ("none",), wrt_x=True, batch_max=4)
+    w2 = mx.workspace_bytes(4)
+    assert L.dlvm_gradient(mx._h, A, A, A, 4, A, A, None, A, w2, None) == dl.ERR_INVALID_ARG
+    mc = dl.Model((8, 8), ("none",), "f32", "chain8", True, 4)
+    w3 = mc.workspace_bytes(4)
+    assert L.dlvm_gradient(mc._h, A, A, None, 4, A, A, None, A, w3, None) == dl.ERR_INVALID_ARG
+
+
+def test_step_level_errors_are_host_side():
+    L = dl.lib()
+    A = 0x100000
+    assert L.dlvm_dense_forward(0, 1, 0, 4, 4, 4, 1.0, A, A, None, A, None) == dl.ERR_UNSUPPORTED
+    assert L.dlvm_dense_forward(0, 0, 0, 0, 4, 4, 1.0, A, A, None, A, None) == dl.ERR_INVALID_ARG
+    assert L.dlvm_dense_forward(0, 0, 0, 4, 4, 4, 1.0, A + 8, A, None, A, None) == dl.ERR_MISALIGNED
+    assert L.dlvm_dense_backward_data(0, 0, 1, 4, 4, 4, A, A, None, None, A, None) == dl.ERR_INVALID_ARG
+    assert L.dlvm_dense_backward_params(3, 4, 4, 4, A, A, A, None, None) == dl.ERR_INVALID_ARG
+    assert L.dlvm_softmax_xent(0, 4, 10, A, A, 0.25, A, A, A, 0, None) == dl.ERR_WORKSPACE
+    assert L.dlvm_chain8(4, 4, A, A, A, A, None, A, A, 1 << 20, None) == dl.ERR_INVALID_ARG
+    assert L.dlvm_sgd(1, 16, A, None, A, 0.1, None) == dl.ERR_INVALID_ARG
+    assert L.dlvm_softmax_xent_ws_bytes(0) == 0 and L.dlvm_softmax_xent_ws_bytes(5) > 0
+    assert L.dlvm_chain8_ws_bytes(3, 0) == 0 and L.dlvm_chain8_ws_bytes(3, 5) > 0
+
+
+def test_probe_arguments_are_validated():
+    L = dl.lib()
+    m = dl.Model((8, 8), ("none",), batch_max=4)
+    assert L.dlvm_probe_arm(m._h, -2, 4) == dl.ERR_INVALID_ARG
+    assert L.dlvm_probe_arm(m._h, 0, 0) == dl.ERR_INVALID_ARG
+    n = ctypes.c_int64()
+    t = ctypes.c_double()
+    assert L.dlvm_probe_read(m._h, 0, ctypes.byref(n), ctypes.byref(t)) == dl.OK
+    assert n.value == 0
+    assert L.dlvm_probe_disarm(m._h) == dl.OK
+    info = dl.LaunchInfo()
+    assert L.dlvm_plan_entry(m._h, 4, 99, ctypes.byref(info)) == dl.ERR_INVALID_ARG
+    assert L.dlvm_plan_size(m._h, 5) == 0
