@@ -22,6 +22,13 @@
 
 using dlvm::GemmDesc;
 using dlvm::Layout;
+using dlvm::PacketEvents;
+using dlvm::packet_events;
+
+dlvm::PacketEvents& dlvm::packet_events() {
+  thread_local PacketEvents e;
+  return e;
+}
 
 // Events of the timing probe (see dlvm_probe_arm).
 struct ProbeState {
@@ -230,10 +237,10 @@ class Launcher {
     }
     ProbeState& p = m_->probe;
     const bool rec = p.armed && (p.index < 0 || p.index == idx) && p.used < p.capacity;
-    if (rec) (void)hipEventRecord(p.start[p.used], s_);
+    if (rec) packet_events() = PacketEvents{p.start[p.used], p.stop[p.used]};
     const hipError_t e = launch();
     if (rec) {
-      (void)hipEventRecord(p.stop[p.used], s_);
+      packet_events() = PacketEvents{};
       p.pos[p.used] = idx;
       ++p.used;
     }

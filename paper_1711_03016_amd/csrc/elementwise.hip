@@ -279,11 +279,11 @@ hipError_t launch_softmax_xent(int dtype, int64_t rows, int64_t classes, const f
   const int nb = softmax_xent_partials(rows);
   *n_partials = nb;
   if (dtype == F32)
-    hipLaunchKernelGGL(dlvm_softmax_xent_kernel<float>, dim3(nb), dim3(kBlock), 0, s, rows,
+    launch_kernel(dlvm_softmax_xent_kernel<float>, dim3(nb), dim3(kBlock), s, rows,
                        classes, logits, labels, scale, static_cast<float*>(dlogits), ld_dlogits,
                        partials, bad);
   else
-    hipLaunchKernelGGL(dlvm_softmax_xent_kernel<bf16_t>, dim3(nb), dim3(kBlock), 0, s, rows,
+    launch_kernel(dlvm_softmax_xent_kernel<bf16_t>, dim3(nb), dim3(kBlock), s, rows,
                        classes, logits, labels, scale, static_cast<bf16_t*>(dlogits), ld_dlogits,
                        partials, bad);
   return hipGetLastError();
@@ -307,17 +307,17 @@ hipError_t launch_chain8(int64_t rows, int64_t cols, const float* z, const float
   const float inv_n = static_cast<float>(1.0 / (static_cast<double>(rows) * static_cast<double>(cols)));
   if (vec) {
     if (fwd_only)
-      hipLaunchKernelGGL((dlvm_chain8_kernel<true, true>), dim3(nb), dim3(kBlock), 0, s, rows, cols,
+      launch_kernel((dlvm_chain8_kernel<true, true>), dim3(nb), dim3(kBlock), s, rows, cols,
                          z, bias, x_skip, zbar, xbar, partials, inv_n);
     else
-      hipLaunchKernelGGL((dlvm_chain8_kernel<true, false>), dim3(nb), dim3(kBlock), 0, s, rows,
+      launch_kernel((dlvm_chain8_kernel<true, false>), dim3(nb), dim3(kBlock), s, rows,
                          cols, z, bias, x_skip, zbar, xbar, partials, inv_n);
   } else {
     if (fwd_only)
-      hipLaunchKernelGGL((dlvm_chain8_kernel<false, true>), dim3(nb), dim3(kBlock), 0, s, rows,
+      launch_kernel((dlvm_chain8_kernel<false, true>), dim3(nb), dim3(kBlock), s, rows,
                          cols, z, bias, x_skip, zbar, xbar, partials, inv_n);
     else
-      hipLaunchKernelGGL((dlvm_chain8_kernel<false, false>), dim3(nb), dim3(kBlock), 0, s, rows,
+      launch_kernel((dlvm_chain8_kernel<false, false>), dim3(nb), dim3(kBlock), s, rows,
                          cols, z, bias, x_skip, zbar, xbar, partials, inv_n);
   }
   return hipGetLastError();
@@ -326,7 +326,7 @@ hipError_t launch_chain8(int64_t rows, int64_t cols, const float* z, const float
 hipError_t launch_finalize(const float* partials, const int32_t* bad, int n, float scale,
                            float* out, int32_t* flags, float* zero_base, const ZeroGaps& gaps,
                            hipStream_t s) {
-  hipLaunchKernelGGL(dlvm_finalize_kernel, dim3(1), dim3(kBlock), 0, s, partials, bad, n, scale,
+  launch_kernel(dlvm_finalize_kernel, dim3(1), dim3(kBlock), s, partials, bad, n, scale,
                      out, flags, zero_base, gaps);
   return hipGetLastError();
 }
@@ -335,10 +335,10 @@ hipError_t launch_sgd(int dtype, int64_t n, void* params, float* master, const f
                       float lr, hipStream_t s) {
   const unsigned nb = grid_for((n + 3) / 4, 4096);
   if (dtype == F32)
-    hipLaunchKernelGGL(dlvm_sgd_f32_kernel, dim3(nb), dim3(kBlock), 0, s, n,
+    launch_kernel(dlvm_sgd_f32_kernel, dim3(nb), dim3(kBlock), s, n,
                        static_cast<float*>(params), grads, lr);
   else
-    hipLaunchKernelGGL(dlvm_sgd_bf16_kernel, dim3(nb), dim3(kBlock), 0, s, n,
+    launch_kernel(dlvm_sgd_bf16_kernel, dim3(nb), dim3(kBlock), s, n,
                        static_cast<bf16_t*>(params), master, grads, lr);
   return hipGetLastError();
 }

@@ -1,5 +1,7 @@
 // Host side of the dense-layer products: choice of the tile configuration for
 // a given problem, and the launch.
+#include <cstdlib>
+
 #include "gemm_kernel.hpp"
 
 namespace dlvm {
@@ -13,23 +15,38 @@ constexpr double kRateF32 = 256.0;
 constexpr double kRateBF16 = 4096.0;
 constexpr double kL2BytesPerClock = 64.0;
 
-// Tile configurations of the kernel template (see gemm_kernel.hpp) with the
-// fraction of the matrix-core rate each sustains when not starved.
+// Tile configurations with the fraction of the matrix-core rate each sustains
+// when not starved. Configurations 0-4 are the register-staged kernel
+// (gemm_kernel.hpp), 10-13 the bf16 kernel with direct-to-LDS loads
+// (gemm_async.hpp).
 struct TileShape {
+  int cfg;
   int bm, bn;
   double eff;
+  bool async;
 };
-constexpr TileShape kTiles[5] = {
-    {128, 128, 0.8}, {64, 64, 0.6}, {128, 32, 0.6}, {32, 32, 0.5}, {64, 64, 0.65}};
+constexpr TileShape kTiles[] = {
+    {0, 128, 128, 0.8, false}, {1, 64, 64, 0.6, false},   {2, 128, 32, 0.6, false},
+    {3, 32, 32, 0.5, false},   {4, 64, 64, 0.65, false},  {10, 256, 256, 0.9, true},
+    {11, 256, 128, 0.7, true}, {12, 128, 128, 0.84, true}, {13, 256, 256, 0.85, true}};
 
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 bool aligned16(const void* q) { return (reinterpret_cast<uintptr_t>(q) & 15u) == 0; }
 
+// The direct-to-LDS kernel moves whole 16-byte chunks: bf16 operands with
+// 16-byte aligned bases, leading dimensions and contraction extent; its
+// epilogue moves 8 consecutive outputs at a time (16-byte aligned output rows,
+// saved activation and residual).
+bool async_ok(const GemmDesc& d) {
+  return d.dtype == BF16 && aligned16(d.A) && aligned16(d.B) && d.lda % 8 == 0 &&
+         d.ldb % 8 == 0 && d.K % 8 == 0 && d.ldc % 8 == 0 && aligned16(d.C) &&
+         aligned16(d.aux) && aligned16(d.residual) && aligned16(d.bias);
+}
+
 // Clock cycles one configuration needs: rounds of tiles over the compute
 // units, each tile bound by its matrix-core work or its operand traffic.
-double estimate(const GemmDesc& d, int cfg) {
-  const TileShape& t = kTiles[cfg];
+double estimate(const GemmDesc& d, const TileShape& t) {
   const int64_t tiles = ceil_div(d.M, t.bm) * ceil_div(d.N, t.bn);
   const double es = d.dtype == F32 ? 4.0 : 2.0;
   const double rate = (d.dtype == F32 ? kRateF32 : kRateBF16) * t.eff;
@@ -41,21 +58,39 @@ double estimate(const GemmDesc& d, int cfg) {
 
 }  // namespace
 
+// Tile configuration forced through the environment variable
+// DLVM_GEMM_CONFIG (for tests and tuning), or -1. A forced configuration that
+// cannot run the product is ignored.
+int forced_config() {
+  const char* v = std::getenv("DLVM_GEMM_CONFIG");
+  if (v == nullptr || *v == 0) return -1;
+  char* end = nullptr;
+  const long c = std::strtol(v, &end, 10);
+  return (end != nullptr && *end == 0) ? static_cast<int>(c) : -1;
+}
+
 GemmPlan plan_gemm(const GemmDesc& d) {
-  int best = 0;
+  const bool can_async = async_ok(d);
+  const int forced = forced_config();
+  const TileShape* best = nullptr;
   double best_t = 0.0;
-  for (int cfg = 0; cfg < 5; ++cfg) {
-    if (cfg == 2 && d.N > 32) continue;  // the narrow tile only for narrow outputs
-    const double t = estimate(d, cfg);
-    if (cfg == 0 || t < best_t * 0.97) {  // prefer earlier (larger) tiles on near ties
-      best = cfg;
-      best_t = t;
+  for (const TileShape& t : kTiles) {
+    if (t.cfg == 2 && d.N > 32) continue;  // the narrow tile only for narrow outputs
+    if (t.async && !can_async) continue;
+    if (t.cfg == forced) {
+      best = &t;
+      break;
+    }
+    const double e = estimate(d, t);
+    if (best == nullptr || e < best_t * 0.97) {  // prefer earlier (larger) tiles on near ties
+      best = &t;
+      best_t = e;
     }
   }
   GemmPlan pl{};
-  pl.cfg = best;
-  pl.bm = kTiles[best].bm;
-  pl.bn = kTiles[best].bn;
+  pl.cfg = best->cfg;
+  pl.bm = best->bm;
+  pl.bn = best->bn;
   pl.tiles_m = static_cast<int>(ceil_div(d.M, pl.bm));
   pl.tiles_n = static_cast<int>(ceil_div(d.N, pl.bn));
   return pl;

@@ -1,0 +1,499 @@
+// bf16 dense-layer products with asynchronous direct-to-LDS loads and an LDS
+// ring of STAGES k-tiles.
+//
+// Same products and fused epilogues as gemm_kernel.hpp (NN forward, NT adjoint
+// wrt the input, TN adjoint wrt the weights), for bf16 operands with 16-byte
+// aligned rows (every leading dimension and K a multiple of 8). Differences:
+//
+// * Global -> LDS with global_load_lds_dwordx4: one wave instruction moves
+//   64 x 16 bytes into one contiguous kilobyte of LDS without passing through
+//   registers, so several k-tiles are in flight while the matrix cores work on
+//   an earlier one. Each lane picks which 16-byte chunk of the operand it
+//   fetches so that the contiguous kilobyte holds the swizzled layout below.
+// * LDS layouts (no padding). A k-contiguous operand tile is ROWS rows of 128
+//   bytes (64 k); the 16-byte chunk c of row r sits in slot c ^ h(r). An
+//   m-contiguous (or n-contiguous) tile is 64 k-rows of 2*ROWS bytes; its
+//   32-byte column group g of k-row k sits in group g ^ f(k & 3). h and f make
+//   the fragment reads below free of bank conflicts whether the LDS serves 128
+//   or 256 bytes per clock.
+// * Fragments. A k-contiguous operand gives each lane its 8 consecutive k in
+//   one 16-byte LDS read. An m-contiguous operand is read with the transposing
+//   ds_read_b64_tr_b16: inside a group of 16 lanes, lane r points at 4
+//   consecutive elements (columns 4(r%4) .. 4(r%4)+3) of k-row r/4 and lane i
+//   receives the 4 k values of column i; two such reads give the 8 k of a
+//   fragment. The transposes of the adjoint products are thus done by the LDS
+//   read, not by registers and not in memory.
+// * Ragged edges. Rows or columns past M or N are loaded from a clamped valid
+//   address (they only reach outputs that are not stored). k past K is loaded
+//   from a clamped address and then zeroed in LDS before the last k-tile is
+//   multiplied.
+// * Tile order. Workgroups are dealt round-robin over the 8 XCDs; the tile
+//   index is remapped so that each XCD gets a contiguous range of tiles, and
+//   within a range tiles are visited in bands of 8 tile-rows, so workgroups
+//   running together on one XCD share A and B tiles in its L2.
+#pragma once
+
+#include "common.hpp"
+#include "kernels.hpp"
+#include "gemm_kernel.hpp"
+
+namespace dlvm {
+namespace gemm {
+
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+#define DLVM_LDS_PTR(p) ((__attribute__((address_space(3))) void*)(p))
+
+constexpr int kXcds = 8;
+
+// Tile (tm, tn) of workgroup `bid`.
+__device__ __forceinline__ void tile_of(int bid, int tiles_m, int tiles_n, int& tm, int& tn) {
+  const int nt = tiles_m * tiles_n;
+  int t = bid;
+  if (nt % kXcds == 0) t = (bid % kXcds) * (nt / kXcds) + bid / kXcds;
+  constexpr int GM = 8;
+  const int band = t / (GM * tiles_n);
+  const int first = band * GM;
+  const int rows = tiles_m - first < GM ? tiles_m - first : GM;
+  const int r = t - band * GM * tiles_n;
+  tm = first + r % rows;
+  tn = r / rows;
+}
+
+// Swizzle of a k-contiguous tile row: the 16-byte chunk c of row r sits in
+// slot c ^ kswz(r). Rows of 128 bytes (BK = 64) have 8 slots, rows of 64 bytes
+// (BK = 32) have 4.
+template <int BK>
+__device__ __forceinline__ int kswz(int r) {
+  if constexpr (BK == 64) return (r ^ (r >> 3)) & 7;
+  else return ((r >> 1) ^ (r >> 3)) & 3;
+}
+// Byte offset of 16-byte chunk c of row r in a k-contiguous tile.
+template <int BK>
+__device__ __forceinline__ int kmaj_off(int r, int c) {
+  return r * (2 * BK) + ((c ^ kswz<BK>(r)) << 4);
+}
+// Byte offset of 16-byte chunk c of k-row k in an m-contiguous tile of RB-byte rows.
+template <int RB>
+__device__ __forceinline__ int mmaj_off(int k, int c) {
+  const int q = k & 3;
+  return k * RB + ((c ^ ((q ^ ((q & 1) << 2)) << 1)) << 4);
+}
+
+// Element offset (from the operand base) of the 16-byte chunk that lane `lane`
+// of wave instruction `kb` fetches for the k-tile starting at k0. Rows past
+// rlim and k past klim are clamped to valid addresses.
+template <bool KMAJ, int ROWS, int BK>
+__device__ __forceinline__ int64_t chunk_src(int kb, int lane, int64_t ld, int64_t r0, int64_t rlim,
+                                             int64_t k0, int64_t klim) {
+  const int b = kb * 1024 + lane * 16;  // byte of this lane inside the tile
+  if constexpr (KMAJ) {
+    constexpr int RBK = 2 * BK;
+    const int r = b / RBK;
+    const int c = ((b % RBK) >> 4) ^ kswz<BK>(r);
+    int64_t gr = r0 + r;
+    int64_t gk = k0 + c * 8;
+    gr = gr < rlim ? gr : rlim - 1;
+    gk = gk < klim ? gk : 0;
+    return gr * ld + gk;
+  } else {
+    constexpr int RB = ROWS * 2;
+    const int k = b / RB;
+    const int q = k & 3;
+    const int c = ((b % RB) >> 4) ^ ((q ^ ((q & 1) << 2)) << 1);
+    int64_t gk = k0 + k;
+    int64_t gr = r0 + c * 8;
+    gk = gk < klim ? gk : k0;
+    gr = gr < rlim ? gr : 0;
+    return gk * ld + gr;
+  }
+}
+
+template <bool KMAJ, int ROWS, int BK, int NWAVES>
+__device__ __forceinline__ void async_tile(const bf16_t* __restrict__ P, int64_t ld, int64_t r0,
+                                           int64_t rlim, int64_t k0, int64_t klim, char* lds,
+                                           int wave, int lane) {
+  constexpr int KB = ROWS * 2 * BK / 1024;  // wave instructions per tile
+  static_assert(KB % NWAVES == 0, "tile split over waves");
+#pragma unroll
+  for (int j = 0; j < KB / NWAVES; ++j) {
+    const int kb = wave * (KB / NWAVES) + j;
+    const bf16_t* src = P + chunk_src<KMAJ, ROWS, BK>(kb, lane, ld, r0, rlim, k0, klim);
+    __builtin_amdgcn_global_load_lds(src, DLVM_LDS_PTR(lds + kb * 1024), 16, 0, 0);
+  }
+}
+
+// Zero the k >= kv part of a tile (last k-tile of a ragged K; kv % 8 == 0).
+template <bool KMAJ, int ROWS, int BK, int THREADS>
+__device__ __forceinline__ void zero_k_tail(char* lds, int kv, int tid) {
+  const uint4 z = make_uint4(0u, 0u, 0u, 0u);
+  if constexpr (KMAJ) {
+    constexpr int KC = BK / 8;
+    for (int q = tid; q < ROWS * KC; q += THREADS) {
+      const int r = q / KC, c = q % KC;
+      if (c * 8 >= kv) *reinterpret_cast<uint4*>(lds + kmaj_off<BK>(r, c)) = z;
+    }
+  } else {
+    constexpr int RB = ROWS * 2;
+    for (int q = kv * (RB / 16) + tid; q < BK * (RB / 16); q += THREADS)
+      *reinterpret_cast<uint4*>(lds + q * 16) = z;  // whole k-rows: the swizzle does not matter
+  }
+}
+
+// Fragment (8 k per lane) of the 32-row block at `row0` for k-step s (16 k).
+template <bool KMAJ, int ROWS, int BK>
+__device__ __forceinline__ bf16x8 frag(const char* lds, int row0, int s, int lane) {
+  if constexpr (KMAJ) {
+    const int r = row0 + (lane & 31);
+    const int c = 2 * s + (lane >> 5);
+    return *reinterpret_cast<const bf16x8*>(lds + kmaj_off<BK>(r, c));
+  } else {
+    constexpr int RB = ROWS * 2;
+    const int g = lane >> 4, r = lane & 15;
+    const int col = row0 + 16 * (g & 1) + 4 * (r & 3);
+    const int k = 16 * s + 8 * (g >> 1) + (r >> 2);
+    const int in16 = (col & 7) * 2;
+    const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (__attribute__((address_space(3))) v4i16*)(lds + mmaj_off<RB>(k, col >> 3) + in16));
+    const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (__attribute__((address_space(3))) v4i16*)(lds + mmaj_off<RB>(k + 4, col >> 3) + in16));
+    const v4i16 v8[2] = {lo, hi};
+    return __builtin_bit_cast(bf16x8, v8);
+  }
+}
+
+// Wait until at most N vector-memory operations of this wave are outstanding.
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+template <int LOADS, int MAXA>
+__device__ __forceinline__ void wait_stage(int ahead) {
+  if constexpr (MAXA >= 3) { if (ahead >= 3) { wait_vm<3 * LOADS>(); return; } }
+  if constexpr (MAXA >= 2) { if (ahead == 2) { wait_vm<2 * LOADS>(); return; } }
+  if constexpr (MAXA >= 1) { if (ahead == 1) { wait_vm<LOADS>(); return; } }
+  wait_vm<0>();
+}
+
+// Barrier between the waves of the workgroup that waits for nothing itself
+// (the callers wait for exactly what must have landed), plus a compiler-only
+// fence so that no LDS access is moved across it.
+__device__ __forceinline__ void barrier_only() {
+  __builtin_amdgcn_s_barrier();
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
+// One k-tile (BK k) of the wave's TM x TN blocks of 32 x 32. The operand
+// tiles come in through restrict parameters: the LDS reads then carry
+// alias-scope information, which tells the compiler that they do not depend on
+// the direct-to-LDS loads in flight into the other ring slots (the explicit
+// waits and barriers order the slot being read).
+//
+// With CS and do_cs, cs[j] also accumulates the B fragments of block column j:
+// lane l adds the 8 k values it holds of column l % 32, so that over all
+// k-tiles the two halves of the wave (lanes l and l + 32) hold complementary
+// partial column sums of B.
+template <bool AK, bool BKM, int BM, int BN, int BK, int TM, int TN, bool CS>
+__device__ __forceinline__ void mma_ktile(const char* __restrict__ As, const char* __restrict__ Bs,
+                                          int arow, int brow, int lane, f32x16 (&acc)[TM][TN],
+                                          float (&cs)[TN], bool do_cs) {
+#pragma unroll
+  for (int s = 0; s < BK / 16; ++s) {
+    bf16x8 af[TM], bfr[TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i) af[i] = frag<AK, BM, BK>(As, arow + i * 32, s, lane);
+#pragma unroll
+    for (int j = 0; j < TN; ++j) bfr[j] = frag<BKM, BN, BK>(Bs, brow + j * 32, s, lane);
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+    if constexpr (CS) {
+      if (do_cs) {
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          const uint4 w = __builtin_bit_cast(uint4, bfr[j]);
+          const uint32_t q[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            cs[j] += __uint_as_float(q[e] << 16);
+            cs[j] += __uint_as_float(q[e] & 0xffff0000u);
+          }
+        }
+      }
+    }
+  }
+}
+
+// Vector access to 8 consecutive elements (16 bytes of bf16, 32 of float32).
+__device__ __forceinline__ void load8(const bf16_t* p, float (&v)[8]) {
+  const uint4 w = *reinterpret_cast<const uint4*>(p);
+  const uint32_t q[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    v[2 * e] = __uint_as_float(q[e] << 16);
+    v[2 * e + 1] = __uint_as_float(q[e] & 0xffff0000u);
+  }
+}
+__device__ __forceinline__ void load8(const float* p, float (&v)[8]) {
+  const float4 a = *reinterpret_cast<const float4*>(p);
+  const float4 b = *reinterpret_cast<const float4*>(p + 4);
+  v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+  v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+}
+__device__ __forceinline__ void store8(bf16_t* p, const float (&v)[8]) {
+  uint32_t q[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e)
+    q[e] = static_cast<uint32_t>(f32_to_bf16(v[2 * e])) |
+           (static_cast<uint32_t>(f32_to_bf16(v[2 * e + 1])) << 16);
+  *reinterpret_cast<uint4*>(p) = make_uint4(q[0], q[1], q[2], q[3]);
+}
+__device__ __forceinline__ void store8(float* p, const float (&v)[8]) {
+  *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
+  *reinterpret_cast<float4*>(p + 4) = make_float4(v[4], v[5], v[6], v[7]);
+}
+
+// Epilogue of one row of a wave's 32 x 32 accumulator blocks (32 x WTN
+// outputs starting at (r0, c0)) through the wave's own LDS region: the
+// accumulators are written to LDS in row-major order, then every lane takes
+// chunks of 8 consecutive columns of one row, so the saved activation,
+// residual, bias and output move as 16-byte (bf16) or 32-byte (float32)
+// vectors, 8 lanes covering a row segment of WTN columns. Chunks that cross
+// the output's edge are done element by element. Requires ldc % 8 == 0 and
+// 16-byte aligned C, aux, residual and bias.
+template <typename TO, int EPI, int TN>
+__device__ __forceinline__ void epilogue_row(const Params& p, const f32x16 (&acc)[TN],
+                                             float* region, int64_t r0, int64_t c0, int lane) {
+  constexpr int WTN = TN * 32;
+  constexpr int LDF = WTN + 4;         // floats per LDS row (padding spreads the banks)
+  constexpr int CPR = WTN / 8;         // chunks per row
+  constexpr int CPL = 32 * CPR / 64;   // chunks per lane
+  constexpr int BATCH = 2;             // chunks whose loads are in flight together
+  static_assert(CPL % BATCH == 0, "chunk batches");
+  TO* __restrict__ C = static_cast<TO*>(p.C);
+  const bf16_t* __restrict__ aux = static_cast<const bf16_t*>(p.aux);
+  const TO* __restrict__ res = static_cast<const TO*>(p.residual);
+  const bf16_t* __restrict__ bias = static_cast<const bf16_t*>(p.bias);
+  const bool has_act = p.act != ACT_NONE;
+#pragma unroll
+  for (int j = 0; j < TN; ++j)
+#pragma unroll
+    for (int r = 0; r < 16; ++r)
+      region[(8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)) * LDF + j * 32 + (lane & 31)] = acc[j][r];
+  // The rows are read back by other lanes of the same wave: wait for the
+  // writes, and keep the compiler from moving the reads above them.
+  __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  for (int t0 = 0; t0 < CPL; t0 += BATCH) {
+    float x[BATCH][8], g[BATCH][8], rv[BATCH][8];
+    int64_t row[BATCH], col[BATCH];
+    bool full[BATCH];
+#pragma unroll
+    for (int b = 0; b < BATCH; ++b) {
+      const int q = lane + 64 * (t0 + b);
+      const int rr = q / CPR, cc = (q % CPR) * 8;
+      row[b] = r0 + rr;
+      col[b] = c0 + cc;
+      full[b] = row[b] < p.M && col[b] + 8 <= p.N;
+      const float4 lo = *reinterpret_cast<const float4*>(region + rr * LDF + cc);
+      const float4 hi = *reinterpret_cast<const float4*>(region + rr * LDF + cc + 4);
+      x[b][0] = lo.x; x[b][1] = lo.y; x[b][2] = lo.z; x[b][3] = lo.w;
+      x[b][4] = hi.x; x[b][5] = hi.y; x[b][6] = hi.z; x[b][7] = hi.w;
+      const int64_t idx = row[b] * p.ldc + col[b];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) { g[b][e] = 0.0f; rv[b][e] = 0.0f; }
+      if constexpr (EPI == EPI_STORE) {
+        if (bias != nullptr) {
+          if (col[b] + 8 <= p.nvec) {
+            load8(bias + col[b], g[b]);
+          } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+              if (col[b] + e < p.nvec) g[b][e] = bf16_to_f32(bias[col[b] + e]);
+          }
+        }
+      } else if constexpr (EPI == EPI_DACT) {
+        if (full[b]) {
+          if (has_act) load8(aux + idx, g[b]);
+          if (res != nullptr) load8(res + idx, rv[b]);
+        } else if (row[b] < p.M) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            if (col[b] + e < p.N) {
+              if (has_act) g[b][e] = bf16_to_f32(aux[idx + e]);
+              if (res != nullptr) rv[b][e] = load_as_f32<TO>(res + idx + e);
+            }
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int b = 0; b < BATCH; ++b) {
+      float v[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        v[e] = x[b][e];
+        if constexpr (EPI == EPI_STORE) {
+          v[e] = apply_act(p.act, p.alpha * v[e] + g[b][e]);
+        } else if constexpr (EPI == EPI_DACT) {
+          if (has_act) v[e] *= act_grad_from_output(p.act, g[b][e]);
+          v[e] += rv[b][e];
+        }
+      }
+      const int64_t idx = row[b] * p.ldc + col[b];
+      if (full[b]) {
+        store8(C + idx, v);
+      } else if (row[b] < p.M) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (col[b] + e < p.N) C[idx + e] = store_cast<TO>(v[e]);
+      }
+    }
+  }
+  // The region is written again for the next row: keep its reads above.
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
+// All TM rows of blocks, each with a statically indexed accumulator row.
+template <typename TO, int EPI, int TM, int TN, int I = 0>
+__device__ __forceinline__ void epilogue_lds(const Params& p, const f32x16 (&acc)[TM][TN],
+                                             float* region, int64_t r0, int64_t c0, int lane) {
+  if constexpr (I < TM) {
+    epilogue_row<TO, EPI, TN>(p, acc[I], region, r0 + 32 * I, c0, lane);
+    epilogue_lds<TO, EPI, TM, TN, I + 1>(p, acc, region, r0, c0, lane);
+  }
+}
+
+template <typename TO, bool AK, bool BKM, int BM, int BN, int BK, int WM, int WN, int STAGES,
+          int EPI>
+__global__ __launch_bounds__(64 * WM * WN) void dlvm_gemm_async_kernel(Params p) {
+  constexpr int NW = WM * WN;
+  constexpr int THREADS = 64 * NW;
+  constexpr int WTM = BM / WM, WTN = BN / WN;
+  constexpr int TM = WTM / 32, TN = WTN / 32;
+  constexpr int A_BYTES = BM * 2 * BK, B_BYTES = BN * 2 * BK;
+  constexpr int STAGE = A_BYTES + B_BYTES;
+  constexpr int LOADS = STAGE / 1024 / NW;  // direct loads per lane per k-tile
+  static_assert(BK == 32 || BK == 64, "k-tile depth");
+  static_assert(STAGES >= 2 && STAGES - 2 <= 3 && 3 * LOADS < 64, "pipeline depth");
+  static_assert(AK || BM >= 128, "m-contiguous tile needs 256-byte k-rows");
+  static_assert(BKM || BN >= 128, "n-contiguous tile needs 256-byte k-rows");
+  __shared__ __attribute__((aligned(1024))) char smem[STAGES * STAGE];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+  int tm, tn;
+  tile_of(static_cast<int>(blockIdx.x), p.tiles_m, p.tiles_n, tm, tn);
+  const int64_t m0 = static_cast<int64_t>(tm) * BM;
+  const int64_t n0 = static_cast<int64_t>(tn) * BN;
+  const bf16_t* __restrict__ A = static_cast<const bf16_t*>(p.A);
+  const bf16_t* __restrict__ B = static_cast<const bf16_t*>(p.B);
+  const int nk = static_cast<int>((p.K + BK - 1) / BK);
+  const int kv_last = static_cast<int>(p.K - static_cast<int64_t>(nk - 1) * BK);  // valid k of the last tile
+
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+  // Bias-gradient column sums (TN): taken from the B fragments by the waves
+  // of the first row of tiles that cover the first WTM rows.
+  float cs[TN];
+#pragma unroll
+  for (int j = 0; j < TN; ++j) cs[j] = 0.0f;
+  const bool do_colsum = (EPI == EPI_DW) && (p.colsum != nullptr) && (tm == 0) && (wm == 0);
+
+  auto issue = [&](int kt) {
+    char* st = smem + (kt % STAGES) * STAGE;
+    const int64_t k0 = static_cast<int64_t>(kt) * BK;
+    async_tile<AK, BM, BK, NW>(A, p.lda, m0, p.M, k0, p.K, st, wave, lane);
+    async_tile<BKM, BN, BK, NW>(B, p.ldb, n0, p.N, k0, p.K, st + A_BYTES, wave, lane);
+  };
+
+#pragma unroll
+  for (int s = 0; s < STAGES - 1; ++s)
+    if (s < nk) issue(s);
+
+  for (int kt = 0; kt < nk; ++kt) {
+    // Stage kt has landed once at most `ahead` later stages are outstanding.
+    const int left = nk - 1 - kt;
+    wait_stage<LOADS, STAGES - 2>(left < STAGES - 2 ? left : STAGES - 2);
+    barrier_only();
+    char* As = smem + (kt % STAGES) * STAGE;
+    char* Bs = As + A_BYTES;
+    if (kt == nk - 1 && kv_last < BK) {
+      zero_k_tail<AK, BM, BK, THREADS>(As, kv_last, tid);
+      zero_k_tail<BKM, BN, BK, THREADS>(Bs, kv_last, tid);
+      __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): the LDS writes are done
+      barrier_only();
+    }
+    // The slot refilled here was last read in iteration kt - 1, before the barrier.
+    if (kt + STAGES - 1 < nk) issue(kt + STAGES - 1);
+    mma_ktile<AK, BKM, BM, BN, BK, TM, TN, EPI == EPI_DW>(As, Bs, wm * WTM, wn * WTN, lane, acc,
+                                                          cs, do_colsum);
+  }
+
+  if constexpr (EPI == EPI_DACT) {
+    // The adjoint epilogue reads the saved activation (and a residual): it
+    // goes through a per-wave LDS region once every wave is done with the
+    // ring, so those reads and the stores move 8 consecutive columns at a time.
+    static_assert(NW * 32 * (WTN + 4) * 4 <= STAGES * STAGE, "epilogue staging fits the ring");
+    barrier_only();
+    epilogue_lds<TO, EPI, TM, TN>(p, acc, reinterpret_cast<float*>(smem) + wave * 32 * (WTN + 4),
+                                  m0 + wm * WTM, n0 + wn * WTN, lane);
+  } else {
+    // Stores only: straight from the accumulator registers, block by block.
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+        store_block<bf16_t, TO, EPI>(p, acc[i][j], m0 + wm * WTM + i * 32, n0 + wn * WTN + j * 32,
+                                     lane);
+  }
+  if constexpr (EPI == EPI_DW) {
+    if (do_colsum) {
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const float t = cs[j] + __shfl_xor(cs[j], 32);
+        const int64_t col = n0 + wn * WTN + j * 32 + lane;
+        if (lane < 32 && col < p.nvec) p.colsum[col] = t;
+      }
+    }
+  }
+}
+
+// Configurations (bf16): BM x BN tile, k-tile depth BK, WM x WN waves, LDS ring depth.
+//   10: 256 x 256, BK 64, 2 x 4 waves (128 x 64 per wave),  2 stages (128 KiB LDS)
+//   11: 256 x 128, BK 64, 2 x 2 waves (128 x 64 per wave),  3 stages (144 KiB LDS)
+//   12: 128 x 128, BK 64, 2 x 2 waves (64 x 64 per wave),   4 stages (128 KiB LDS)
+//   13: 256 x 256, BK 32, 2 x 4 waves (128 x 64 per wave),  4 stages (128 KiB LDS)
+constexpr int kAsyncFirst = 10;
+
+template <typename TO, bool AK, bool BKM, int EPI>
+hipError_t launch_async(const Params& p, int cfg, unsigned grid, hipStream_t s) {
+  switch (cfg) {
+    case 10:
+      launch_kernel((dlvm_gemm_async_kernel<TO, AK, BKM, 256, 256, 64, 2, 4, 2, EPI>), dim3(grid), dim3(512), s, p);
+      break;
+    case 11:
+      launch_kernel((dlvm_gemm_async_kernel<TO, AK, BKM, 256, 128, 64, 2, 2, 3, EPI>), dim3(grid), dim3(256), s, p);
+      break;
+    case 12:
+      launch_kernel((dlvm_gemm_async_kernel<TO, AK, BKM, 128, 128, 64, 2, 2, 4, EPI>), dim3(grid), dim3(256), s, p);
+      break;
+    default:
+      launch_kernel((dlvm_gemm_async_kernel<TO, AK, BKM, 256, 256, 32, 2, 4, 4, EPI>), dim3(grid), dim3(512), s, p);
+      break;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace gemm
+}  // namespace dlvm

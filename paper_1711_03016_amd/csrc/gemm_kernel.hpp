@@ -237,6 +237,70 @@ __device__ __forceinline__ void mfma_frag<bf16_t>(f32x16& acc, const uint4& a, c
                                                  __builtin_bit_cast(bf16x8, b), acc, 0, 0, 0);
 }
 
+// Epilogue of one 32 x 32 accumulator block whose first output is (r0, c0).
+// Accumulator register r of the block holds row 8*(r/4) + 4*(lane/32) + r%4
+// and column lane%32. A block that lies entirely inside the output takes an
+// unguarded path; the saved activation and residual of 8 registers are loaded
+// before their results are stored, so those loads are in flight together.
+template <typename T, typename TO, int EPI>
+__device__ __forceinline__ void store_block(const Params& p, const f32x16& acc, int64_t r0,
+                                            int64_t c0, int lane) {
+  const int64_t col = c0 + (lane & 31);
+  const int64_t rb = r0 + 4 * (lane >> 5);
+  const bool full = r0 + 32 <= p.M && c0 + 32 <= p.N;
+  const bool col_ok = col < p.N;
+  const int ld = static_cast<int>(p.ldc);
+  float bias_v = 0.0f;
+  if constexpr (EPI == EPI_STORE) {
+    if (p.bias != nullptr && col < p.nvec) bias_v = load_as_f32<T>(static_cast<const T*>(p.bias) + col);
+  }
+  const int64_t base = rb * p.ldc + col;  // element (rb, col); rows past M are never dereferenced
+  TO* __restrict__ C = static_cast<TO*>(p.C) + base;
+  const T* __restrict__ aux = static_cast<const T*>(p.aux);
+  const TO* __restrict__ res = static_cast<const TO*>(p.residual);
+  const bool has_act = p.act != ACT_NONE;
+  if (full) {
+#pragma unroll
+    for (int h = 0; h < 16; h += 8) {
+      float g[8], rv[8];
+      if constexpr (EPI == EPI_DACT) {
+#pragma unroll
+        for (int r = 0; r < 8; ++r) {
+          const int ro = 8 * ((h + r) >> 2) + (r & 3);
+          g[r] = has_act ? load_as_f32<T>(aux + base + ro * ld) : 0.0f;
+          rv[r] = res != nullptr ? load_as_f32<TO>(res + base + ro * ld) : 0.0f;
+        }
+      }
+#pragma unroll
+      for (int r = 0; r < 8; ++r) {
+        const int ro = 8 * ((h + r) >> 2) + (r & 3);
+        float v = acc[h + r];
+        if constexpr (EPI == EPI_STORE) {
+          v = apply_act(p.act, p.alpha * v + bias_v);
+        } else if constexpr (EPI == EPI_DACT) {
+          if (has_act) v *= act_grad_from_output(p.act, g[r]);
+          v += rv[r];
+        }
+        C[ro * ld] = store_cast<TO>(v);
+      }
+    }
+  } else if (col_ok) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int ro = 8 * (r >> 2) + (r & 3);
+      if (rb + ro >= p.M) continue;
+      float v = acc[r];
+      if constexpr (EPI == EPI_STORE) {
+        v = apply_act(p.act, p.alpha * v + bias_v);
+      } else if constexpr (EPI == EPI_DACT) {
+        if (has_act) v *= act_grad_from_output(p.act, load_as_f32<T>(aux + base + ro * ld));
+        if (res != nullptr) v += load_as_f32<TO>(res + base + ro * ld);
+      }
+      C[ro * ld] = store_cast<TO>(v);
+    }
+  }
+}
+
 template <typename T, typename TO, bool AK, bool BKM, int BM, int BN, int WM, int WN, int WK,
           int KSEG, bool VA, bool VB, int EPI>
 __global__ __launch_bounds__(64 * WM * WN * WK) void dlvm_gemm_kernel(Params p) {
@@ -400,36 +464,12 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void dlvm_gemm_kernel(Params p) 
     }
   }
 
-  // Epilogue. Accumulator register r of a 32x32 block holds row
-  // 8*(r/4) + 4*(lane/32) + r%4 and column lane%32 of the block.
-  TO* __restrict__ C = static_cast<TO*>(p.C);
+  // Epilogue.
 #pragma unroll
-  for (int j = 0; j < TN; ++j) {
-    const int64_t col = n0 + wn * WTN + j * 32 + (lane & 31);
-    const bool col_ok = col < p.N;
-    float bias_v = 0.0f;
-    if constexpr (EPI == EPI_STORE) {
-      if (p.bias != nullptr && col < p.nvec) bias_v = load_as_f32<T>(static_cast<const T*>(p.bias) + col);
-    }
+  for (int j = 0; j < TN; ++j)
 #pragma unroll
-    for (int i = 0; i < TM; ++i) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int64_t row = m0 + wm * WTM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-        if (!col_ok || row >= p.M) continue;
-        float v = acc[i][j][r];
-        const int64_t idx = row * p.ldc + col;
-        if constexpr (EPI == EPI_STORE) {
-          v = apply_act(p.act, p.alpha * v + bias_v);
-        } else if constexpr (EPI == EPI_DACT) {
-          if (p.act != ACT_NONE)
-            v *= act_grad_from_output(p.act, load_as_f32<T>(static_cast<const T*>(p.aux) + idx));
-          if (p.residual != nullptr) v += load_as_f32<TO>(static_cast<const TO*>(p.residual) + idx);
-        }
-        C[idx] = store_cast<TO>(v);
-      }
-    }
-  }
+    for (int i = 0; i < TM; ++i)
+      store_block<T, TO, EPI>(p, acc[i][j], m0 + wm * WTM + i * 32, n0 + wn * WTN + j * 32, lane);
   if constexpr (EPI == EPI_DW) {
     if (do_colsum) {
 #pragma unroll
@@ -452,24 +492,19 @@ template <typename T, typename TO, bool AK, bool BKM, bool VA, bool VB, int EPI>
 hipError_t launch_cfg(const Params& p, int cfg, unsigned grid, hipStream_t s) {
   switch (cfg) {
     case 0:
-      hipLaunchKernelGGL((dlvm_gemm_kernel<T, TO, AK, BKM, 128, 128, 2, 2, 1, 1, VA, VB, EPI>),
-                         dim3(grid), dim3(256), 0, s, p);
+      launch_kernel((dlvm_gemm_kernel<T, TO, AK, BKM, 128, 128, 2, 2, 1, 1, VA, VB, EPI>), dim3(grid), dim3(256), s, p);
       break;
     case 1:
-      hipLaunchKernelGGL((dlvm_gemm_kernel<T, TO, AK, BKM, 64, 64, 2, 2, 1, 2, VA, VB, EPI>),
-                         dim3(grid), dim3(256), 0, s, p);
+      launch_kernel((dlvm_gemm_kernel<T, TO, AK, BKM, 64, 64, 2, 2, 1, 2, VA, VB, EPI>), dim3(grid), dim3(256), s, p);
       break;
     case 2:
-      hipLaunchKernelGGL((dlvm_gemm_kernel<T, TO, AK, BKM, 128, 32, 4, 1, 1, 2, VA, VB, EPI>),
-                         dim3(grid), dim3(256), 0, s, p);
+      launch_kernel((dlvm_gemm_kernel<T, TO, AK, BKM, 128, 32, 4, 1, 1, 2, VA, VB, EPI>), dim3(grid), dim3(256), s, p);
       break;
     case 3:
-      hipLaunchKernelGGL((dlvm_gemm_kernel<T, TO, AK, BKM, 32, 32, 1, 1, 4, 4, VA, VB, EPI>),
-                         dim3(grid), dim3(256), 0, s, p);
+      launch_kernel((dlvm_gemm_kernel<T, TO, AK, BKM, 32, 32, 1, 1, 4, 4, VA, VB, EPI>), dim3(grid), dim3(256), s, p);
       break;
     default:
-      hipLaunchKernelGGL((dlvm_gemm_kernel<T, TO, AK, BKM, 64, 64, 2, 2, 2, 2, VA, VB, EPI>),
-                         dim3(grid), dim3(512), 0, s, p);
+      launch_kernel((dlvm_gemm_kernel<T, TO, AK, BKM, 64, 64, 2, 2, 2, 2, VA, VB, EPI>), dim3(grid), dim3(512), s, p);
       break;
   }
   return hipGetLastError();

@@ -1,6 +1,6 @@
 // Instantiations of the dense-layer product for the NT layout (adjoint with respect to the layer
 // input: activation-derivative epilogue).
-#include "gemm_kernel.hpp"
+#include "gemm_async.hpp"
 
 namespace dlvm {
 namespace gemm {
@@ -8,6 +8,10 @@ namespace gemm {
 hipError_t launch_nt(const Params& p, int dtype, int out_dtype, int cfg, unsigned grid, bool va,
                      bool vb, hipStream_t s) {
   if (dtype == F32) return launch_vec<float, float, true, true, EPI_DACT>(p, cfg, grid, va, vb, s);
+  if (cfg >= kAsyncFirst) {
+    if (out_dtype == F32) return launch_async<float, true, true, EPI_DACT>(p, cfg, grid, s);
+    return launch_async<bf16_t, true, true, EPI_DACT>(p, cfg, grid, s);
+  }
   if (out_dtype == F32) return launch_vec<bf16_t, float, true, true, EPI_DACT>(p, cfg, grid, va, vb, s);
   return launch_vec<bf16_t, bf16_t, true, true, EPI_DACT>(p, cfg, grid, va, vb, s);
 }

@@ -1,11 +1,31 @@
 // Host-side launch interface of the gfx950 kernels (internal to the library).
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 #include <stdint.h>
 
 namespace dlvm {
+
+// Timing events for the next kernel launches of the calling host thread. When
+// `start` is set, launch_kernel records both events from the kernel's own
+// dispatch packet (its begin and end on the GPU), so their difference is the
+// kernel's duration without the gap an event recorded beside the launch adds.
+struct PacketEvents {
+  hipEvent_t start = nullptr;
+  hipEvent_t stop = nullptr;
+};
+PacketEvents& packet_events();
+
+template <typename K, typename... Args>
+inline void launch_kernel(K kernel, dim3 grid, dim3 block, hipStream_t s, Args... args) {
+  const PacketEvents& e = packet_events();
+  if (e.start != nullptr)
+    hipExtLaunchKernelGGL(kernel, grid, block, 0, s, e.start, e.stop, 0, args...);
+  else
+    hipLaunchKernelGGL(kernel, grid, block, 0, s, args...);
+}
 
 enum class Layout : int {
   NN = 0,  // C = A.B        A [M,K] K-contiguous, B [K,N] N-contiguous (forward)
