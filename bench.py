@@ -44,6 +44,9 @@ def parse():
     ap.add_argument("--workload", default="c2", choices=sorted(workloads.WORKLOADS))
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="budget of the oracle CPU baseline (0 disables it)")
+    ap.add_argument("--graph", action="store_true",
+                    help="replay a captured step graph instead of enqueueing every step's "
+                         "launches from the host")
     ap.add_argument("--traffic", default=None,
                     help="JSON file with measured HBM bytes per launch of the dominant kernel")
     return ap.parse_args()
@@ -136,10 +139,16 @@ def main():
     dx = torch.empty((B, wl.widths[0]), device=dev) if wl.wrt_x else None
     stream = torch.cuda.current_stream()
 
-    def step():
+    def eager_step():
         m.gradient(P, xd, yd, B, loss, dP, dx, ws, stream)
         if wl.sgd:
             m.sgd_step(P, master, dP, wl.lr, stream)
+
+    # A step is the same launches either way; with --graph they are captured
+    # once into a HIP graph and replayed.
+    graph = None if not args.graph else m.step_graph(P, master, xd, yd, B, loss, dP, dx, ws,
+                                                 update=wl.sgd, lr=wl.lr)
+    step = eager_step if graph is None else (lambda: graph.launch(stream))
 
     for _ in range(warmup):
         step()
@@ -154,7 +163,7 @@ def main():
     probe_steps = 3
     m.probe_arm(-1, probe_steps * len(plan) + 8)
     for _ in range(probe_steps):
-        step()
+        eager_step()
     torch.cuda.synchronize()
     times = []
     for e in plan:
@@ -179,7 +188,7 @@ def main():
     torch.cuda.synchronize()
     t2 = time.perf_counter()
     for _ in range(steps):
-        step()
+        eager_step()
     torch.cuda.synchronize()
     t3 = time.perf_counter()
     n_dom, ms_dom = m.probe_read(dom["index"])
@@ -224,11 +233,12 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"{wl.name}: {wl.title}", "global_batch": B,
                    "widths": list(wl.widths), "loss": wl.loss, "parallelism": "none"},
+        "launch": "eager" if graph is None else "hip_graph",
         "tflops": round(tflops, 3),
         "mfma_frac": round(tflops / PEAK_TFLOPS[wl.dtype], 4),
         "roofline": roof,
     }
-    del P, master, xd, ws, dP, dx
+    del graph, P, master, xd, ws, dP, dx
     out["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
     print(json.dumps(out), flush=True)
 

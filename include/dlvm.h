@@ -24,7 +24,8 @@
  *   conditions (a label out of range, a non-finite loss) are latched in the
  *   workspace and reported by dlvm_check.
  * - No call allocates device memory or issues a memset, so the calls can be
- *   captured into a HIP graph.
+ *   captured into a HIP graph (dlvm_step_graph_create does so for a whole
+ *   training step).
  * - Results are deterministic: the same inputs give bitwise-identical outputs
  *   (fixed reduction orders, no floating-point atomics).
  * - No C++ exception crosses this interface. dlvm_last_error() returns a
@@ -131,6 +132,28 @@ dlvm_status dlvm_gradient(const dlvm_model* m, const void* params, const void* x
  * update the float32 `master` copy and write params = bf16(master). */
 dlvm_status dlvm_sgd_step(const dlvm_model* m, void* params, float* master,
                           const float* dparams, float lr, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Captured training step (HIP graph)
+ * ------------------------------------------------------------------------- */
+
+/* A training step recorded once and replayed: the launches of one
+ * dlvm_gradient call followed (if `update`) by those of one dlvm_sgd_step call
+ * with learning rate `lr`, captured into a HIP graph with the given device
+ * pointers baked in. Replaying it (dlvm_graph_launch) does exactly the work of
+ * those two calls on the same buffers, with a smaller per-launch cost; the
+ * caller refills x and labels in place between replays. Arguments and errors
+ * as for dlvm_gradient and dlvm_sgd_step; the timing probe must be disarmed.
+ * Capturing runs nothing on the device. The graph is owned by the caller
+ * (dlvm_graph_destroy) and must not outlive the model or the buffers. */
+typedef struct dlvm_graph dlvm_graph;
+dlvm_status dlvm_step_graph_create(const dlvm_model* m, void* params, float* master,
+                                   const void* x, const int32_t* labels, int64_t batch,
+                                   float* loss, float* dparams, float* dx, void* ws,
+                                   size_t ws_bytes, int32_t update, float lr, dlvm_graph** out);
+/* Enqueue one replay of the captured step on `stream`. */
+dlvm_status dlvm_graph_launch(dlvm_graph* g, void* stream);
+void dlvm_graph_destroy(dlvm_graph* g);
 
 /* Synchronise `stream` and read the device flags that the last gradient call
  * using `ws` wrote (every gradient call rewrites them): returns

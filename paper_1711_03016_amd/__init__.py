@@ -81,6 +81,10 @@ _SIGS = {
     "dlvm_probe_arm": (_I32, [_P, _I32, _I32]),
     "dlvm_probe_read": (_I32, [_P, _I32, ctypes.POINTER(_I64), ctypes.POINTER(ctypes.c_double)]),
     "dlvm_probe_disarm": (_I32, [_P]),
+    "dlvm_step_graph_create": (_I32, [_P, _P, _P, _P, _P, _I64, _P, _P, _P, _P, ctypes.c_size_t,
+                                      _I32, _F, ctypes.POINTER(_P)]),
+    "dlvm_graph_launch": (_I32, [_P, _P]),
+    "dlvm_graph_destroy": (None, [_P]),
 }
 
 
@@ -237,9 +241,36 @@ class Model:
     def probe_disarm(self) -> None:
         _check(lib().dlvm_probe_disarm(self._h))
 
+    def step_graph(self, params, master, x, labels, batch, loss, dparams, dx, ws,
+                   update: bool = False, lr: float = 0.0) -> "StepGraph":
+        """Capture one training step (gradient [+ SGD]) for replay (``dlvm_step_graph_create``)."""
+        g = _P()
+        _check(lib().dlvm_step_graph_create(self._h, _ptr(params), _ptr(master), _ptr(x),
+                                            _ptr(labels), int(batch), _ptr(loss), _ptr(dparams),
+                                            _ptr(dx), _ptr(ws), ws.numel() * ws.element_size(),
+                                            int(bool(update)), float(lr), ctypes.byref(g)))
+        return StepGraph(g, self)
+
     def check(self, ws, stream=None) -> int:
         """Status of the device flags (0, ERR_LABEL_RANGE or ERR_NONFINITE)."""
         return int(lib().dlvm_check(self._h, _ptr(ws), _stream(stream)))
+
+
+class StepGraph:
+    """A captured training step; ``launch()`` enqueues one replay."""
+
+    def __init__(self, handle, model):
+        self._g = handle
+        self._model = model  # the graph must not outlive the model
+
+    def launch(self, stream=None) -> None:
+        _check(lib().dlvm_graph_launch(self._g, _stream(stream)))
+
+    def __del__(self):
+        g = getattr(self, "_g", None)
+        if g is not None and g.value and _lib is not None:
+            _lib.dlvm_graph_destroy(g)
+            self._g = None
 
 
 # ---------------------------------------------------------------------------

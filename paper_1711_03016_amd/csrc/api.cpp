@@ -56,6 +56,11 @@ struct dlvm_model {
   mutable ProbeState probe;
 };
 
+struct dlvm_graph {
+  hipGraph_t graph = nullptr;
+  hipGraphExec_t exec = nullptr;
+};
+
 namespace {
 
 thread_local std::string g_last_error;
@@ -83,7 +88,8 @@ struct WsLayout {
   size_t bad = 0;           // int32 bad-label counts, one per loss partial
   std::vector<size_t> H;    // H[l], l = 1 .. L-1: saved layer outputs (storage dtype)
   size_t logits = 0;        // float32 [B, widths[L]] (logits, or z for the chain)
-  size_t dz[2] = {0, 0};    // adjoint ping-pong buffers (storage dtype; float32 for the chain)
+  std::vector<size_t> dz;   // dz[l], l = 0 .. L-1: adjoint of layer l's pre-activation output,
+                            // [B, ldw[l]] (storage dtype; float32 for the chain)
   size_t total = 0;
 };
 
@@ -106,13 +112,11 @@ WsLayout ws_layout(const dlvm_model* m, int64_t B) {
   }
   w.logits = off;
   off = align_up(off + static_cast<size_t>(B) * m->widths[m->L] * 4);
-  int64_t maxw = 0;
-  for (int l = 0; l <= m->L; ++l) maxw = std::max<int64_t>(maxw, m->widths[l]);
-  for (int l = 0; l < m->L; ++l) maxw = std::max<int64_t>(maxw, m->ldw[l]);
   const size_t dz_es = m->loss == DLVM_LOSS_CHAIN8 ? 4 : es;
-  for (int i = 0; i < 2; ++i) {
-    w.dz[i] = off;
-    off = align_up(off + static_cast<size_t>(B) * maxw * dz_es);
+  w.dz.assign(m->L, 0);
+  for (int l = 0; l < m->L; ++l) {
+    w.dz[l] = off;
+    off = align_up(off + static_cast<size_t>(B) * m->ldw[l] * dz_es);
   }
   w.total = off;
   return w;
@@ -221,12 +225,12 @@ LaunchInfo elementwise_info(const char* name, int64_t rows, int64_t cols, double
 
 // Every launch of the model-level calls goes through one Launcher. With a
 // plan vector it only records what it would launch (no pointer is touched);
-// otherwise it enqueues the launch, bracketed by the probe's events when the
-// probe is armed for this position.
+// otherwise it enqueues the launch on the caller's stream, bracketed by the
+// probe's events when the probe is armed for this position.
 class Launcher {
  public:
   Launcher(const dlvm_model* m, hipStream_t s, std::vector<LaunchInfo>* plan, int32_t first)
-      : m_(m), s_(s), plan_(plan), index_(first) {}
+      : m_(m), main_(s), plan_(plan), index_(first) {}
 
   template <class F>
   dlvm_status run(LaunchInfo info, F&& launch, const char* what) {
@@ -238,7 +242,7 @@ class Launcher {
     ProbeState& p = m_->probe;
     const bool rec = p.armed && (p.index < 0 || p.index == idx) && p.used < p.capacity;
     if (rec) packet_events() = PacketEvents{p.start[p.used], p.stop[p.used]};
-    const hipError_t e = launch();
+    const hipError_t e = launch(main_);
     if (rec) {
       packet_events() = PacketEvents{};
       p.pos[p.used] = idx;
@@ -252,15 +256,16 @@ class Launcher {
     const dlvm::GemmPlan pl = dlvm::plan_gemm(d);
     LaunchInfo info = gemm_info(d);
     info.name += "_" + std::to_string(pl.bm) + "x" + std::to_string(pl.bn) + "c" + std::to_string(pl.cfg);
-    return run(std::move(info), [&] { return dlvm::launch_gemm(d, pl, s_); }, "gemm launch");
+    return run(std::move(info), [&](hipStream_t st) { return dlvm::launch_gemm(d, pl, st); },
+               "gemm launch");
   }
 
-  hipStream_t stream() const { return s_; }
+  hipStream_t stream() const { return main_; }
   bool dry() const { return plan_ != nullptr; }
 
  private:
   const dlvm_model* m_;
-  hipStream_t s_;
+  hipStream_t main_;
   std::vector<LaunchInfo>* plan_;
   int32_t index_;
 };
@@ -279,12 +284,21 @@ dlvm_status plan_gradient(const dlvm_model* m, const void* params, const void* x
   int32_t* flags = at<int32_t>(ws, w.flags);
   auto P = [&](int idx) { return param_ptr(m, params, m->offsets[idx]); };
   auto G = [&](int idx) { return at<float>(dparams, static_cast<size_t>(m->offsets[idx]) * 4); };
-  hipStream_t s = run.stream();
   dlvm_status st = DLVM_OK;
   int np = 0;
   float scale = 1.0f;
+  const bool chain = m->loss == DLVM_LOSS_CHAIN8;
+  const int32_t* badp = chain ? nullptr : bad;
+  auto finalize = [&]() {
+    return run.run(elementwise_info("finalize", np, 1, 8.0 * np + 4.0),
+                   [&](hipStream_t s) {
+                     return dlvm::launch_finalize(partials, badp, np, scale, loss, flags, dparams,
+                                                  m->gaps, s);
+                   },
+                   "loss finalisation launch");
+  };
 
-  if (m->loss == DLVM_LOSS_CHAIN8) {
+  if (chain) {
     const int64_t N = m->widths[1], K = m->widths[0];
     float* z = at<float>(ws, w.logits);
     float* zbar = at<float>(ws, w.dz[0]);
@@ -292,8 +306,9 @@ dlvm_status plan_gradient(const dlvm_model* m, const void* params, const void* x
                                z, N))) != DLVM_OK)
       return st;
     np = dlvm::chain8_partials(batch, N);
+    scale = static_cast<float>(1.0 / (static_cast<double>(batch) * static_cast<double>(N)));
     st = run.run(elementwise_info("chain8", batch, N, 16.0 * double(batch) * N + 4.0 * N),
-                 [&] {
+                 [&](hipStream_t s) {
                    int n = 0;
                    return dlvm::launch_chain8(batch, N, z, static_cast<const float*>(P(1)),
                                               static_cast<const float*>(x), zbar, dx, partials,
@@ -306,78 +321,67 @@ dlvm_status plan_gradient(const dlvm_model* m, const void* params, const void* x
     if ((st = run.gemm(gemm_nt(dt, DLVM_F32, DLVM_ACT_NONE, batch, N, K, zbar, N, P(0), N, nullptr,
                                dx, dx))) != DLVM_OK)
       return st;
-    scale = static_cast<float>(1.0 / (static_cast<double>(batch) * static_cast<double>(N)));
-  } else {
-    // Forward, keeping every layer output.
-    const void* h = x;
-    for (int l = 0; l < L; ++l) {
-      const bool last = l == L - 1;
-      const int64_t N = m->widths[l + 1];
-      void* dst = last ? at<void>(ws, w.logits) : at<void>(ws, w.H[l + 1]);
-      if ((st = run.gemm(gemm_nn(dt, last ? DLVM_F32 : dt, m->acts[l], batch, N, m->widths[l], 1.0f,
-                                 h, P(2 * l), m->ldw[l], P(2 * l + 1), dst, N))) != DLVM_OK)
-        return st;
-      h = dst;
-    }
-    const int64_t C = m->widths[L];
-    const int64_t ldc = m->ldw[L - 1];  // dZ_L rows are padded like W_L's
-    scale = static_cast<float>(1.0 / static_cast<double>(batch));
-    void* dz = at<void>(ws, w.dz[0]);
-    np = dlvm::softmax_xent_partials(batch);
-    st = run.run(elementwise_info("softmax_xent", batch, C,
-                                  double(batch) * C * (4.0 + es) + 4.0 * batch),
-                 [&] {
-                   int n = 0;
-                   return dlvm::launch_softmax_xent(dt, batch, C, at<float>(ws, w.logits), labels,
-                                                    scale, dz, ldc, partials, bad, &n, s);
-                 },
-                 "softmax cross-entropy launch");
-    if (st != DLVM_OK) return st;
-    // Adjoint sweep, last layer first.
-    int cur = 0;
-    // On the padded class columns dZ_L and W_L are zero, so the products run
-    // over the padded width and the padding columns of dW_L come out zero.
-    for (int l = L - 1; l >= 0; --l) {
-      const void* hin = l == 0 ? x : at<void>(ws, w.H[l]);
-      const int64_t K = m->widths[l], N = m->widths[l + 1];
-      const int64_t Np = m->ldw[l];  // padded width (== N except the last layer)
-      void* dzl = at<void>(ws, w.dz[cur]);
-      if ((st = run.gemm(gemm_tn(dt, batch, Np, K, hin, dzl, Np, G(2 * l), Np, G(2 * l + 1), N))) !=
-          DLVM_OK)
-        return st;
-      if (l > 0) {
-        void* dzp = at<void>(ws, w.dz[cur ^ 1]);
-        GemmDesc d = gemm_nt(dt, dt, m->acts[l - 1], batch, Np, K, dzl, Np, P(2 * l), Np,
-                             at<void>(ws, w.H[l]), nullptr, dzp);
-        d.kvalid = N;
-        if ((st = run.gemm(d)) != DLVM_OK) return st;
-        cur ^= 1;
-      } else if (m->wrt_x) {
-        GemmDesc d = gemm_nt(dt, DLVM_F32, DLVM_ACT_NONE, batch, Np, K, dzl, Np, P(0), Np, nullptr,
-                             nullptr, dx);
-        d.kvalid = N;
-        if ((st = run.gemm(d)) != DLVM_OK) return st;
-      }
+    return finalize();
+  }
+
+  // Forward, keeping every layer output.
+  const void* h = x;
+  for (int l = 0; l < L; ++l) {
+    const bool last = l == L - 1;
+    const int64_t N = m->widths[l + 1];
+    void* dst = last ? at<void>(ws, w.logits) : at<void>(ws, w.H[l + 1]);
+    if ((st = run.gemm(gemm_nn(dt, last ? DLVM_F32 : dt, m->acts[l], batch, N, m->widths[l], 1.0f,
+                               h, P(2 * l), m->ldw[l], P(2 * l + 1), dst, N))) != DLVM_OK)
+      return st;
+    h = dst;
+  }
+  const int64_t C = m->widths[L];
+  const int64_t ldc = m->ldw[L - 1];  // dZ_L rows are padded like W_L's
+  scale = static_cast<float>(1.0 / static_cast<double>(batch));
+  np = dlvm::softmax_xent_partials(batch);
+  st = run.run(elementwise_info("softmax_xent", batch, C, double(batch) * C * (4.0 + es) + 4.0 * batch),
+               [&](hipStream_t s) {
+                 int n = 0;
+                 return dlvm::launch_softmax_xent(dt, batch, C, at<float>(ws, w.logits), labels,
+                                                  scale, at<void>(ws, w.dz[L - 1]), ldc, partials,
+                                                  bad, &n, s);
+               },
+               "softmax cross-entropy launch");
+  if (st != DLVM_OK) return st;
+  // Adjoint sweep, last layer first. On the padded class columns dZ_L and W_L
+  // are zero, so the products run over the padded width and the padding
+  // columns of dW_L come out zero.
+  for (int l = L - 1; l >= 0; --l) {
+    const void* hin = l == 0 ? x : at<void>(ws, w.H[l]);
+    const int64_t K = m->widths[l], N = m->widths[l + 1];
+    const int64_t Np = m->ldw[l];  // padded width (== N except the last layer)
+    void* dzl = at<void>(ws, w.dz[l]);
+    if ((st = run.gemm(gemm_tn(dt, batch, Np, K, hin, dzl, Np, G(2 * l), Np, G(2 * l + 1), N))) !=
+        DLVM_OK)
+      return st;
+    if (l > 0) {
+      GemmDesc d = gemm_nt(dt, dt, m->acts[l - 1], batch, Np, K, dzl, Np, P(2 * l), Np,
+                           at<void>(ws, w.H[l]), nullptr, at<void>(ws, w.dz[l - 1]));
+      d.kvalid = N;
+      if ((st = run.gemm(d)) != DLVM_OK) return st;
+    } else if (m->wrt_x) {
+      GemmDesc d = gemm_nt(dt, DLVM_F32, DLVM_ACT_NONE, batch, Np, K, dzl, Np, P(0), Np, nullptr,
+                           nullptr, dx);
+      d.kvalid = N;
+      if ((st = run.gemm(d)) != DLVM_OK) return st;
     }
   }
-  const int32_t* badp = m->loss == DLVM_LOSS_CHAIN8 ? nullptr : bad;
-  return run.run(elementwise_info("finalize", np, 1, 8.0 * np + 4.0),
-                 [&] {
-                   return dlvm::launch_finalize(partials, badp, np, scale, loss, flags, dparams,
-                                                m->gaps, s);
-                 },
-                 "loss finalisation launch");
+  return finalize();
 }
 
-// The launches of one forward call: nothing is kept, two ping-pong buffers
-// hold the layer outputs.
+// The launches of one forward call: nothing is kept; layer l's output goes to
+// the adjoint buffer of layer l (unused by a forward call).
 dlvm_status plan_forward(const dlvm_model* m, const void* params, const void* x, int64_t batch,
                          float* out, void* ws, Launcher& run) {
   const WsLayout w = ws_layout(m, batch);
   dlvm_status st = DLVM_OK;
   const int L = m->L;
   const int dt = m->dtype;
-  hipStream_t s = run.stream();
   if (m->loss == DLVM_LOSS_CHAIN8) {
     const int64_t N = m->widths[1];
     float* z = at<float>(ws, w.logits);
@@ -386,7 +390,7 @@ dlvm_status plan_forward(const dlvm_model* m, const void* params, const void* x,
       return st;
     const float* bias = static_cast<const float*>(param_ptr(m, params, m->offsets[1]));
     return run.run(elementwise_info("chain8_forward", batch, N, 12.0 * double(batch) * N + 4.0 * N),
-                   [&] {
+                   [&](hipStream_t s) {
                      int n = 0;
                      return dlvm::launch_chain8(batch, N, z, bias, static_cast<const float*>(x),
                                                 out, nullptr, at<float>(ws, w.partials), true, &n, s);
@@ -396,7 +400,7 @@ dlvm_status plan_forward(const dlvm_model* m, const void* params, const void* x,
   const void* h = x;
   for (int l = 0; l < L; ++l) {
     const bool last = l == L - 1;
-    void* dst = last ? static_cast<void*>(out) : at<void>(ws, w.dz[l & 1]);
+    void* dst = last ? static_cast<void*>(out) : at<void>(ws, w.dz[l]);
     if ((st = run.gemm(gemm_nn(dt, last ? DLVM_F32 : dt, m->acts[l], batch, m->widths[l + 1],
                                m->widths[l], 1.0f, h, param_ptr(m, params, m->offsets[2 * l]),
                                m->ldw[l], param_ptr(m, params, m->offsets[2 * l + 1]), dst,
@@ -534,9 +538,12 @@ dlvm_status dlvm_forward(const dlvm_model* m, const void* params, const void* x,
   return plan_forward(m, params, x, batch, out, ws, run);
 }
 
-dlvm_status dlvm_gradient(const dlvm_model* m, const void* params, const void* x,
-                          const int32_t* labels, int64_t batch, float* loss, float* dparams,
-                          float* dx, void* ws, size_t ws_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+dlvm_status check_gradient_args(const dlvm_model* m, const void* params, const void* x,
+                                const int32_t* labels, int64_t batch, float* loss,
+                                float* dparams, float* dx, void* ws, size_t ws_bytes) {
   if (m == nullptr || params == nullptr || x == nullptr || loss == nullptr || dparams == nullptr)
     return fail(DLVM_ERR_INVALID_ARG, "null argument");
   if (m->loss == DLVM_LOSS_SOFTMAX_CE && labels == nullptr)
@@ -547,25 +554,109 @@ dlvm_status dlvm_gradient(const dlvm_model* m, const void* params, const void* x
     return fail(DLVM_ERR_MISALIGNED, "device pointers must be 16-byte aligned");
   dlvm_status st = check_batch(m, batch);
   if (st != DLVM_OK) return st;
-  if ((st = check_ws(m, batch, ws, ws_bytes)) != DLVM_OK) return st;
-  Launcher run(m, static_cast<hipStream_t>(stream), nullptr, 0);
-  return plan_gradient(m, params, x, labels, batch, loss, dparams, dx, ws, run);
+  return check_ws(m, batch, ws, ws_bytes);
 }
 
-dlvm_status dlvm_sgd_step(const dlvm_model* m, void* params, float* master, const float* dparams,
-                          float lr, void* stream) {
+dlvm_status check_sgd_args(const dlvm_model* m, void* params, float* master, const float* dparams) {
   if (m == nullptr || params == nullptr || dparams == nullptr)
     return fail(DLVM_ERR_INVALID_ARG, "null argument");
   if (m->dtype == DLVM_BF16 && master == nullptr)
     return fail(DLVM_ERR_INVALID_ARG, "bf16 models need float32 master weights");
   if (!aligned16(params) || !aligned16(dparams) || (master && !aligned16(master)))
     return fail(DLVM_ERR_MISALIGNED, "device pointers must be 16-byte aligned");
-  hipStream_t s = static_cast<hipStream_t>(stream);
+  return DLVM_OK;
+}
+
+dlvm_status enqueue_sgd(const dlvm_model* m, void* params, float* master, const float* dparams,
+                        float lr, hipStream_t s) {
   Launcher run(m, s, nullptr, m->n_grad_launches);
   float* mst = m->dtype == DLVM_BF16 ? master : nullptr;
   return run.run(sgd_info(m),
-                 [&] { return dlvm::launch_sgd(m->dtype, m->param_count, params, mst, dparams, lr, s); },
+                 [&](hipStream_t st) {
+                   return dlvm::launch_sgd(m->dtype, m->param_count, params, mst, dparams, lr, st);
+                 },
                  "sgd launch");
+}
+}  // namespace
+
+extern "C" {
+
+dlvm_status dlvm_gradient(const dlvm_model* m, const void* params, const void* x,
+                          const int32_t* labels, int64_t batch, float* loss, float* dparams,
+                          float* dx, void* ws, size_t ws_bytes, void* stream) {
+  dlvm_status st = check_gradient_args(m, params, x, labels, batch, loss, dparams, dx, ws, ws_bytes);
+  if (st != DLVM_OK) return st;
+  Launcher run(m, static_cast<hipStream_t>(stream), nullptr, 0);
+  return plan_gradient(m, params, x, labels, batch, loss, dparams, dx, ws, run);
+}
+
+dlvm_status dlvm_sgd_step(const dlvm_model* m, void* params, float* master, const float* dparams,
+                          float lr, void* stream) {
+  const dlvm_status st = check_sgd_args(m, params, master, dparams);
+  if (st != DLVM_OK) return st;
+  return enqueue_sgd(m, params, master, dparams, lr, static_cast<hipStream_t>(stream));
+}
+
+dlvm_status dlvm_step_graph_create(const dlvm_model* m, void* params, float* master,
+                                   const void* x, const int32_t* labels, int64_t batch,
+                                   float* loss, float* dparams, float* dx, void* ws,
+                                   size_t ws_bytes, int32_t update, float lr, dlvm_graph** out) {
+  if (out == nullptr) return fail(DLVM_ERR_INVALID_ARG, "null argument");
+  *out = nullptr;
+  dlvm_status st = check_gradient_args(m, params, x, labels, batch, loss, dparams, dx, ws, ws_bytes);
+  if (st != DLVM_OK) return st;
+  if (update && (st = check_sgd_args(m, params, master, dparams)) != DLVM_OK) return st;
+  if (m->probe.armed)
+    return fail(DLVM_ERR_UNSUPPORTED, "disarm the timing probe before capturing a step");
+  hipStream_t cs = nullptr;
+  hipError_t e = hipStreamCreateWithFlags(&cs, hipStreamNonBlocking);
+  if (e != hipSuccess) return hip_fail(e, "creating the capture stream");
+  dlvm_graph* g = new (std::nothrow) dlvm_graph();
+  if (g == nullptr) {
+    (void)hipStreamDestroy(cs);
+    return fail(DLVM_ERR_INVALID_ARG, "out of host memory");
+  }
+  e = hipStreamBeginCapture(cs, hipStreamCaptureModeThreadLocal);
+  if (e != hipSuccess) {
+    delete g;
+    (void)hipStreamDestroy(cs);
+    return hip_fail(e, "beginning the capture");
+  }
+  {
+    Launcher run(m, cs, nullptr, 0);
+    st = plan_gradient(m, params, x, labels, batch, loss, dparams, dx, ws, run);
+  }
+  if (st == DLVM_OK && update) st = enqueue_sgd(m, params, master, dparams, lr, cs);
+  const std::string err = st == DLVM_OK ? std::string() : g_last_error;
+  e = hipStreamEndCapture(cs, &g->graph);
+  if (st == DLVM_OK && e != hipSuccess) st = hip_fail(e, "ending the capture");
+  if (st == DLVM_OK) {
+    e = hipGraphInstantiate(&g->exec, g->graph, nullptr, nullptr, 0);
+    if (e != hipSuccess) st = hip_fail(e, "instantiating the step graph");
+  } else if (!err.empty()) {
+    g_last_error = err;
+  }
+  (void)hipStreamDestroy(cs);
+  if (st != DLVM_OK) {
+    dlvm_graph_destroy(g);
+    return st;
+  }
+  *out = g;
+  return DLVM_OK;
+}
+
+dlvm_status dlvm_graph_launch(dlvm_graph* g, void* stream) {
+  if (g == nullptr || g->exec == nullptr) return fail(DLVM_ERR_INVALID_ARG, "null graph");
+  const hipError_t e = hipGraphLaunch(g->exec, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "launching the step graph");
+  return DLVM_OK;
+}
+
+void dlvm_graph_destroy(dlvm_graph* g) {
+  if (g == nullptr) return;
+  if (g->exec) (void)hipGraphExecDestroy(g->exec);
+  if (g->graph) (void)hipGraphDestroy(g->graph);
+  delete g;
 }
 
 int32_t dlvm_plan_size(const dlvm_model* m, int64_t batch) {

@@ -27,6 +27,23 @@ __device__ __forceinline__ bf16_t f32_to_bf16(float f) {
   return static_cast<bf16_t>(u >> 16);
 }
 
+// Streaming 16-byte and 8-byte accesses that bypass cache retention
+// (nontemporal): for data touched exactly once per pass.
+typedef float f32v4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32v2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ float4 load_nt(const float4* p) {
+  const f32v4 v = __builtin_nontemporal_load(reinterpret_cast<const f32v4*>(p));
+  return make_float4(v.x, v.y, v.z, v.w);
+}
+__device__ __forceinline__ void store_nt(float4* p, const float4& v) {
+  f32v4 w = {v.x, v.y, v.z, v.w};
+  __builtin_nontemporal_store(w, reinterpret_cast<f32v4*>(p));
+}
+__device__ __forceinline__ void store_nt(uint2* p, const uint2& v) {
+  u32v2 w = {v.x, v.y};
+  __builtin_nontemporal_store(w, reinterpret_cast<u32v2*>(p));
+}
+
 template <typename T> __device__ __forceinline__ float load_as_f32(const T* p);
 template <> __device__ __forceinline__ float load_as_f32<float>(const float* p) { return *p; }
 template <> __device__ __forceinline__ float load_as_f32<bf16_t>(const bf16_t* p) {

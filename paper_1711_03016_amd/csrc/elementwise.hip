@@ -102,6 +102,103 @@ __global__ __launch_bounds__(kBlock) void dlvm_softmax_xent_kernel(
   }
 }
 
+// Rows whose logits and dlogits move as 16-byte float32 chunks (classes and
+// the dlogits row stride multiples of 4, aligned bases) and fit in registers:
+// lane l of the row's wavefront holds chunks l, l + 64, ... (NCH of them), so
+// each logit is read from memory once and exponentiated once. The maximum and
+// the sum of exponentials are wavefront butterflies (fixed order).
+template <typename TD>
+__device__ __forceinline__ void store4(TD* p, float a, float b, float c, float d);
+template <>
+__device__ __forceinline__ void store4<float>(float* p, float a, float b, float c, float d) {
+  *reinterpret_cast<float4*>(p) = make_float4(a, b, c, d);
+}
+template <>
+__device__ __forceinline__ void store4<bf16_t>(bf16_t* p, float a, float b, float c, float d) {
+  uint2 o;
+  o.x = static_cast<uint32_t>(f32_to_bf16(a)) | (static_cast<uint32_t>(f32_to_bf16(b)) << 16);
+  o.y = static_cast<uint32_t>(f32_to_bf16(c)) | (static_cast<uint32_t>(f32_to_bf16(d)) << 16);
+  *reinterpret_cast<uint2*>(p) = o;
+}
+
+template <typename TD, int NCH>
+__global__ __launch_bounds__(kBlock) void dlvm_softmax_xent_rows_kernel(
+    int64_t rows, int64_t C, const float* __restrict__ Z, const int32_t* __restrict__ labels,
+    float scale, TD* __restrict__ dZ, int64_t ld_dz, float* __restrict__ partials,
+    int32_t* __restrict__ bad) {
+  __shared__ float red[kWaves];
+  __shared__ int32_t nbad[kWaves];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t row = static_cast<int64_t>(blockIdx.x) * kWaves + wave;
+  float li = 0.0f;
+  int32_t badrow = 0;
+  if (row < rows) {
+    const int64_t C4 = C / 4;
+    const float4* __restrict__ z4 = reinterpret_cast<const float4*>(Z + row * C);
+    const int32_t y = labels[row];
+    float4 v[NCH];
+    float m = -INFINITY;
+    float zy = 0.0f;  // the label's logit, held by exactly one lane
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      const int64_t j = lane + 64 * c;
+      v[c] = j < C4 ? load_nt(z4 + j) : make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
+      m = fmaxf(m, fmaxf(fmaxf(v[c].x, v[c].y), fmaxf(v[c].z, v[c].w)));
+      const int64_t k = 4 * j;
+      zy = k == y ? v[c].x : k + 1 == y ? v[c].y : k + 2 == y ? v[c].z : k + 3 == y ? v[c].w : zy;
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+      m = fmaxf(m, __shfl_xor(m, o, 64));
+      zy += __shfl_xor(zy, o, 64);  // one nonzero term: exact
+    }
+    float s = 0.0f;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      v[c].x = __expf(v[c].x - m);
+      v[c].y = __expf(v[c].y - m);
+      v[c].z = __expf(v[c].z - m);
+      v[c].w = __expf(v[c].w - m);
+      s += (v[c].x + v[c].y) + (v[c].z + v[c].w);
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) s += __shfl_xor(s, o, 64);
+    const bool ok = y >= 0 && y < C;
+    badrow = ok ? 0 : 1;
+    li = ok ? (m + __logf(s)) - zy : NAN;
+    const float ps = scale / s;
+    TD* d = dZ + row * ld_dz;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      const int64_t j = lane + 64 * c;
+      if (j < C4) {
+        const int64_t k = 4 * j;
+        store4<TD>(d + k, ps * v[c].x - (k == y ? scale : 0.0f),
+                   ps * v[c].y - (k + 1 == y ? scale : 0.0f),
+                   ps * v[c].z - (k + 2 == y ? scale : 0.0f),
+                   ps * v[c].w - (k + 3 == y ? scale : 0.0f));
+      }
+    }
+    for (int64_t j = C + lane; j < ld_dz; j += 64) d[j] = store_cast<TD>(0.0f);
+  }
+  if (lane == 0) {
+    red[wave] = li;
+    nbad[wave] = badrow;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float t = 0.0f;
+    int32_t b = 0;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+      t += red[w];
+      b += nbad[w];
+    }
+    partials[blockIdx.x] = t;
+    bad[blockIdx.x] = b;
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Eight-operator chain, forward and adjoint in one pass. With L the mean of
 // e^2 over rows*cols elements the seed of e is known before the reduction,
@@ -110,6 +207,7 @@ __global__ __launch_bounds__(kBlock) void dlvm_softmax_xent_kernel(
 //   ebar = 2 e / (rows cols), xbar = ebar s, zbar = ebar x s (1 - s) (1/2) (1 - a^2)
 // ---------------------------------------------------------------------------
 constexpr int kChainBlocks = 2048;
+constexpr int kChainUnroll = 4;
 
 __device__ __forceinline__ float chain_elem(float z, float b, float x, float inv_n, bool fwd_only,
                                             float& zbar, float& xbar, float& e_out) {
@@ -135,6 +233,8 @@ __global__ __launch_bounds__(kBlock) void dlvm_chain8_kernel(
   float acc = 0.0f;
   const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
   if constexpr (VEC) {
+    // kChainUnroll 16-byte chunks of each operand per thread and iteration,
+    // loads first; z and x_skip are read once (nontemporal).
     const int64_t n4 = rows * cols / 4;
     const int64_t c4 = cols / 4;
     const float4* z4 = reinterpret_cast<const float4*>(z);
@@ -142,18 +242,35 @@ __global__ __launch_bounds__(kBlock) void dlvm_chain8_kernel(
     const float4* b4 = reinterpret_cast<const float4*>(bias);
     float4* zb4 = reinterpret_cast<float4*>(zbar);
     float4* xb4 = reinterpret_cast<float4*>(xbar);
-    for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < n4; i += stride) {
-      const float4 zv = z4[i], xv = x4[i], bv = b4[i % c4];
-      float4 zo, xo, eo;
-      acc += chain_elem(zv.x, bv.x, xv.x, inv_n, FWD_ONLY, zo.x, xo.x, eo.x);
-      acc += chain_elem(zv.y, bv.y, xv.y, inv_n, FWD_ONLY, zo.y, xo.y, eo.y);
-      acc += chain_elem(zv.z, bv.z, xv.z, inv_n, FWD_ONLY, zo.z, xo.z, eo.z);
-      acc += chain_elem(zv.w, bv.w, xv.w, inv_n, FWD_ONLY, zo.w, xo.w, eo.w);
-      if constexpr (FWD_ONLY) {
-        zb4[i] = eo;
-      } else {
-        zb4[i] = zo;
-        xb4[i] = xo;
+    constexpr int64_t kStep = int64_t(kBlock) * kChainUnroll;
+    for (int64_t base = static_cast<int64_t>(blockIdx.x) * kStep + threadIdx.x; base < n4;
+         base += static_cast<int64_t>(gridDim.x) * kStep) {
+      float4 zv[kChainUnroll], xv[kChainUnroll];
+#pragma unroll
+      for (int u = 0; u < kChainUnroll; ++u) {
+        const int64_t i = base + u * kBlock;
+        if (i < n4) {
+          zv[u] = load_nt(z4 + i);
+          xv[u] = load_nt(x4 + i);
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < kChainUnroll; ++u) {
+        const int64_t i = base + u * kBlock;
+        if (i < n4) {
+          const float4 bv = b4[i % c4];
+          float4 zo, xo, eo;
+          acc += chain_elem(zv[u].x, bv.x, xv[u].x, inv_n, FWD_ONLY, zo.x, xo.x, eo.x);
+          acc += chain_elem(zv[u].y, bv.y, xv[u].y, inv_n, FWD_ONLY, zo.y, xo.y, eo.y);
+          acc += chain_elem(zv[u].z, bv.z, xv[u].z, inv_n, FWD_ONLY, zo.z, xo.z, eo.z);
+          acc += chain_elem(zv[u].w, bv.w, xv[u].w, inv_n, FWD_ONLY, zo.w, xo.w, eo.w);
+          if constexpr (FWD_ONLY) {
+            zb4[i] = eo;
+          } else {
+            zb4[i] = zo;
+            xb4[i] = xo;
+          }
+        }
       }
     }
   } else {
@@ -209,25 +326,47 @@ __global__ __launch_bounds__(kBlock) void dlvm_finalize_kernel(const float* __re
 
 // ---------------------------------------------------------------------------
 // SGD over a flat buffer: w <- w - lr * g (fused multiply-add, one rounding).
+// Each thread moves kSgdUnroll 16-byte chunks of every operand per iteration,
+// all loads issued before the first store, so that enough bytes are in flight
+// to keep HBM busy; the chunks of one wave instruction are contiguous. Every
+// byte is touched once, so the accesses are nontemporal.
 // ---------------------------------------------------------------------------
+constexpr int kSgdUnroll = 4;
+constexpr int64_t kSgdChunk = int64_t(kBlock) * kSgdUnroll;  // float4 per block iteration
+
+__device__ __forceinline__ float4 sgd4(float4 w, float4 g, float lr) {
+  w.x = fmaf(-lr, g.x, w.x);
+  w.y = fmaf(-lr, g.y, w.y);
+  w.z = fmaf(-lr, g.z, w.z);
+  w.w = fmaf(-lr, g.w, w.w);
+  return w;
+}
+
 __global__ __launch_bounds__(kBlock) void dlvm_sgd_f32_kernel(int64_t n, float* __restrict__ w,
                                                               const float* __restrict__ g,
                                                               float lr) {
   const int64_t n4 = n / 4;
-  const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
-  float4* w4 = reinterpret_cast<float4*>(w);
-  const float4* g4 = reinterpret_cast<const float4*>(g);
-  for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < n4; i += stride) {
-    float4 a = w4[i];
-    const float4 b = g4[i];
-    a.x = fmaf(-lr, b.x, a.x);
-    a.y = fmaf(-lr, b.y, a.y);
-    a.z = fmaf(-lr, b.z, a.z);
-    a.w = fmaf(-lr, b.w, a.w);
-    w4[i] = a;
+  float4* __restrict__ w4 = reinterpret_cast<float4*>(w);
+  const float4* __restrict__ g4 = reinterpret_cast<const float4*>(g);
+  for (int64_t base = static_cast<int64_t>(blockIdx.x) * kSgdChunk + threadIdx.x; base < n4;
+       base += static_cast<int64_t>(gridDim.x) * kSgdChunk) {
+    float4 a[kSgdUnroll], b[kSgdUnroll];
+#pragma unroll
+    for (int u = 0; u < kSgdUnroll; ++u) {
+      const int64_t i = base + u * kBlock;
+      if (i < n4) {
+        a[u] = load_nt(w4 + i);
+        b[u] = load_nt(g4 + i);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kSgdUnroll; ++u) {
+      const int64_t i = base + u * kBlock;
+      if (i < n4) store_nt(w4 + i, sgd4(a[u], b[u], lr));
+    }
   }
   for (int64_t i = n4 * 4 + static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < n;
-       i += stride)
+       i += static_cast<int64_t>(gridDim.x) * kBlock)
     w[i] = fmaf(-lr, g[i], w[i]);
 }
 
@@ -236,25 +375,35 @@ __global__ __launch_bounds__(kBlock) void dlvm_sgd_bf16_kernel(int64_t n, bf16_t
                                                                const float* __restrict__ g,
                                                                float lr) {
   const int64_t n4 = n / 4;
-  const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
-  float4* m4 = reinterpret_cast<float4*>(master);
-  const float4* g4 = reinterpret_cast<const float4*>(g);
-  uint2* w4 = reinterpret_cast<uint2*>(w);
-  for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < n4; i += stride) {
-    float4 a = m4[i];
-    const float4 b = g4[i];
-    a.x = fmaf(-lr, b.x, a.x);
-    a.y = fmaf(-lr, b.y, a.y);
-    a.z = fmaf(-lr, b.z, a.z);
-    a.w = fmaf(-lr, b.w, a.w);
-    m4[i] = a;
-    uint2 o;
-    o.x = static_cast<uint32_t>(f32_to_bf16(a.x)) | (static_cast<uint32_t>(f32_to_bf16(a.y)) << 16);
-    o.y = static_cast<uint32_t>(f32_to_bf16(a.z)) | (static_cast<uint32_t>(f32_to_bf16(a.w)) << 16);
-    w4[i] = o;
+  float4* __restrict__ m4 = reinterpret_cast<float4*>(master);
+  const float4* __restrict__ g4 = reinterpret_cast<const float4*>(g);
+  bf16_t* __restrict__ wb = w;
+  for (int64_t base = static_cast<int64_t>(blockIdx.x) * kSgdChunk + threadIdx.x; base < n4;
+       base += static_cast<int64_t>(gridDim.x) * kSgdChunk) {
+    float4 a[kSgdUnroll], b[kSgdUnroll];
+#pragma unroll
+    for (int u = 0; u < kSgdUnroll; ++u) {
+      const int64_t i = base + u * kBlock;
+      if (i < n4) {
+        a[u] = load_nt(m4 + i);
+        b[u] = load_nt(g4 + i);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kSgdUnroll; ++u) {
+      const int64_t i = base + u * kBlock;
+      if (i < n4) {
+        const float4 r = sgd4(a[u], b[u], lr);
+        store_nt(m4 + i, r);
+        uint2 o;
+        o.x = static_cast<uint32_t>(f32_to_bf16(r.x)) | (static_cast<uint32_t>(f32_to_bf16(r.y)) << 16);
+        o.y = static_cast<uint32_t>(f32_to_bf16(r.z)) | (static_cast<uint32_t>(f32_to_bf16(r.w)) << 16);
+        store_nt(reinterpret_cast<uint2*>(wb + 4 * i), o);
+      }
+    }
   }
   for (int64_t i = n4 * 4 + static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < n;
-       i += stride) {
+       i += static_cast<int64_t>(gridDim.x) * kBlock) {
     const float a = fmaf(-lr, g[i], master[i]);
     master[i] = a;
     w[i] = f32_to_bf16(a);
@@ -268,6 +417,29 @@ unsigned grid_for(int64_t work_items, int64_t cap) {
   return static_cast<unsigned>(b);
 }
 
+template <typename TD>
+hipError_t launch_softmax_rows(int64_t chunks, int nb, int64_t rows, int64_t classes,
+                               const float* logits, const int32_t* labels, float scale, TD* dlogits,
+                               int64_t ld, float* partials, int32_t* bad, hipStream_t s) {
+  const dim3 g(nb), b(kBlock);
+  if (chunks <= 1)
+    launch_kernel(dlvm_softmax_xent_rows_kernel<TD, 1>, g, b, s, rows, classes, logits, labels,
+                  scale, dlogits, ld, partials, bad);
+  else if (chunks <= 2)
+    launch_kernel(dlvm_softmax_xent_rows_kernel<TD, 2>, g, b, s, rows, classes, logits, labels,
+                  scale, dlogits, ld, partials, bad);
+  else if (chunks <= 4)
+    launch_kernel(dlvm_softmax_xent_rows_kernel<TD, 4>, g, b, s, rows, classes, logits, labels,
+                  scale, dlogits, ld, partials, bad);
+  else if (chunks <= 8)
+    launch_kernel(dlvm_softmax_xent_rows_kernel<TD, 8>, g, b, s, rows, classes, logits, labels,
+                  scale, dlogits, ld, partials, bad);
+  else
+    launch_kernel(dlvm_softmax_xent_rows_kernel<TD, 16>, g, b, s, rows, classes, logits, labels,
+                  scale, dlogits, ld, partials, bad);
+  return hipGetLastError();
+}
+
 }  // namespace
 
 int softmax_xent_partials(int64_t rows) { return static_cast<int>((rows + kWaves - 1) / kWaves); }
@@ -278,6 +450,17 @@ hipError_t launch_softmax_xent(int dtype, int64_t rows, int64_t classes, const f
                                hipStream_t s) {
   const int nb = softmax_xent_partials(rows);
   *n_partials = nb;
+  const bool vec = classes % 4 == 0 && ld_dlogits % 4 == 0 &&
+                   ((reinterpret_cast<uintptr_t>(logits) | reinterpret_cast<uintptr_t>(dlogits)) &
+                    15u) == 0;
+  const int64_t chunks = (classes / 4 + 63) / 64;  // 16-byte chunks per lane
+  if (vec && chunks <= 16) {
+    if (dtype == F32)
+      return launch_softmax_rows<float>(chunks, nb, rows, classes, logits, labels, scale,
+                                        static_cast<float*>(dlogits), ld_dlogits, partials, bad, s);
+    return launch_softmax_rows<bf16_t>(chunks, nb, rows, classes, logits, labels, scale,
+                                       static_cast<bf16_t*>(dlogits), ld_dlogits, partials, bad, s);
+  }
   if (dtype == F32)
     launch_kernel(dlvm_softmax_xent_kernel<float>, dim3(nb), dim3(kBlock), s, rows,
                        classes, logits, labels, scale, static_cast<float*>(dlogits), ld_dlogits,
@@ -291,7 +474,7 @@ hipError_t launch_softmax_xent(int dtype, int64_t rows, int64_t classes, const f
 
 int chain8_partials(int64_t rows, int64_t cols) {
   const bool vec = cols % 4 == 0;
-  const int64_t items = vec ? rows * cols / 4 : rows * cols;
+  const int64_t items = vec ? (rows * cols / 4 + kChainUnroll - 1) / kChainUnroll : rows * cols;
   return static_cast<int>(grid_for(items, kChainBlocks));
 }
 
@@ -333,7 +516,10 @@ hipError_t launch_finalize(const float* partials, const int32_t* bad, int n, flo
 
 hipError_t launch_sgd(int dtype, int64_t n, void* params, float* master, const float* grads,
                       float lr, hipStream_t s) {
-  const unsigned nb = grid_for((n + 3) / 4, 4096);
+  // one block per kSgdChunk float4 chunks, up to 16 blocks per compute unit
+  int64_t nb64 = ((n / 4) + kSgdChunk - 1) / kSgdChunk;
+  nb64 = nb64 < 1 ? 1 : (nb64 > 4096 ? 4096 : nb64);
+  const unsigned nb = static_cast<unsigned>(nb64);
   if (dtype == F32)
     launch_kernel(dlvm_sgd_f32_kernel, dim3(nb), dim3(kBlock), s, n,
                        static_cast<float*>(params), grads, lr);

@@ -27,7 +27,7 @@ struct TileShape {
 };
 constexpr TileShape kTiles[] = {
     {0, 128, 128, 0.8, false}, {1, 64, 64, 0.6, false},   {2, 128, 32, 0.6, false},
-    {3, 32, 32, 0.5, false},   {4, 64, 64, 0.65, false},  {10, 256, 256, 0.9, true},
+    {3, 32, 32, 0.5, false},   {4, 64, 64, 0.65, false},  {5, 32, 32, 0.5, false},  {10, 256, 256, 0.9, true},
     {11, 256, 128, 0.7, true}, {12, 128, 128, 0.84, true}, {13, 256, 256, 0.85, true}};
 
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
@@ -76,6 +76,7 @@ GemmPlan plan_gemm(const GemmDesc& d) {
   double best_t = 0.0;
   for (const TileShape& t : kTiles) {
     if (t.cfg == 2 && d.N > 32) continue;  // the narrow tile only for narrow outputs
+    if (t.cfg == 5 && forced != 5) continue;
     if (t.async && !can_async) continue;
     if (t.cfg == forced) {
       best = &t;

@@ -488,6 +488,9 @@ hipError_t launch_async(const Params& p, int cfg, unsigned grid, hipStream_t s) 
     case 12:
       launch_kernel((dlvm_gemm_async_kernel<TO, AK, BKM, 128, 128, 64, 2, 2, 4, EPI>), dim3(grid), dim3(256), s, p);
       break;
+    case 14:
+      launch_kernel((dlvm_gemm_async_kernel<TO, AK, BKM, 256, 256, 64, 2, 2, 2, EPI>), dim3(grid), dim3(256), s, p);
+      break;
     default:
       launch_kernel((dlvm_gemm_async_kernel<TO, AK, BKM, 256, 256, 32, 2, 4, 4, EPI>), dim3(grid), dim3(512), s, p);
       break;

@@ -503,6 +503,9 @@ hipError_t launch_cfg(const Params& p, int cfg, unsigned grid, hipStream_t s) {
     case 3:
       launch_kernel((dlvm_gemm_kernel<T, TO, AK, BKM, 32, 32, 1, 1, 4, 4, VA, VB, EPI>), dim3(grid), dim3(256), s, p);
       break;
+    case 5:
+      launch_kernel((dlvm_gemm_kernel<T, TO, AK, BKM, 32, 32, 1, 1, 4, 8, VA, VB, EPI>), dim3(grid), dim3(256), s, p);
+      break;
     default:
       launch_kernel((dlvm_gemm_kernel<T, TO, AK, BKM, 64, 64, 2, 2, 2, 2, VA, VB, EPI>), dim3(grid), dim3(512), s, p);
       break;

@@ -275,3 +275,63 @@ def test_bf16_storage_effect_against_exact_math():
     for l, ((gw, gb), (rw, rb)) in enumerate(zip(got["grads"], rg)):
         assert rel_l2(gw, rw) <= 0.06, l
         assert rel_l2(gb, rb) <= 0.06, l
+
+
+@pytest.mark.parametrize("name,batch", [("c2", 256), ("c1", 16), ("c3", 64), ("c4", 32)])
+def test_step_graph_replays_match_eager_steps(name, batch):
+    """A captured training step replayed K times equals K eager steps, bit for bit.
+
+    Between replays the program does eager work of its own on the same stream
+    and synchronises; every replay's loss, gradient and updated parameters are
+    checked against the eager sequence (the kernels are deterministic).
+    """
+    import torch
+    from dataclasses import replace
+    wl = replace(workloads.WORKLOADS[name], batch=batch)
+    x, params, y = workloads.make_inputs(wl, bias_scale=0.05)
+    dev = device()
+    m = dl.Model(wl.widths, wl.acts, wl.dtype, wl.loss, wl.wrt_x, batch)
+    tdt = torch_dtype(wl.dtype)
+    update = True
+    lr = 0.05
+
+    def fresh():
+        P = m.pack(params, dev, tdt)
+        master = m.pack(params, dev, torch.float32) if wl.dtype == "bf16" else None
+        return P, master
+
+    xd = to_dev(x, wl.dtype)
+    yd = None if y is None else torch.from_numpy(np.asarray(y, np.int32)).to(dev)
+    ws = torch.empty(m.workspace_bytes(batch), dtype=torch.uint8, device=dev)
+    steps = 4
+    # eager reference sequence
+    P, master = fresh()
+    loss = torch.empty(1, device=dev)
+    dP = torch.empty(m.param_count(), device=dev)
+    dx = torch.empty((batch, wl.widths[0]), device=dev) if wl.wrt_x else None
+    ref = []
+    for _ in range(steps):
+        m.gradient(P, xd, yd, batch, loss, dP, dx, ws)
+        m.sgd_step(P, master, dP, lr)
+        torch.cuda.synchronize()
+        ref.append((loss.clone(), dP.clone(), P.clone(), None if dx is None else dx.clone()))
+    # captured step on fresh parameters and fresh output buffers
+    P2, master2 = fresh()
+    ws2 = torch.empty_like(ws)
+    loss2 = torch.empty(1, device=dev)
+    dP2 = torch.empty(m.param_count(), device=dev)
+    dx2 = torch.empty_like(dx) if dx is not None else None
+    g = m.step_graph(P2, master2, xd, yd, batch, loss2, dP2, dx2, ws2, update=update, lr=lr)
+    scratch = torch.zeros(1 << 16, device=dev)
+    for k in range(steps):
+        g.launch()
+        scratch.mul_(0.5).add_(float(k))  # eager work between replays
+        torch.cuda.synchronize()
+        rl, rdp, rp, rdx = ref[k]
+        assert torch.equal(loss2, rl), (k, loss2.item(), rl.item())
+        assert torch.equal(dP2, rdp), k
+        assert torch.equal(P2, rp), k
+        if rdx is not None:
+            assert torch.equal(dx2, rdx), k
+    assert m.check(ws2) == dl.OK
+    del g
