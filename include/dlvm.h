@@ -104,8 +104,11 @@ dlvm_status dlvm_param_layout(const dlvm_model* m, int64_t* offsets, int64_t* ld
 
 /* Bytes of workspace a forward or gradient call at `batch` rows needs
  * (0 if the batch is invalid). Holds saved activations, adjoints, loss
- * partials and the device error flags. One workspace must not be used by two
- * calls that may run concurrently. */
+ * partials, the float32 partial products of a split batch reduction (an
+ * adjoint product wrt the weights whose output has too few tiles to occupy
+ * the device is computed in k-slices and summed in slice order) and the device
+ * error flags. One workspace must not be used by two calls that may run
+ * concurrently. */
 size_t dlvm_workspace_bytes(const dlvm_model* m, int64_t batch);
 
 /* The original function (Fig. 3's @foo): writes `out`, float32 [batch, widths[L]]:

@@ -52,7 +52,9 @@ struct dlvm_model {
   std::vector<int64_t> ldw;      // row stride of W_l (N_l, or N_L rounded up to 8)
   int64_t param_count = 0;
   dlvm::ZeroGaps gaps{};         // padding ranges of the flat buffer
-  int32_t n_grad_launches = 0;   // launches of one gradient call
+  // Launches of the most recent gradient call (the SGD launch that follows it
+  // is the next position of the step for the timing probe).
+  mutable int32_t n_grad_launches = 0;
   mutable ProbeState probe;
 };
 
@@ -90,8 +92,13 @@ struct WsLayout {
   size_t logits = 0;        // float32 [B, widths[L]] (logits, or z for the chain)
   std::vector<size_t> dz;   // dz[l], l = 0 .. L-1: adjoint of layer l's pre-activation output,
                             // [B, ldw[l]] (storage dtype; float32 for the chain)
+  size_t splitk = 0;        // float32 partials of a split adjoint product wrt the weights
+  int64_t splitk_elems = 0;
   size_t total = 0;
 };
+
+GemmDesc gemm_tn(int dtype, int64_t M, int64_t N, int64_t K, const void* X, const void* dY,
+                 int64_t ldy, float* dW, int64_t ldw, float* db, int64_t nvec);
 
 WsLayout ws_layout(const dlvm_model* m, int64_t B) {
   WsLayout w;
@@ -118,6 +125,16 @@ WsLayout ws_layout(const dlvm_model* m, int64_t B) {
     w.dz[l] = off;
     off = align_up(off + static_cast<size_t>(B) * m->ldw[l] * dz_es);
   }
+  // Scratch for the partials of the largest split among the adjoint products
+  // wrt the weights (the planner splits their batch reduction when their
+  // output has too few tiles to occupy the device).
+  for (int l = 0; l < m->L; ++l) {
+    const int64_t K = m->widths[l], N = m->widths[l + 1], Np = m->ldw[l];
+    const GemmDesc d = gemm_tn(m->dtype, B, Np, K, nullptr, nullptr, Np, nullptr, Np, nullptr, N);
+    w.splitk_elems = std::max<int64_t>(w.splitk_elems, dlvm::split_ws_elems(d));
+  }
+  w.splitk = off;
+  off = align_up(off + static_cast<size_t>(w.splitk_elems) * 4);
   w.total = off;
   return w;
 }
@@ -256,12 +273,27 @@ class Launcher {
     const dlvm::GemmPlan pl = dlvm::plan_gemm(d);
     LaunchInfo info = gemm_info(d);
     info.name += "_" + std::to_string(pl.bm) + "x" + std::to_string(pl.bn) + "c" + std::to_string(pl.cfg);
-    return run(std::move(info), [&](hipStream_t st) { return dlvm::launch_gemm(d, pl, st); },
-               "gemm launch");
+    if (pl.splits > 1) info.name += "s" + std::to_string(pl.splits);
+    dlvm_status st = run(std::move(info), [&](hipStream_t s) { return dlvm::launch_gemm(d, pl, s); },
+                         "gemm launch");
+    if (st != DLVM_OK || pl.splits <= 1) return st;
+    // The k-slices' partial products (and column sums) summed in slice order.
+    const int64_t nv = d.nvec > 0 ? d.nvec : d.N;
+    const int64_t c_split = d.M * d.ldc;
+    const float* cs = d.split_ws + pl.splits * c_split;
+    const double bytes = (double(pl.splits) + 1.0) * double(d.M) * double(d.N) * 4.0 +
+                         (d.colsum ? (double(pl.splits) + 1.0) * double(nv) * 4.0 : 0.0);
+    return run(elementwise_info("splitk_reduce", d.M, d.N, bytes),
+               [&](hipStream_t s) {
+                 return dlvm::launch_splitk_reduce(pl.splits, d.M, d.N, d.ldc, d.split_ws, c_split,
+                                                   static_cast<float*>(d.C), cs, nv, d.colsum, nv, s);
+               },
+               "split reduction launch");
   }
 
   hipStream_t stream() const { return main_; }
   bool dry() const { return plan_ != nullptr; }
+  int32_t launches() const { return index_; }
 
  private:
   const dlvm_model* m_;
@@ -316,7 +348,10 @@ dlvm_status plan_gradient(const dlvm_model* m, const void* params, const void* x
                  },
                  "chain launch");
     if (st != DLVM_OK) return st;
-    if ((st = run.gemm(gemm_tn(dt, batch, N, K, x, zbar, N, G(0), N, G(1), N))) != DLVM_OK) return st;
+    GemmDesc dw = gemm_tn(dt, batch, N, K, x, zbar, N, G(0), N, G(1), N);
+    dw.split_ws = at<float>(ws, w.splitk);
+    dw.split_ws_elems = w.splitk_elems;
+    if ((st = run.gemm(dw)) != DLVM_OK) return st;
     // dx = zbar . W^T + xbar (xbar already in dx: in-place accumulate)
     if ((st = run.gemm(gemm_nt(dt, DLVM_F32, DLVM_ACT_NONE, batch, N, K, zbar, N, P(0), N, nullptr,
                                dx, dx))) != DLVM_OK)
@@ -356,9 +391,10 @@ dlvm_status plan_gradient(const dlvm_model* m, const void* params, const void* x
     const int64_t K = m->widths[l], N = m->widths[l + 1];
     const int64_t Np = m->ldw[l];  // padded width (== N except the last layer)
     void* dzl = at<void>(ws, w.dz[l]);
-    if ((st = run.gemm(gemm_tn(dt, batch, Np, K, hin, dzl, Np, G(2 * l), Np, G(2 * l + 1), N))) !=
-        DLVM_OK)
-      return st;
+    GemmDesc dw = gemm_tn(dt, batch, Np, K, hin, dzl, Np, G(2 * l), Np, G(2 * l + 1), N);
+    dw.split_ws = at<float>(ws, w.splitk);
+    dw.split_ws_elems = w.splitk_elems;
+    if ((st = run.gemm(dw)) != DLVM_OK) return st;
     if (l > 0) {
       GemmDesc d = gemm_nt(dt, dt, m->acts[l - 1], batch, Np, K, dzl, Np, P(2 * l), Np,
                            at<void>(ws, w.H[l]), nullptr, at<void>(ws, w.dz[l - 1]));
@@ -587,7 +623,9 @@ dlvm_status dlvm_gradient(const dlvm_model* m, const void* params, const void* x
   dlvm_status st = check_gradient_args(m, params, x, labels, batch, loss, dparams, dx, ws, ws_bytes);
   if (st != DLVM_OK) return st;
   Launcher run(m, static_cast<hipStream_t>(stream), nullptr, 0);
-  return plan_gradient(m, params, x, labels, batch, loss, dparams, dx, ws, run);
+  st = plan_gradient(m, params, x, labels, batch, loss, dparams, dx, ws, run);
+  m->n_grad_launches = run.launches();
+  return st;
 }
 
 dlvm_status dlvm_sgd_step(const dlvm_model* m, void* params, float* master, const float* dparams,
@@ -625,6 +663,7 @@ dlvm_status dlvm_step_graph_create(const dlvm_model* m, void* params, float* mas
   {
     Launcher run(m, cs, nullptr, 0);
     st = plan_gradient(m, params, x, labels, batch, loss, dparams, dx, ws, run);
+    m->n_grad_launches = run.launches();
   }
   if (st == DLVM_OK && update) st = enqueue_sgd(m, params, master, dparams, lr, cs);
   const std::string err = st == DLVM_OK ? std::string() : g_last_error;
@@ -661,7 +700,10 @@ void dlvm_graph_destroy(dlvm_graph* g) {
 
 int32_t dlvm_plan_size(const dlvm_model* m, int64_t batch) {
   if (m == nullptr || batch < 1 || batch > m->batch_max) return 0;
-  return m->n_grad_launches + 1;
+  std::vector<LaunchInfo> plan;
+  Launcher dry(m, nullptr, &plan, 0);
+  plan_gradient(m, nullptr, nullptr, nullptr, batch, nullptr, nullptr, nullptr, nullptr, dry);
+  return static_cast<int32_t>(plan.size()) + 1;
 }
 
 dlvm_status dlvm_plan_entry(const dlvm_model* m, int64_t batch, int32_t index,

@@ -410,6 +410,48 @@ __global__ __launch_bounds__(kBlock) void dlvm_sgd_bf16_kernel(int64_t n, bf16_t
   }
 }
 
+// ---------------------------------------------------------------------------
+// Split reduction: the k-slices of a product summed in slice order (fixed
+// order, so the result is the same on every run). The partials are read once.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kBlock) void dlvm_splitk_reduce_kernel(
+    int S, int64_t rows, int64_t cols, int64_t ld, const float* __restrict__ part,
+    int64_t c_split, float* __restrict__ out, const float* __restrict__ cs_part,
+    int64_t cs_split, float* __restrict__ colsum, int64_t nvec, bool vec) {
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
+  const int64_t t0 = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+  if (vec) {
+    const int64_t c4 = cols / 4;
+    const int64_t n4 = rows * c4;
+    for (int64_t i = t0; i < n4; i += stride) {
+      const int64_t r = i / c4, c = (i - r * c4) * 4;
+      const int64_t o = r * ld + c;
+      float4 acc = load_nt(reinterpret_cast<const float4*>(part + o));
+      for (int q = 1; q < S; ++q) {
+        const float4 v = load_nt(reinterpret_cast<const float4*>(part + q * c_split + o));
+        acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+      }
+      *reinterpret_cast<float4*>(out + o) = acc;
+    }
+  } else {
+    const int64_t n = rows * cols;
+    for (int64_t i = t0; i < n; i += stride) {
+      const int64_t r = i / cols, c = i - r * cols;
+      const int64_t o = r * ld + c;
+      float acc = part[o];
+      for (int q = 1; q < S; ++q) acc += part[q * c_split + o];
+      out[o] = acc;
+    }
+  }
+  if (colsum != nullptr) {
+    for (int64_t i = t0; i < nvec; i += stride) {
+      float acc = cs_part[i];
+      for (int q = 1; q < S; ++q) acc += cs_part[q * cs_split + i];
+      colsum[i] = acc;
+    }
+  }
+}
+
 unsigned grid_for(int64_t work_items, int64_t cap) {
   int64_t b = (work_items + kBlock - 1) / kBlock;
   if (b < 1) b = 1;
@@ -526,6 +568,18 @@ hipError_t launch_sgd(int dtype, int64_t n, void* params, float* master, const f
   else
     launch_kernel(dlvm_sgd_bf16_kernel, dim3(nb), dim3(kBlock), s, n,
                        static_cast<bf16_t*>(params), master, grads, lr);
+  return hipGetLastError();
+}
+
+hipError_t launch_splitk_reduce(int splits, int64_t rows, int64_t cols, int64_t ld,
+                                const float* part, int64_t c_split, float* out,
+                                const float* cs_part, int64_t cs_split, float* colsum,
+                                int64_t nvec, hipStream_t s) {
+  const bool vec = cols % 4 == 0 && ld % 4 == 0 && c_split % 4 == 0 &&
+                   ((reinterpret_cast<uintptr_t>(part) | reinterpret_cast<uintptr_t>(out)) & 15u) == 0;
+  const unsigned nb = grid_for(vec ? rows * cols / 4 : rows * cols, 8192);
+  launch_kernel(dlvm_splitk_reduce_kernel, dim3(nb), dim3(kBlock), s, splits, rows, cols, ld, part,
+                c_split, out, cs_part, cs_split, colsum, nvec, vec);
   return hipGetLastError();
 }
 

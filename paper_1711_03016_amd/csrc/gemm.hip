@@ -16,19 +16,36 @@ constexpr double kRateBF16 = 4096.0;
 constexpr double kL2BytesPerClock = 64.0;
 
 // Tile configurations with the fraction of the matrix-core rate each sustains
-// when not starved. Configurations 0-4 are the register-staged kernel
+// when not starved, for float32 and for bf16 operands (measured on large
+// products). Configurations 0-5 are the register-staged kernel
 // (gemm_kernel.hpp), 10-13 the bf16 kernel with direct-to-LDS loads
-// (gemm_async.hpp).
+// (gemm_async.hpp), 14-15 the four-wave bf16 kernel (gemm_xl.hpp).
 struct TileShape {
   int cfg;
   int bm, bn;
-  double eff;
+  double eff_f32, eff_bf16;
   bool async;
+  int kseg;  // register-staged kernel: 128-byte k-segments per pipeline stage
 };
 constexpr TileShape kTiles[] = {
-    {0, 128, 128, 0.8, false}, {1, 64, 64, 0.6, false},   {2, 128, 32, 0.6, false},
-    {3, 32, 32, 0.5, false},   {4, 64, 64, 0.65, false},  {5, 32, 32, 0.5, false},  {10, 256, 256, 0.9, true},
-    {11, 256, 128, 0.7, true}, {12, 128, 128, 0.84, true}, {13, 256, 256, 0.85, true}};
+    {0, 128, 128, 0.8, 0.55, false, 1},  {1, 64, 64, 0.6, 0.3, false, 2},
+    {2, 128, 32, 0.6, 0.3, false, 2},    {3, 32, 32, 0.5, 0.25, false, 4},
+    {4, 64, 64, 0.65, 0.2, false, 2},    {5, 32, 32, 0.5, 0.25, false, 8},
+    {10, 256, 256, 0.0, 0.9, true, 0},   {11, 256, 128, 0.0, 0.63, true, 0},
+    {12, 128, 128, 0.0, 0.54, true, 0},  {13, 256, 256, 0.0, 0.88, true, 0},
+    {14, 256, 256, 0.0, 0.89, true, 0},  {15, 256, 256, 0.0, 0.85, true, 0}};
+
+// The register-staged kernel has one stage of loads in flight: a stage costs
+// at least one load round trip (measured on small float32 products).
+constexpr double kStageCycles = 3500.0;
+
+// Fixed cost of one round of tiles (first loads, epilogue) and of the extra
+// launch of a split reduction, in clock cycles; HBM bytes per clock.
+constexpr double kTileFixed = 4000.0;
+constexpr double kLaunch = 9600.0;
+constexpr double kHbmBytesPerClock = 2000.0;
+constexpr int kMaxSplits = 16;
+constexpr int64_t kMinChunk = 256;  // k per slice at least (a multiple of every k-tile)
 
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
@@ -44,16 +61,62 @@ bool async_ok(const GemmDesc& d) {
          aligned16(d.aux) && aligned16(d.residual) && aligned16(d.bias);
 }
 
+// Extent in bytes of a row-major operand of `rows` rows of `cols` elements at
+// stride `ld`.
+int64_t extent_bytes(int64_t rows, int64_t cols, int64_t ld, int64_t es) {
+  return ((rows - 1) * ld + cols) * es;
+}
+
+// Operand rows and columns of a product (A is M x K or K x M, B is N x K or K x N).
+void operand_dims(const GemmDesc& d, int64_t& ar, int64_t& ac, int64_t& br, int64_t& bc) {
+  const bool ak = d.layout != Layout::TN, bk = d.layout == Layout::NT;
+  ar = ak ? d.M : d.K; ac = ak ? d.K : d.M;
+  br = bk ? d.N : d.K; bc = bk ? d.K : d.N;
+}
+
+// The buffer-descriptor kernel addresses its operands with 32-bit byte
+// offsets: every offset it forms (up to one tile past either extent) must stay
+// below 2^31.
+bool xl_ok(const GemmDesc& d) {
+  if (!async_ok(d)) return false;
+  int64_t ar, ac, br, bc;
+  operand_dims(d, ar, ac, br, bc);
+  const int64_t lim = int64_t(1) << 31;
+  return (ar + 256) * d.lda * 2 + 512 < lim && (br + 256) * d.ldb * 2 + 512 < lim &&
+         ac <= d.lda && bc <= d.ldb;
+}
+
+// k per slice when K is split `splits` ways (a multiple of 64, so every
+// slice but the last is whole k-tiles for every kernel).
+int64_t slice_k(int64_t K, int splits) { return ceil_div(ceil_div(K, splits), 64) * 64; }
+
 // Clock cycles one configuration needs: rounds of tiles over the compute
-// units, each tile bound by its matrix-core work or its operand traffic.
-double estimate(const GemmDesc& d, const TileShape& t) {
+// units, each tile bound by its matrix-core work or its operand traffic, plus
+// the reduction of a split product.
+double estimate(const GemmDesc& d, const TileShape& t, int splits) {
   const int64_t tiles = ceil_div(d.M, t.bm) * ceil_div(d.N, t.bn);
+  const int64_t kc = splits > 1 ? slice_k(d.K, splits) : d.K;
+  const int64_t slices = ceil_div(d.K, kc);
   const double es = d.dtype == F32 ? 4.0 : 2.0;
-  const double rate = (d.dtype == F32 ? kRateF32 : kRateBF16) * t.eff;
-  const double flops = 2.0 * t.bm * t.bn * double(d.K);
-  const double bytes = double(t.bm + t.bn) * double(d.K) * es;
-  const double per_tile = std::max(flops / rate, bytes / kL2BytesPerClock);
-  return double(ceil_div(tiles, kComputeUnits)) * per_tile;
+  const double eff = d.dtype == F32 ? t.eff_f32 : t.eff_bf16;
+  const double rate = (d.dtype == F32 ? kRateF32 : kRateBF16) * eff;
+  const double flops = 2.0 * t.bm * t.bn * double(kc);
+  const double bytes = double(t.bm + t.bn) * double(kc) * es;
+  double per_tile = std::max(flops / rate, bytes / kL2BytesPerClock);
+  if (!t.async && d.dtype == BF16) {  // (the float32 choices were measured without it)
+    const int64_t kstage = int64_t(t.kseg) * 64;
+    per_tile = std::max(per_tile, double(ceil_div(kc, kstage)) * kStageCycles);
+  }
+  per_tile += kTileFixed;
+  double c = double(ceil_div(tiles * slices, kComputeUnits)) * per_tile;
+  if (slices > 1) c += kLaunch + double(slices + 1) * double(d.M) * double(d.N) * 4.0 / kHbmBytesPerClock;
+  return c;
+}
+
+// Float32 elements the partials of a `splits`-way split of product d take.
+int64_t split_need(const GemmDesc& d, int splits) {
+  const int64_t nv = d.nvec > 0 ? d.nvec : d.N;
+  return static_cast<int64_t>(splits) * (d.M * d.ldc + nv);
 }
 
 }  // namespace
@@ -69,32 +132,70 @@ int forced_config() {
   return (end != nullptr && *end == 0) ? static_cast<int>(c) : -1;
 }
 
-GemmPlan plan_gemm(const GemmDesc& d) {
-  const bool can_async = async_ok(d);
-  const int forced = forced_config();
+namespace {
+
+// The configuration and split (only products wrt the weights, TN, with
+// scratch for the partials) that the estimate prefers. `assume_aligned`
+// ignores the operands' addresses (for sizing scratch before they exist).
+GemmPlan choose(const GemmDesc& d, bool assume_aligned, int64_t capacity, int forced) {
+  const bool can_async = assume_aligned ? (d.dtype == BF16 && d.lda % 8 == 0 && d.ldb % 8 == 0 &&
+                                           d.K % 8 == 0 && d.ldc % 8 == 0)
+                                        : async_ok(d);
   const TileShape* best = nullptr;
+  int best_s = 1;
   double best_t = 0.0;
   for (const TileShape& t : kTiles) {
     if (t.cfg == 2 && d.N > 32) continue;  // the narrow tile only for narrow outputs
     if (t.cfg == 5 && forced != 5) continue;
     if (t.async && !can_async) continue;
-    if (t.cfg == forced) {
-      best = &t;
-      break;
-    }
-    const double e = estimate(d, t);
-    if (best == nullptr || e < best_t * 0.97) {  // prefer earlier (larger) tiles on near ties
-      best = &t;
-      best_t = e;
+    if (t.async && d.dtype == F32) continue;
+    // Measured: where the direct-to-LDS kernels can run a bf16 product, the
+    // register-staged 64 x 64 and 128 x 128 tiles are never faster (with one
+    // workgroup per compute unit they cannot hide their load latency).
+    if (can_async && (t.cfg == 0 || t.cfg == 1 || t.cfg == 4) && forced != t.cfg) continue;
+    if ((t.cfg == 14 || t.cfg == 15) && !xl_ok(d)) continue;
+    // Measured on 16384 x 4096 x 4096: the four-wave kernel is the faster
+    // one for the forward layout only; 15 runs only when forced.
+    if (t.cfg == 14 && d.layout != Layout::NN && forced != 14) continue;
+    if (t.cfg == 15 && forced != 15) continue;
+    if (forced >= 0 && t.cfg != forced) continue;
+    for (int sp = 1; sp <= kMaxSplits; sp *= 2) {
+      if (sp > 1) {
+        if (d.layout != Layout::TN || capacity <= 0) break;
+        if (slice_k(d.K, sp) < kMinChunk || ceil_div(d.K, slice_k(d.K, sp)) < sp) break;
+        if (split_need(d, sp) > capacity) break;
+      }
+      const double e = estimate(d, t, sp);
+      if (best == nullptr || e < best_t * 0.97) {  // prefer earlier (larger) tiles, fewer splits
+        best = &t;
+        best_s = sp;
+        best_t = e;
+      }
     }
   }
+  if (best == nullptr)  // a forced configuration that cannot run this product is ignored
+    return choose(d, assume_aligned, capacity, -1);
   GemmPlan pl{};
   pl.cfg = best->cfg;
   pl.bm = best->bm;
   pl.bn = best->bn;
   pl.tiles_m = static_cast<int>(ceil_div(d.M, pl.bm));
   pl.tiles_n = static_cast<int>(ceil_div(d.N, pl.bn));
+  pl.k_chunk = best_s > 1 ? slice_k(d.K, best_s) : d.K;
+  pl.splits = static_cast<int>(ceil_div(d.K, pl.k_chunk));
   return pl;
+}
+
+}  // namespace
+
+GemmPlan plan_gemm(const GemmDesc& d) {
+  return choose(d, false, d.split_ws != nullptr ? d.split_ws_elems : 0, forced_config());
+}
+
+int64_t split_ws_elems(const GemmDesc& d) {
+  if (d.layout != Layout::TN) return 0;
+  const GemmPlan pl = choose(d, true, int64_t(1) << 40, forced_config());
+  return pl.splits > 1 ? split_need(d, pl.splits) : 0;
 }
 
 hipError_t launch_gemm(const GemmDesc& d, const GemmPlan& pl, hipStream_t s) {
@@ -118,7 +219,26 @@ hipError_t launch_gemm(const GemmDesc& d, const GemmPlan& pl, hipStream_t s) {
   p.alpha = d.alpha; p.act = d.act;
   p.tiles_m = pl.tiles_m; p.tiles_n = pl.tiles_n;
   p.nvec = d.nvec > 0 ? d.nvec : d.N;
-  const unsigned grid = static_cast<unsigned>(static_cast<int64_t>(pl.tiles_m) * pl.tiles_n);
+  p.splits = pl.splits;
+  p.k_chunk = pl.k_chunk;
+  if (pl.splits > 1) {
+    p.C = d.split_ws;                  // partial products, then partial column sums
+    p.c_split = d.M * d.ldc;
+    p.colsum = d.colsum != nullptr ? d.split_ws + pl.splits * p.c_split : nullptr;
+    p.cs_split = p.nvec;
+  } else {
+    p.c_split = p.cs_split = 0;
+  }
+  if (pl.cfg == 14 || pl.cfg == 15) {
+    int64_t ar, ac, br, bc;
+    operand_dims(d, ar, ac, br, bc);
+    p.a_bytes = static_cast<uint32_t>(extent_bytes(ar, ac, d.lda, 2));
+    p.b_bytes = static_cast<uint32_t>(extent_bytes(br, bc, d.ldb, 2));
+  } else {
+    p.a_bytes = p.b_bytes = 0;
+  }
+  const unsigned grid =
+      static_cast<unsigned>(static_cast<int64_t>(pl.tiles_m) * pl.tiles_n * pl.splits);
   switch (d.layout) {
     case Layout::NN: return gemm::launch_nn(p, d.dtype, d.out_dtype, pl.cfg, grid, va, vb, s);
     case Layout::NT: return gemm::launch_nt(p, d.dtype, d.out_dtype, pl.cfg, grid, va, vb, s);

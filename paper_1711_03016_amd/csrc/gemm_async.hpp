@@ -183,8 +183,9 @@ __device__ __forceinline__ void barrier_only() {
   __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
 
-// One k-tile (BK k) of the wave's TM x TN blocks of 32 x 32. The operand
-// tiles come in through restrict parameters: the LDS reads then carry
+// One k-tile (BK k) of the wave's TM x TN blocks of 32 x 32, the fragments of
+// the next 16 k read while the matrix cores work on the current ones. The
+// operand tiles come in through restrict parameters: the LDS reads then carry
 // alias-scope information, which tells the compiler that they do not depend on
 // the direct-to-LDS loads in flight into the other ring slots (the explicit
 // waits and barriers order the slot being read).
@@ -197,23 +198,35 @@ template <bool AK, bool BKM, int BM, int BN, int BK, int TM, int TN, bool CS>
 __device__ __forceinline__ void mma_ktile(const char* __restrict__ As, const char* __restrict__ Bs,
                                           int arow, int brow, int lane, f32x16 (&acc)[TM][TN],
                                           float (&cs)[TN], bool do_cs) {
+  constexpr int S = BK / 16;
+  bf16x8 af[2][TM], bfr[2][TN];
 #pragma unroll
-  for (int s = 0; s < BK / 16; ++s) {
-    bf16x8 af[TM], bfr[TN];
+  for (int i = 0; i < TM; ++i) af[0][i] = frag<AK, BM, BK>(As, arow + i * 32, 0, lane);
 #pragma unroll
-    for (int i = 0; i < TM; ++i) af[i] = frag<AK, BM, BK>(As, arow + i * 32, s, lane);
+  for (int j = 0; j < TN; ++j) bfr[0][j] = frag<BKM, BN, BK>(Bs, brow + j * 32, 0, lane);
 #pragma unroll
-    for (int j = 0; j < TN; ++j) bfr[j] = frag<BKM, BN, BK>(Bs, brow + j * 32, s, lane);
+  for (int s = 0; s < S; ++s) {
+    const int cur = s & 1, nxt = cur ^ 1;
+    if (s + 1 < S) {
+#pragma unroll
+      for (int i = 0; i < TM; ++i) af[nxt][i] = frag<AK, BM, BK>(As, arow + i * 32, s + 1, lane);
+#pragma unroll
+      for (int j = 0; j < TN; ++j) bfr[nxt][j] = frag<BKM, BN, BK>(Bs, brow + j * 32, s + 1, lane);
+    }
+    // The next step's fragment reads stay ahead of this step's matrix
+    // instructions (otherwise the scheduler waits on each read in turn).
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
       for (int j = 0; j < TN; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cur][i], bfr[cur][j], acc[i][j], 0, 0, 0);
+    __builtin_amdgcn_sched_barrier(0);
     if constexpr (CS) {
       if (do_cs) {
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
-          const uint4 w = __builtin_bit_cast(uint4, bfr[j]);
+          const uint4 w = __builtin_bit_cast(uint4, bfr[cur][j]);
           const uint32_t q[4] = {w.x, w.y, w.z, w.w};
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
@@ -387,7 +400,7 @@ __global__ __launch_bounds__(64 * WM * WN) void dlvm_gemm_async_kernel(Params p)
   const int wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
   int tm, tn;
-  tile_of(static_cast<int>(blockIdx.x), p.tiles_m, p.tiles_n, tm, tn);
+  tile_of(split_slice<bf16_t, AK, BKM>(p), p.tiles_m, p.tiles_n, tm, tn);
   const int64_t m0 = static_cast<int64_t>(tm) * BM;
   const int64_t n0 = static_cast<int64_t>(tn) * BN;
   const bf16_t* __restrict__ A = static_cast<const bf16_t*>(p.A);
@@ -487,9 +500,6 @@ hipError_t launch_async(const Params& p, int cfg, unsigned grid, hipStream_t s) 
       break;
     case 12:
       launch_kernel((dlvm_gemm_async_kernel<TO, AK, BKM, 128, 128, 64, 2, 2, 4, EPI>), dim3(grid), dim3(256), s, p);
-      break;
-    case 14:
-      launch_kernel((dlvm_gemm_async_kernel<TO, AK, BKM, 256, 256, 64, 2, 2, 2, EPI>), dim3(grid), dim3(256), s, p);
       break;
     default:
       launch_kernel((dlvm_gemm_async_kernel<TO, AK, BKM, 256, 256, 32, 2, 4, 4, EPI>), dim3(grid), dim3(512), s, p);

@@ -71,7 +71,38 @@ struct Params {
   int act;
   int tiles_m, tiles_n;
   int64_t nvec;  // entries of bias / colsum (columns n >= nvec have none)
+  uint32_t a_bytes, b_bytes;  // extents of A and B in bytes (buffer-descriptor kernels)
+  // Split reduction (adjoint wrt the weights): workgroup b handles tile
+  // b % (tiles_m * tiles_n) over k-slice b / (tiles_m * tiles_n) of k_chunk
+  // k, and writes its float32 partial product (and partial column sums) at
+  // C + slice * c_split (colsum + slice * cs_split). splits == 1: no split.
+  int splits;
+  int64_t k_chunk, c_split, cs_split;
 };
+
+// Tile index of this workgroup; with a split reduction, also narrows p to the
+// workgroup's k-slice and partial outputs.
+template <typename T, bool AK, bool BKM>
+__device__ __forceinline__ int split_slice(Params& p) {
+  int bid = static_cast<int>(blockIdx.x);
+  if (p.splits > 1) {
+    const int tiles = p.tiles_m * p.tiles_n;
+    const int sl = bid / tiles;
+    bid -= sl * tiles;
+    const int64_t k0 = static_cast<int64_t>(sl) * p.k_chunk;
+    const int64_t kl = p.K - k0 < p.k_chunk ? p.K - k0 : p.k_chunk;
+    const int64_t sa = AK ? k0 : k0 * p.lda;
+    const int64_t sb = BKM ? k0 : k0 * p.ldb;
+    p.A = static_cast<const T*>(p.A) + sa;
+    p.B = static_cast<const T*>(p.B) + sb;
+    p.a_bytes -= static_cast<uint32_t>(sa * static_cast<int64_t>(sizeof(T)));
+    p.b_bytes -= static_cast<uint32_t>(sb * static_cast<int64_t>(sizeof(T)));
+    p.K = kl;
+    p.C = static_cast<float*>(p.C) + sl * p.c_split;
+    if (p.colsum != nullptr) p.colsum += sl * p.cs_split;
+  }
+  return bid;
+}
 
 __device__ __forceinline__ uint32_t perm_b32(uint32_t hi, uint32_t lo, uint32_t sel) {
   return __builtin_amdgcn_perm(hi, lo, sel);
@@ -326,7 +357,7 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void dlvm_gemm_kernel(Params p) 
 
   // Consecutive workgroups walk down a column of tiles, so they share the
   // B tile (the weights in the forward) through L2.
-  const int tile = static_cast<int>(blockIdx.x);
+  const int tile = split_slice<T, AK, BKM>(p);
   const int tm = tile % p.tiles_m;
   const int tn = tile / p.tiles_m;
   const int64_t m0 = static_cast<int64_t>(tm) * BM;

@@ -1,6 +1,6 @@
 // Instantiations of the dense-layer product for the NN layout (forward products: bias + activation
 // epilogue).
-#include "gemm_async.hpp"
+#include "gemm_xl.hpp"
 
 namespace dlvm {
 namespace gemm {
@@ -9,8 +9,8 @@ hipError_t launch_nn(const Params& p, int dtype, int out_dtype, int cfg, unsigne
                      bool vb, hipStream_t s) {
   if (dtype == F32) return launch_vec<float, float, true, false, EPI_STORE>(p, cfg, grid, va, vb, s);
   if (cfg >= kAsyncFirst) {
-    if (out_dtype == F32) return launch_async<float, true, false, EPI_STORE>(p, cfg, grid, s);
-    return launch_async<bf16_t, true, false, EPI_STORE>(p, cfg, grid, s);
+    if (out_dtype == F32) return launch_bf16<float, true, false, EPI_STORE>(p, cfg, grid, s);
+    return launch_bf16<bf16_t, true, false, EPI_STORE>(p, cfg, grid, s);
   }
   if (out_dtype == F32) return launch_vec<bf16_t, float, true, false, EPI_STORE>(p, cfg, grid, va, vb, s);
   return launch_vec<bf16_t, bf16_t, true, false, EPI_STORE>(p, cfg, grid, va, vb, s);

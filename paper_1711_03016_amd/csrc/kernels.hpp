@@ -50,6 +50,9 @@ struct GemmDesc {
   int64_t nvec;          // entries of bias / colsum (0 means N). Columns n >= nvec
                          // have none; with a padded operand they are zero.
   int64_t kvalid;        // unpadded contraction extent, for work accounting (0 means K)
+  // TN only: float32 scratch for a split reduction over K (null: no split).
+  float* split_ws;
+  int64_t split_ws_elems;
 };
 
 // How one product is launched: tile configuration and grid.
@@ -57,7 +60,13 @@ struct GemmPlan {
   int cfg;               // tile configuration index
   int bm, bn;            // tile shape
   int tiles_m, tiles_n;
+  int splits;            // k-slices (1: none); partials in GemmDesc::split_ws
+  int64_t k_chunk;       // k per slice
 };
+
+// Float32 scratch elements a split reduction of this product may use: enough
+// for the largest split the planner can choose (0 for products it never splits).
+int64_t split_ws_elems(const GemmDesc& d);
 
 // Choose the launch of a product.
 GemmPlan plan_gemm(const GemmDesc& d);
@@ -98,5 +107,13 @@ hipError_t launch_finalize(const float* partials, const int32_t* bad, int n, flo
 
 hipError_t launch_sgd(int dtype, int64_t n, void* params, float* master, const float* grads,
                       float lr, hipStream_t s);
+
+// Sum of the k-slices of a split product in slice order: out[r, c] (row
+// stride ld) = sum_s part[s * c_split + r * ld + c] for c < cols, and
+// colsum[n] = sum_s cs_part[s * cs_split + n] for n < nvec (if colsum).
+hipError_t launch_splitk_reduce(int splits, int64_t rows, int64_t cols, int64_t ld,
+                                const float* part, int64_t c_split, float* out,
+                                const float* cs_part, int64_t cs_split, float* colsum,
+                                int64_t nvec, hipStream_t s);
 
 }  // namespace dlvm

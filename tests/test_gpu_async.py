@@ -1,8 +1,10 @@
-"""GPU parity of the bf16 direct-to-LDS GEMM kernel in each of its tile configurations.
+"""GPU parity of the bf16 direct-to-LDS GEMM kernels in each of their tile configurations.
 
-The planner picks this kernel only for large bf16 products; here each of its
-configurations (10: 256x256, 11: 256x128, 12: 128x128, 13: 256x256 with 32-deep
-k-tiles and a deeper ring) is forced through
+The planner picks these kernels only for large bf16 products; here each
+configuration (10: 256x256, 11: 256x128, 12: 128x128, 13: 256x256 with 32-deep
+k-tiles and a deeper ring, 14 and 15: 256x256 on four waves of 128x128 with
+buffer-descriptor loads, 64-deep k-tiles in 2 stages or 32-deep in 4) is
+forced through
 DLVM_GEMM_CONFIG on shapes that span several tiles and stages with ragged M,
 N and K (K a multiple of 8 but not of 64, K smaller than one k-tile), for the
 three layouts (forward NN, adjoint wrt the input NT, adjoint wrt the weights
@@ -24,7 +26,7 @@ from helpers import TOL, device, quant, rel_l2, to_dev, to_np
 
 pytestmark = pytest.mark.gpu
 
-CFGS = [10, 11, 12, 13]
+CFGS = [10, 11, 12, 13, 14, 15]
 EXACT = 1e-5
 # (M, N, K): single tile with K = 8, exact tiles, ragged edges with K % 64 != 0,
 # many k-tiles (deeper than every ring), and a wide ragged product.
