@@ -276,8 +276,14 @@ class Launcher {
     if (pl.splits > 1) info.name += "s" + std::to_string(pl.splits);
     dlvm_status st = run(std::move(info), [&](hipStream_t s) { return dlvm::launch_gemm(d, pl, s); },
                          "gemm launch");
-    if (st != DLVM_OK || pl.splits <= 1) return st;
-    // The k-slices' partial products (and column sums) summed in slice order.
+    if (st != DLVM_OK) return st;
+    return reduce_split(d, pl);
+  }
+
+  // The k-slices' partial products (and column sums) of a split product,
+  // summed in slice order (nothing if the product is not split).
+  dlvm_status reduce_split(const GemmDesc& d, const dlvm::GemmPlan& pl) {
+    if (pl.splits <= 1) return DLVM_OK;
     const int64_t nv = d.nvec > 0 ? d.nvec : d.N;
     const int64_t c_split = d.M * d.ldc;
     const float* cs = d.split_ws + pl.splits * c_split;
@@ -289,6 +295,30 @@ class Launcher {
                                                    static_cast<float*>(d.C), cs, nv, d.colsum, nv, s);
                },
                "split reduction launch");
+  }
+
+  // A layer's two adjoint products (tn: wrt the weights, nt: wrt the input):
+  // one launch when both are planned on a configuration that has a paired
+  // kernel, else two; then the split reduction of the product wrt the weights.
+  dlvm_status gemm_pair(const GemmDesc& tn, const GemmDesc& nt) {
+    const dlvm::GemmPlan p1 = dlvm::plan_gemm(tn), p2 = dlvm::plan_gemm(nt);
+    if (!dlvm::pairable(tn, p1, nt, p2)) {
+      dlvm_status st = gemm(tn);
+      return st != DLVM_OK ? st : gemm(nt);
+    }
+    LaunchInfo a = gemm_info(tn), b = gemm_info(nt);
+    LaunchInfo info;
+    info.name = std::string("gemm_pair_") + (tn.dtype == DLVM_F32 ? "f32_" : "bf16_") +
+                std::to_string(p1.bm) + "x" + std::to_string(p1.bn) + "c" + std::to_string(p1.cfg) +
+                (p1.splits > 1 ? "s" + std::to_string(p1.splits) : std::string());
+    info.M = a.M; info.N = a.N; info.K = a.K;  // the product wrt the weights
+    info.flops = a.flops + b.flops;
+    info.bytes = a.bytes + b.bytes;
+    dlvm_status st = run(std::move(info),
+                         [&](hipStream_t s) { return dlvm::launch_gemm_pair(tn, p1, nt, p2, s); },
+                         "paired gemm launch");
+    if (st != DLVM_OK) return st;
+    return reduce_split(tn, p1);
   }
 
   hipStream_t stream() const { return main_; }
@@ -351,11 +381,10 @@ dlvm_status plan_gradient(const dlvm_model* m, const void* params, const void* x
     GemmDesc dw = gemm_tn(dt, batch, N, K, x, zbar, N, G(0), N, G(1), N);
     dw.split_ws = at<float>(ws, w.splitk);
     dw.split_ws_elems = w.splitk_elems;
-    if ((st = run.gemm(dw)) != DLVM_OK) return st;
     // dx = zbar . W^T + xbar (xbar already in dx: in-place accumulate)
-    if ((st = run.gemm(gemm_nt(dt, DLVM_F32, DLVM_ACT_NONE, batch, N, K, zbar, N, P(0), N, nullptr,
-                               dx, dx))) != DLVM_OK)
-      return st;
+    const GemmDesc dxd = gemm_nt(dt, DLVM_F32, DLVM_ACT_NONE, batch, N, K, zbar, N, P(0), N,
+                                 nullptr, dx, dx);
+    if ((st = run.gemm_pair(dw, dxd)) != DLVM_OK) return st;
     return finalize();
   }
 
@@ -394,17 +423,20 @@ dlvm_status plan_gradient(const dlvm_model* m, const void* params, const void* x
     GemmDesc dw = gemm_tn(dt, batch, Np, K, hin, dzl, Np, G(2 * l), Np, G(2 * l + 1), N);
     dw.split_ws = at<float>(ws, w.splitk);
     dw.split_ws_elems = w.splitk_elems;
-    if ((st = run.gemm(dw)) != DLVM_OK) return st;
+    // The product wrt the input (dead for the first layer unless x is
+    // differentiated) reads the same adjoint: the two share one launch.
     if (l > 0) {
       GemmDesc d = gemm_nt(dt, dt, m->acts[l - 1], batch, Np, K, dzl, Np, P(2 * l), Np,
                            at<void>(ws, w.H[l]), nullptr, at<void>(ws, w.dz[l - 1]));
       d.kvalid = N;
-      if ((st = run.gemm(d)) != DLVM_OK) return st;
+      if ((st = run.gemm_pair(dw, d)) != DLVM_OK) return st;
     } else if (m->wrt_x) {
       GemmDesc d = gemm_nt(dt, DLVM_F32, DLVM_ACT_NONE, batch, Np, K, dzl, Np, P(0), Np, nullptr,
                            nullptr, dx);
       d.kvalid = N;
-      if ((st = run.gemm(d)) != DLVM_OK) return st;
+      if ((st = run.gemm_pair(dw, d)) != DLVM_OK) return st;
+    } else if ((st = run.gemm(dw)) != DLVM_OK) {
+      return st;
     }
   }
   return finalize();

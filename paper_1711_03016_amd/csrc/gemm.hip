@@ -198,20 +198,26 @@ int64_t split_ws_elems(const GemmDesc& d) {
   return pl.splits > 1 ? split_need(d, pl.splits) : 0;
 }
 
-hipError_t launch_gemm(const GemmDesc& d, const GemmPlan& pl, hipStream_t s) {
+namespace {
+
+// Whether 16-byte loads are legal for each operand of the register-staged
+// kernel. 16-byte loads need 16-byte aligned rows (ld a multiple of the vector
+// width). Along k a chunk must lie entirely inside or outside [0, K) (k
+// padding would reach every output); along m or n a chunk that starts inside
+// the extent stays inside its row, and its elements past the extent only reach
+// outputs that are not stored.
+void vector_ok(const GemmDesc& d, bool& va, bool& vb) {
   const int vw = d.dtype == F32 ? 4 : 8;
-  // 16-byte loads need 16-byte aligned rows (ld a multiple of the vector
-  // width). Along k a chunk must lie entirely inside or outside [0, K) (k
-  // padding would reach every output); along m or n a chunk that starts inside
-  // the extent stays inside its row, and its elements past the extent only
-  // reach outputs that are not stored.
-  bool va = aligned16(d.A) && d.lda % vw == 0;
-  bool vb = aligned16(d.B) && d.ldb % vw == 0;
+  va = aligned16(d.A) && d.lda % vw == 0;
+  vb = aligned16(d.B) && d.ldb % vw == 0;
   switch (d.layout) {
     case Layout::NN: va = va && d.K % vw == 0; break;
     case Layout::NT: va = va && d.K % vw == 0; vb = vb && d.K % vw == 0; break;
     case Layout::TN: break;
   }
+}
+
+gemm::Params make_params(const GemmDesc& d, const GemmPlan& pl) {
   gemm::Params p;
   p.M = d.M; p.N = d.N; p.K = d.K;
   p.A = d.A; p.lda = d.lda; p.B = d.B; p.ldb = d.ldb; p.C = d.C; p.ldc = d.ldc;
@@ -237,14 +243,46 @@ hipError_t launch_gemm(const GemmDesc& d, const GemmPlan& pl, hipStream_t s) {
   } else {
     p.a_bytes = p.b_bytes = 0;
   }
-  const unsigned grid =
-      static_cast<unsigned>(static_cast<int64_t>(pl.tiles_m) * pl.tiles_n * pl.splits);
+  return p;
+}
+
+unsigned grid_of(const GemmPlan& pl) {
+  return static_cast<unsigned>(static_cast<int64_t>(pl.tiles_m) * pl.tiles_n * pl.splits);
+}
+
+}  // namespace
+
+hipError_t launch_gemm(const GemmDesc& d, const GemmPlan& pl, hipStream_t s) {
+  bool va, vb;
+  vector_ok(d, va, vb);
+  const gemm::Params p = make_params(d, pl);
+  const unsigned grid = grid_of(pl);
   switch (d.layout) {
     case Layout::NN: return gemm::launch_nn(p, d.dtype, d.out_dtype, pl.cfg, grid, va, vb, s);
     case Layout::NT: return gemm::launch_nt(p, d.dtype, d.out_dtype, pl.cfg, grid, va, vb, s);
     case Layout::TN: return gemm::launch_tn(p, d.dtype, pl.cfg, grid, va, vb, s);
   }
   return hipErrorInvalidValue;
+}
+
+bool pairable(const GemmDesc& tn, const GemmPlan& ptn, const GemmDesc& nt, const GemmPlan& pnt) {
+  if (tn.layout != Layout::TN || nt.layout != Layout::NT || tn.dtype != nt.dtype) return false;
+  if (ptn.cfg != pnt.cfg || !gemm::pair_config(tn.dtype, ptn.cfg)) return false;
+  if (ptn.cfg < 10) {  // register-staged: 16-byte loads for all four operands
+    bool a1, b1, a2, b2;
+    vector_ok(tn, a1, b1);
+    vector_ok(nt, a2, b2);
+    if (!(a1 && b1 && a2 && b2)) return false;
+  }
+  return int64_t(grid_of(ptn)) + int64_t(grid_of(pnt)) < (int64_t(1) << 31);
+}
+
+hipError_t launch_gemm_pair(const GemmDesc& tn, const GemmPlan& ptn, const GemmDesc& nt,
+                            const GemmPlan& pnt, hipStream_t s) {
+  const gemm::Params p1 = make_params(tn, ptn), p2 = make_params(nt, pnt);
+  const unsigned n1 = grid_of(ptn);
+  return gemm::launch_pair(p1, p2, static_cast<int>(n1), n1 + grid_of(pnt), tn.dtype,
+                           nt.out_dtype, ptn.cfg, s);
 }
 
 }  // namespace dlvm

@@ -379,9 +379,11 @@ __device__ __forceinline__ void epilogue_lds(const Params& p, const f32x16 (&acc
   }
 }
 
+// One output tile (`tile` from split_slice) of the direct-to-LDS kernel, LDS
+// ring at `smem` (STAGES * (BM + BN) * 2 * BK bytes, 1024-byte aligned).
 template <typename TO, bool AK, bool BKM, int BM, int BN, int BK, int WM, int WN, int STAGES,
           int EPI>
-__global__ __launch_bounds__(64 * WM * WN) void dlvm_gemm_async_kernel(Params p) {
+__device__ __forceinline__ void async_gemm_tile(Params& p, const int tile, char* smem) {
   constexpr int NW = WM * WN;
   constexpr int THREADS = 64 * NW;
   constexpr int WTM = BM / WM, WTN = BN / WN;
@@ -393,14 +395,13 @@ __global__ __launch_bounds__(64 * WM * WN) void dlvm_gemm_async_kernel(Params p)
   static_assert(STAGES >= 2 && STAGES - 2 <= 3 && 3 * LOADS < 64, "pipeline depth");
   static_assert(AK || BM >= 128, "m-contiguous tile needs 256-byte k-rows");
   static_assert(BKM || BN >= 128, "n-contiguous tile needs 256-byte k-rows");
-  __shared__ __attribute__((aligned(1024))) char smem[STAGES * STAGE];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
   int tm, tn;
-  tile_of(split_slice<bf16_t, AK, BKM>(p), p.tiles_m, p.tiles_n, tm, tn);
+  tile_of(tile, p.tiles_m, p.tiles_n, tm, tn);
   const int64_t m0 = static_cast<int64_t>(tm) * BM;
   const int64_t n0 = static_cast<int64_t>(tn) * BN;
   const bf16_t* __restrict__ A = static_cast<const bf16_t*>(p.A);
@@ -479,6 +480,30 @@ __global__ __launch_bounds__(64 * WM * WN) void dlvm_gemm_async_kernel(Params p)
         if (lane < 32 && col < p.nvec) p.colsum[col] = t;
       }
     }
+  }
+}
+
+template <typename TO, bool AK, bool BKM, int BM, int BN, int BK, int WM, int WN, int STAGES,
+          int EPI>
+__global__ __launch_bounds__(64 * WM * WN) void dlvm_gemm_async_kernel(Params p) {
+  __shared__ __attribute__((aligned(1024))) char smem[STAGES * (BM + BN) * 2 * BK];
+  const int tile = split_slice<bf16_t, AK, BKM>(p, static_cast<int>(blockIdx.x));
+  async_gemm_tile<TO, AK, BKM, BM, BN, BK, WM, WN, STAGES, EPI>(p, tile, smem);
+}
+
+// The two adjoint products of one dense layer in one launch (blocks [0, n1):
+// TN wrt the weights, the rest: NT wrt the input), as dlvm_gemm_pair_kernel.
+template <typename TO2, int BM, int BN, int BK, int WM, int WN, int STAGES>
+__global__ __launch_bounds__(64 * WM * WN) void dlvm_gemm_async_pair_kernel(Params p1, Params p2,
+                                                                            int n1) {
+  __shared__ __attribute__((aligned(1024))) char smem[STAGES * (BM + BN) * 2 * BK];
+  const int b = static_cast<int>(blockIdx.x);
+  if (b < n1) {
+    const int tile = split_slice<bf16_t, false, false>(p1, b);
+    async_gemm_tile<float, false, false, BM, BN, BK, WM, WN, STAGES, EPI_DW>(p1, tile, smem);
+  } else {
+    const int tile = split_slice<bf16_t, true, true>(p2, b - n1);
+    async_gemm_tile<TO2, true, true, BM, BN, BK, WM, WN, STAGES, EPI_DACT>(p2, tile, smem);
   }
 }
 

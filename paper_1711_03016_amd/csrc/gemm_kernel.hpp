@@ -80,11 +80,10 @@ struct Params {
   int64_t k_chunk, c_split, cs_split;
 };
 
-// Tile index of this workgroup; with a split reduction, also narrows p to the
-// workgroup's k-slice and partial outputs.
+// Tile index of workgroup `bid` of a product; with a split reduction, also
+// narrows p to the workgroup's k-slice and partial outputs.
 template <typename T, bool AK, bool BKM>
-__device__ __forceinline__ int split_slice(Params& p) {
-  int bid = static_cast<int>(blockIdx.x);
+__device__ __forceinline__ int split_slice(Params& p, int bid) {
   if (p.splits > 1) {
     const int tiles = p.tiles_m * p.tiles_n;
     const int sl = bid / tiles;
@@ -332,9 +331,18 @@ __device__ __forceinline__ void store_block(const Params& p, const f32x16& acc, 
   }
 }
 
+// LDS bytes of one workgroup of the register-staged kernel.
+template <typename T, int BM, int BN, int WK, int KSEG>
+constexpr int gemm_smem_bytes() {
+  constexpr int stage = KSEG * (BM + BN) * kRowStride;
+  constexpr int red = (WK - 1) * BM * BN * 4;
+  return 2 * stage > red ? 2 * stage : red;
+}
+
+// One output tile of a product (`tile` from split_slice), LDS at `smem`.
 template <typename T, typename TO, bool AK, bool BKM, int BM, int BN, int WM, int WN, int WK,
           int KSEG, bool VA, bool VB, int EPI>
-__global__ __launch_bounds__(64 * WM * WN * WK) void dlvm_gemm_kernel(Params p) {
+__device__ __forceinline__ void gemm_tile(Params& p, const int tile, char* smem) {
   constexpr int THREADS = 64 * WM * WN * WK;
   constexpr int BK = Elem<T>::BK;
   constexpr int WTM = BM / WM, WTN = BN / WN;
@@ -344,9 +352,6 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void dlvm_gemm_kernel(Params p) 
   constexpr int SEG = (BM + BN) * kRowStride;        // one k-segment of A and B rows
   constexpr int STAGE = KSEG * SEG;                   // one pipeline stage
   constexpr int KSTAGE = KSEG * BK;                   // k elements per stage
-  constexpr int RED_BYTES = (WK - 1) * BM * BN * 4;  // accumulators of groups 1..WK-1
-  constexpr int SMEM = 2 * STAGE > RED_BYTES ? 2 * STAGE : RED_BYTES;
-  __shared__ __attribute__((aligned(16))) char smem[SMEM];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -357,7 +362,6 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void dlvm_gemm_kernel(Params p) 
 
   // Consecutive workgroups walk down a column of tiles, so they share the
   // B tile (the weights in the forward) through L2.
-  const int tile = split_slice<T, AK, BKM>(p);
   const int tm = tile % p.tiles_m;
   const int tn = tile / p.tiles_m;
   const int64_t m0 = static_cast<int64_t>(tm) * BM;
@@ -512,6 +516,33 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void dlvm_gemm_kernel(Params p) 
   }
 }
 
+template <typename T, typename TO, bool AK, bool BKM, int BM, int BN, int WM, int WN, int WK,
+          int KSEG, bool VA, bool VB, int EPI>
+__global__ __launch_bounds__(64 * WM * WN * WK) void dlvm_gemm_kernel(Params p) {
+  __shared__ __attribute__((aligned(16))) char smem[gemm_smem_bytes<T, BM, BN, WK, KSEG>()];
+  const int tile = split_slice<T, AK, BKM>(p, static_cast<int>(blockIdx.x));
+  gemm_tile<T, TO, AK, BKM, BM, BN, WM, WN, WK, KSEG, VA, VB, EPI>(p, tile, smem);
+}
+
+// The two adjoint products of one dense layer in one launch: blocks
+// [0, n1) are tiles of the product wrt the weights (TN, float32 dW and the
+// bias-gradient column sums), the rest tiles of the product wrt the input
+// (NT, activation-derivative epilogue). Both read the same adjoint dY; they
+// share nothing else, so the only change is one launch instead of two.
+template <typename T, typename TO2, int BM, int BN, int WM, int WN, int WK, int KSEG>
+__global__ __launch_bounds__(64 * WM * WN * WK) void dlvm_gemm_pair_kernel(Params p1, Params p2,
+                                                                           int n1) {
+  __shared__ __attribute__((aligned(16))) char smem[gemm_smem_bytes<T, BM, BN, WK, KSEG>()];
+  const int b = static_cast<int>(blockIdx.x);
+  if (b < n1) {
+    const int tile = split_slice<T, false, false>(p1, b);
+    gemm_tile<T, float, false, false, BM, BN, WM, WN, WK, KSEG, true, true, EPI_DW>(p1, tile, smem);
+  } else {
+    const int tile = split_slice<T, true, true>(p2, b - n1);
+    gemm_tile<T, TO2, true, true, BM, BN, WM, WN, WK, KSEG, true, true, EPI_DACT>(p2, tile, smem);
+  }
+}
+
 // Tile configurations: (BM, BN, waves along M, waves along N, k-step groups,
 // k-segments per stage). A stage is KSEG * 128 bytes of k per row.
 //   0: 128 x 128, 2 x 2 waves,             1 segment    large products
@@ -553,6 +584,12 @@ hipError_t launch_vec(const Params& p, int cfg, unsigned grid, bool va, bool vb,
   return vb ? launch_cfg<T, TO, AK, BKM, false, true, EPI>(p, cfg, grid, s)
             : launch_cfg<T, TO, AK, BKM, false, false, EPI>(p, cfg, grid, s);
 }
+
+// The two adjoint products of a layer (TN wrt the weights, NT wrt the input)
+// in one launch, for the configurations pair_config accepts.
+bool pair_config(int dtype, int cfg);
+hipError_t launch_pair(const Params& p1, const Params& p2, int n1, unsigned grid, int dtype,
+                       int out_dtype2, int cfg, hipStream_t s);
 
 // Per-layout entry points (one translation unit each).
 hipError_t launch_nn(const Params& p, int dtype, int out_dtype, int cfg, unsigned grid, bool va,

@@ -155,7 +155,8 @@ __global__ __launch_bounds__(256) void dlvm_gemm_xl_kernel(Params p) {
   const int wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   int tm, tn;
-  tile_of(split_slice<bf16_t, AK, BKM>(p), p.tiles_m, p.tiles_n, tm, tn);
+  tile_of(split_slice<bf16_t, AK, BKM>(p, static_cast<int>(blockIdx.x)), p.tiles_m, p.tiles_n,
+          tm, tn);
   const int64_t m0 = static_cast<int64_t>(tm) * BM;
   const int64_t n0 = static_cast<int64_t>(tn) * BN;
   const int nk = static_cast<int>((p.K + BK - 1) / BK);

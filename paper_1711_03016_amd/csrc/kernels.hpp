@@ -75,6 +75,12 @@ GemmPlan plan_gemm(const GemmDesc& d);
 // the launch error. The caller has validated shapes and pointers.
 hipError_t launch_gemm(const GemmDesc& d, const GemmPlan& plan, hipStream_t s);
 
+// The two adjoint products of one layer (tn: wrt the weights, nt: wrt the
+// input) can run as one launch when planned on the same configuration.
+bool pairable(const GemmDesc& tn, const GemmPlan& ptn, const GemmDesc& nt, const GemmPlan& pnt);
+hipError_t launch_gemm_pair(const GemmDesc& tn, const GemmPlan& ptn, const GemmDesc& nt,
+                            const GemmPlan& pnt, hipStream_t s);
+
 // Softmax cross-entropy rows: one partial loss per row block into `partials`.
 // Returns the number of partials written through *n_partials.
 // `bad` receives, per row block, the number of labels outside [0, classes).

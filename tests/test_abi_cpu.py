@@ -90,9 +90,14 @@ def test_layout_and_plan(name):
     assert plan[-1]["name"].startswith("sgd")
     # the launch plan's matrix work is exactly the workload's algorithmic flops
     assert sum(p["flops"] for p in plan) == wl.flops()
-    # dead-code elimination: no input-gradient product for layer 1 unless x is differentiated
+    # dead-code elimination: no input-gradient product for layer 1 unless x is
+    # differentiated (a paired launch holds one product wrt the weights and one
+    # wrt the input)
+    pair = [p for p in plan if p["name"].startswith("gemm_pair")]
     nt = [p for p in plan if p["name"].startswith("gemm_nt")]
-    assert len(nt) == wl.n_layers - 1 + (1 if wl.wrt_x else 0)
+    tn = [p for p in plan if p["name"].startswith("gemm_tn")]
+    assert len(nt) + len(pair) == wl.n_layers - 1 + (1 if wl.wrt_x else 0)
+    assert len(tn) + len(pair) == wl.n_layers
 
 
 def test_gradient_argument_errors_are_host_side():

@@ -16,6 +16,8 @@ comparisons use a bound of 1e-5, tight enough that a lost or doubled k-chunk
 fails. bf16 results and derivatives taken from a bf16-rounded saved output use
 the bf16 bound.
 """
+import re
+
 import numpy as np
 import pytest
 
@@ -113,7 +115,7 @@ def test_async_model_gradient(cfg):
     x, params, y = workloads.make_inputs(wl, B, seed=5)
     m = dl.Model(wl.widths, wl.acts, wl.dtype, wl.loss, False, B)
     names = [e["name"] for e in m.plan(B)]
-    assert any(n.endswith(f"c{cfg}") for n in names), names
+    assert any(re.search(rf"c{cfg}(s\d+)?$", n) for n in names), names
     dev = device()
     P = m.pack(params, dev, torch.bfloat16)
     ws = torch.empty(m.workspace_bytes(B), dtype=torch.uint8, device=dev)
