@@ -100,6 +100,20 @@ struct WsLayout {
 GemmDesc gemm_tn(int dtype, int64_t M, int64_t N, int64_t K, const void* X, const void* dY,
                  int64_t ldy, float* dW, int64_t ldw, float* db, int64_t nvec);
 
+// k-slices of the output layer's product in a gradient call (1: none). A
+// softmax head with few classes has few output tiles per batch; its
+// contraction is split so that more workgroups share it, and the slices are
+// summed (with the bias) by the softmax cross-entropy kernel that follows.
+int head_splits(const dlvm_model* m, int64_t B) {
+  if (m->loss != DLVM_LOSS_SOFTMAX_CE) return 1;
+  const int64_t C = m->widths[m->L], K = m->widths[m->L - 1];
+  if (C > 256 || K < 128) return 1;
+  const int64_t tiles = (B + 31) / 32 * ((C + 31) / 32);
+  int s = 1;
+  while (s < 8 && K / (2 * s) >= 64 && tiles * 2 * s <= 256) s *= 2;
+  return s;
+}
+
 WsLayout ws_layout(const dlvm_model* m, int64_t B) {
   WsLayout w;
   size_t off = 0;
@@ -132,6 +146,11 @@ WsLayout ws_layout(const dlvm_model* m, int64_t B) {
     const int64_t K = m->widths[l], N = m->widths[l + 1], Np = m->ldw[l];
     const GemmDesc d = gemm_tn(m->dtype, B, Np, K, nullptr, nullptr, Np, nullptr, Np, nullptr, N);
     w.splitk_elems = std::max<int64_t>(w.splitk_elems, dlvm::split_ws_elems(d));
+  }
+  const int hs = head_splits(m, B);
+  if (hs > 1) {
+    const int64_t C = m->widths[m->L];
+    w.splitk_elems = std::max<int64_t>(w.splitk_elems, int64_t(hs) * (B * C + C));
   }
   w.splitk = off;
   off = align_up(off + static_cast<size_t>(w.splitk_elems) * 4);
@@ -297,6 +316,16 @@ class Launcher {
                "split reduction launch");
   }
 
+  // One product without the reduction of its k-slices (the caller sums them).
+  dlvm_status gemm_raw(const GemmDesc& d, dlvm::GemmPlan& pl) {
+    pl = dlvm::plan_gemm(d);
+    LaunchInfo info = gemm_info(d);
+    info.name += "_" + std::to_string(pl.bm) + "x" + std::to_string(pl.bn) + "c" + std::to_string(pl.cfg);
+    if (pl.splits > 1) info.name += "s" + std::to_string(pl.splits);
+    return run(std::move(info), [&](hipStream_t s) { return dlvm::launch_gemm(d, pl, s); },
+               "gemm launch");
+  }
+
   // A layer's two adjoint products (tn: wrt the weights, nt: wrt the input):
   // one launch when both are planned on a configuration that has a paired
   // kernel, else two; then the split reduction of the product wrt the weights.
@@ -390,12 +419,11 @@ dlvm_status plan_gradient(const dlvm_model* m, const void* params, const void* x
 
   // Forward, keeping every layer output.
   const void* h = x;
-  for (int l = 0; l < L; ++l) {
-    const bool last = l == L - 1;
+  for (int l = 0; l < L - 1; ++l) {
     const int64_t N = m->widths[l + 1];
-    void* dst = last ? at<void>(ws, w.logits) : at<void>(ws, w.H[l + 1]);
-    if ((st = run.gemm(gemm_nn(dt, last ? DLVM_F32 : dt, m->acts[l], batch, N, m->widths[l], 1.0f,
-                               h, P(2 * l), m->ldw[l], P(2 * l + 1), dst, N))) != DLVM_OK)
+    void* dst = at<void>(ws, w.H[l + 1]);
+    if ((st = run.gemm(gemm_nn(dt, dt, m->acts[l], batch, N, m->widths[l], 1.0f, h, P(2 * l),
+                               m->ldw[l], P(2 * l + 1), dst, N))) != DLVM_OK)
       return st;
     h = dst;
   }
@@ -403,14 +431,35 @@ dlvm_status plan_gradient(const dlvm_model* m, const void* params, const void* x
   const int64_t ldc = m->ldw[L - 1];  // dZ_L rows are padded like W_L's
   scale = static_cast<float>(1.0 / static_cast<double>(batch));
   np = dlvm::softmax_xent_partials(batch);
-  st = run.run(elementwise_info("softmax_xent", batch, C, double(batch) * C * (4.0 + es) + 4.0 * batch),
-               [&](hipStream_t s) {
-                 int n = 0;
-                 return dlvm::launch_softmax_xent(dt, batch, C, at<float>(ws, w.logits), labels,
-                                                  scale, at<void>(ws, w.dz[L - 1]), ldc, partials,
-                                                  bad, &n, s);
-               },
-               "softmax cross-entropy launch");
+  // Output layer: logits, then softmax cross-entropy and its adjoint. A split
+  // product leaves its k-slices in the scratch; the loss kernel sums them.
+  GemmDesc head = gemm_nn(dt, DLVM_F32, DLVM_ACT_NONE, batch, C, m->widths[L - 1], 1.0f, h,
+                          P(2 * (L - 1)), m->ldw[L - 1], P(2 * L - 1), at<void>(ws, w.logits), C);
+  head.split_ws = at<float>(ws, w.splitk);
+  head.split_ws_elems = w.splitk_elems;
+  head.splits_hint = head_splits(m, batch);
+  dlvm::GemmPlan hp{};
+  if ((st = run.gemm_raw(head, hp)) != DLVM_OK) return st;
+  if (hp.splits > 1) {
+    st = run.run(elementwise_info("split_softmax_xent", batch, C,
+                                  double(batch) * C * (4.0 * hp.splits + es) + 4.0 * batch),
+                 [&](hipStream_t s) {
+                   int n = 0;
+                   return dlvm::launch_split_softmax_xent(
+                       dt, hp.splits, batch, C, head.split_ws, batch * C, C, P(2 * L - 1), labels,
+                       scale, at<void>(ws, w.dz[L - 1]), ldc, partials, bad, &n, s);
+                 },
+                 "softmax cross-entropy launch");
+  } else {
+    st = run.run(elementwise_info("softmax_xent", batch, C, double(batch) * C * (4.0 + es) + 4.0 * batch),
+                 [&](hipStream_t s) {
+                   int n = 0;
+                   return dlvm::launch_softmax_xent(dt, batch, C, at<float>(ws, w.logits), labels,
+                                                    scale, at<void>(ws, w.dz[L - 1]), ldc, partials,
+                                                    bad, &n, s);
+                 },
+                 "softmax cross-entropy launch");
+  }
   if (st != DLVM_OK) return st;
   // Adjoint sweep, last layer first. On the padded class columns dZ_L and W_L
   // are zero, so the products run over the padded width and the padding

@@ -102,6 +102,89 @@ __global__ __launch_bounds__(kBlock) void dlvm_softmax_xent_kernel(
   }
 }
 
+// Softmax cross-entropy of logits that arrive as the k-slices of a split
+// product (summed in slice order, plus the bias): one wavefront per row, each
+// lane holding up to SPL logits of its row in registers.
+template <typename TB>
+__device__ __forceinline__ float bias_at(const TB* b, int64_t j);
+template <>
+__device__ __forceinline__ float bias_at<float>(const float* b, int64_t j) { return b[j]; }
+template <>
+__device__ __forceinline__ float bias_at<bf16_t>(const bf16_t* b, int64_t j) {
+  return bf16_to_f32(b[j]);
+}
+
+template <typename TD, typename TB, int SPL>
+__global__ __launch_bounds__(kBlock) void dlvm_split_softmax_xent_kernel(
+    int S, int64_t rows, int64_t C, const float* __restrict__ part, int64_t c_split, int64_t ldp,
+    const TB* __restrict__ bias, const int32_t* __restrict__ labels, float scale,
+    TD* __restrict__ dZ, int64_t ld_dz, float* __restrict__ partials, int32_t* __restrict__ bad) {
+  __shared__ float red[kWaves];
+  __shared__ int32_t nbad[kWaves];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t row = static_cast<int64_t>(blockIdx.x) * kWaves + wave;
+  float li = 0.0f;
+  int32_t badrow = 0;
+  if (row < rows) {
+    const int32_t y = labels[row];
+    float z[SPL];
+    float m = -INFINITY, zy = 0.0f;
+#pragma unroll
+    for (int c = 0; c < SPL; ++c) {
+      const int64_t j = lane + 64 * c;
+      z[c] = -INFINITY;
+      if (j < C) {
+        float v = part[row * ldp + j];
+        for (int q = 1; q < S; ++q) v += part[q * c_split + row * ldp + j];
+        v += bias != nullptr ? bias_at<TB>(bias, j) : 0.0f;
+        z[c] = v;
+        zy = j == y ? v : zy;
+      }
+      m = fmaxf(m, z[c]);
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+      m = fmaxf(m, __shfl_xor(m, o, 64));
+      zy += __shfl_xor(zy, o, 64);  // one nonzero term: exact
+    }
+    float sum = 0.0f;
+#pragma unroll
+    for (int c = 0; c < SPL; ++c) {
+      z[c] = lane + 64 * c < C ? __expf(z[c] - m) : 0.0f;
+      sum += z[c];
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) sum += __shfl_xor(sum, o, 64);
+    const bool ok = y >= 0 && y < C;
+    badrow = ok ? 0 : 1;
+    li = ok ? (m + __logf(sum)) - zy : NAN;
+    const float ps = scale / sum;
+    TD* d = dZ + row * ld_dz;
+#pragma unroll
+    for (int c = 0; c < SPL; ++c) {
+      const int64_t j = lane + 64 * c;
+      if (j < C) d[j] = store_cast<TD>(ps * z[c] - (j == y ? scale : 0.0f));
+    }
+    for (int64_t j = C + lane; j < ld_dz; j += 64) d[j] = store_cast<TD>(0.0f);
+  }
+  if (lane == 0) {
+    red[wave] = li;
+    nbad[wave] = badrow;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float t = 0.0f;
+    int32_t b = 0;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+      t += red[w];
+      b += nbad[w];
+    }
+    partials[blockIdx.x] = t;
+    bad[blockIdx.x] = b;
+  }
+}
+
 // Rows whose logits and dlogits move as 16-byte float32 chunks (classes and
 // the dlogits row stride multiples of 4, aligned bases) and fit in registers:
 // lane l of the row's wavefront holds chunks l, l + 64, ... (NCH of them), so
@@ -581,6 +664,40 @@ hipError_t launch_splitk_reduce(int splits, int64_t rows, int64_t cols, int64_t 
   launch_kernel(dlvm_splitk_reduce_kernel, dim3(nb), dim3(kBlock), s, splits, rows, cols, ld, part,
                 c_split, out, cs_part, cs_split, colsum, nvec, vec);
   return hipGetLastError();
+}
+
+namespace {
+template <typename TD, typename TB>
+hipError_t launch_split_softmax_typed(int splits, int64_t rows, int64_t classes, const float* part,
+                                      int64_t c_split, int64_t ldp, const TB* bias,
+                                      const int32_t* labels, float scale, TD* dlogits, int64_t ld,
+                                      float* partials, int32_t* bad, int nb, hipStream_t s) {
+  const dim3 g(nb), b(kBlock);
+  if (classes <= 64)
+    launch_kernel(dlvm_split_softmax_xent_kernel<TD, TB, 1>, g, b, s, splits, rows, classes, part,
+                  c_split, ldp, bias, labels, scale, dlogits, ld, partials, bad);
+  else
+    launch_kernel(dlvm_split_softmax_xent_kernel<TD, TB, 4>, g, b, s, splits, rows, classes, part,
+                  c_split, ldp, bias, labels, scale, dlogits, ld, partials, bad);
+  return hipGetLastError();
+}
+}  // namespace
+
+hipError_t launch_split_softmax_xent(int dtype, int splits, int64_t rows, int64_t classes,
+                                     const float* part, int64_t c_split, int64_t ld_part,
+                                     const void* bias, const int32_t* labels, float scale,
+                                     void* dlogits, int64_t ld_dlogits, float* partials,
+                                     int32_t* bad, int* n_partials, hipStream_t s) {
+  if (classes > 256) return hipErrorInvalidValue;  // the callers split only narrow heads
+  const int nb = softmax_xent_partials(rows);
+  *n_partials = nb;
+  if (dtype == F32)
+    return launch_split_softmax_typed<float, float>(
+        splits, rows, classes, part, c_split, ld_part, static_cast<const float*>(bias), labels,
+        scale, static_cast<float*>(dlogits), ld_dlogits, partials, bad, nb, s);
+  return launch_split_softmax_typed<bf16_t, bf16_t>(
+      splits, rows, classes, part, c_split, ld_part, static_cast<const bf16_t*>(bias), labels,
+      scale, static_cast<bf16_t*>(dlogits), ld_dlogits, partials, bad, nb, s);
 }
 
 }  // namespace dlvm

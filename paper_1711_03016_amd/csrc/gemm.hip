@@ -160,7 +160,13 @@ GemmPlan choose(const GemmDesc& d, bool assume_aligned, int64_t capacity, int fo
     if (t.cfg == 15 && forced != 15) continue;
     if (forced >= 0 && t.cfg != forced) continue;
     for (int sp = 1; sp <= kMaxSplits; sp *= 2) {
-      if (sp > 1) {
+      if (d.splits_hint > 0 && split_need(d, d.splits_hint) <= capacity) {
+        // the caller's split (a multiple of 64 k per slice, whole slices)
+        if (sp != d.splits_hint && !(sp == 1 && d.splits_hint == 1)) {
+          if (sp > d.splits_hint) break;
+          continue;
+        }
+      } else if (sp > 1) {
         if (d.layout != Layout::TN || capacity <= 0) break;
         if (slice_k(d.K, sp) < kMinChunk || ceil_div(d.K, slice_k(d.K, sp)) < sp) break;
         if (split_need(d, sp) > capacity) break;
@@ -232,6 +238,7 @@ gemm::Params make_params(const GemmDesc& d, const GemmPlan& pl) {
     p.c_split = d.M * d.ldc;
     p.colsum = d.colsum != nullptr ? d.split_ws + pl.splits * p.c_split : nullptr;
     p.cs_split = p.nvec;
+    if (d.layout == Layout::NN) p.bias = nullptr;  // slices are raw products
   } else {
     p.c_split = p.cs_split = 0;
   }

@@ -50,9 +50,14 @@ struct GemmDesc {
   int64_t nvec;          // entries of bias / colsum (0 means N). Columns n >= nvec
                          // have none; with a padded operand they are zero.
   int64_t kvalid;        // unpadded contraction extent, for work accounting (0 means K)
-  // TN only: float32 scratch for a split reduction over K (null: no split).
+  // Float32 scratch for a split reduction over K (null: no split). The
+  // planner splits products wrt the weights (TN) by its estimate; another
+  // layout is split only when splits_hint asks for it (its caller sums the
+  // slices: an NN product's slices are the raw products, without bias or
+  // activation).
   float* split_ws;
   int64_t split_ws_elems;
+  int splits_hint;  // > 0: use exactly this many k-slices if the scratch holds them
 };
 
 // How one product is launched: tile configuration and grid.
@@ -85,6 +90,15 @@ hipError_t launch_gemm_pair(const GemmDesc& tn, const GemmPlan& ptn, const GemmD
 // Returns the number of partials written through *n_partials.
 // `bad` receives, per row block, the number of labels outside [0, classes).
 // dlogits rows have stride ld_dlogits >= classes; columns [classes, ld) are written as 0.
+// Softmax cross-entropy whose logits arrive as the k-slices of a split
+// product: z[r, c] = sum_s part[s * c_split + r * ld_part + c] (slice order)
+// + bias[c] (bias in the storage dtype `dtype`), then as launch_softmax_xent.
+hipError_t launch_split_softmax_xent(int dtype, int splits, int64_t rows, int64_t classes,
+                                     const float* part, int64_t c_split, int64_t ld_part,
+                                     const void* bias, const int32_t* labels, float scale,
+                                     void* dlogits, int64_t ld_dlogits, float* partials,
+                                     int32_t* bad, int* n_partials, hipStream_t s);
+
 hipError_t launch_softmax_xent(int dtype, int64_t rows, int64_t classes, const float* logits,
                                const int32_t* labels, float scale, void* dlogits,
                                int64_t ld_dlogits, float* partials, int32_t* bad, int* n_partials,

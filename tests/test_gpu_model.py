@@ -168,11 +168,13 @@ def test_ragged_batches(batch):
     _compare(wl, got, rl, rg, rdx, layer_tols=_order_tolerances(wl, x, params, y, rg))
 
 
-def test_label_out_of_range_is_reported():
-    wl = workloads.WORKLOADS["c1"]
+@pytest.mark.parametrize("name,bad", [("c1", 10), ("c2", 10), ("c2", -1)])
+def test_label_out_of_range_is_reported(name, bad):
+    """c2's output layer is a split product whose slices the loss kernel sums."""
+    wl = workloads.WORKLOADS[name]
     x, params, y = workloads.make_inputs(wl)
     y = y.copy()
-    y[3] = 10
+    y[3] = bad
     got = _run(wl, x, params, y, forward=False)
     assert got["status"] == dl.ERR_LABEL_RANGE
     assert np.isnan(got["loss"])
