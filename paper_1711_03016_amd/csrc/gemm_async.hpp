@@ -27,10 +27,7 @@
 //   address (they only reach outputs that are not stored). k past K is loaded
 //   from a clamped address and then zeroed in LDS before the last k-tile is
 //   multiplied.
-// * Tile order. Workgroups are dealt round-robin over the 8 XCDs; the tile
-//   index is remapped so that each XCD gets a contiguous range of tiles, and
-//   within a range tiles are visited in bands of 8 tile-rows, so workgroups
-//   running together on one XCD share A and B tiles in its L2.
+// * Tile order: tile_of (gemm_kernel.hpp), XCD-aware.
 #pragma once
 
 #include "common.hpp"
@@ -42,22 +39,6 @@ namespace gemm {
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 #define DLVM_LDS_PTR(p) ((__attribute__((address_space(3))) void*)(p))
-
-constexpr int kXcds = 8;
-
-// Tile (tm, tn) of workgroup `bid`.
-__device__ __forceinline__ void tile_of(int bid, int tiles_m, int tiles_n, int& tm, int& tn) {
-  const int nt = tiles_m * tiles_n;
-  int t = bid;
-  if (nt % kXcds == 0) t = (bid % kXcds) * (nt / kXcds) + bid / kXcds;
-  constexpr int GM = 8;
-  const int band = t / (GM * tiles_n);
-  const int first = band * GM;
-  const int rows = tiles_m - first < GM ? tiles_m - first : GM;
-  const int r = t - band * GM * tiles_n;
-  tm = first + r % rows;
-  tn = r / rows;
-}
 
 // Swizzle of a k-contiguous tile row: the 16-byte chunk c of row r sits in
 // slot c ^ kswz(r). Rows of 128 bytes (BK = 64) have 8 slots, rows of 64 bytes

@@ -103,6 +103,27 @@ __device__ __forceinline__ int split_slice(Params& p, int bid) {
   return bid;
 }
 
+// Tile order. Workgroups are dealt round-robin over the 8 XCDs, each with its
+// own L2; the tile index is remapped so that each XCD gets a contiguous range
+// of tiles, and within a range tiles are visited in bands of 8 tile-rows, so
+// the workgroups of one XCD share A and B tiles in its L2 (and each XCD reads
+// only part of each operand).
+constexpr int kXcds = 8;
+
+// Tile (tm, tn) of workgroup `bid`.
+__device__ __forceinline__ void tile_of(int bid, int tiles_m, int tiles_n, int& tm, int& tn) {
+  const int nt = tiles_m * tiles_n;
+  int t = bid;
+  if (nt % kXcds == 0) t = (bid % kXcds) * (nt / kXcds) + bid / kXcds;
+  constexpr int GM = 8;
+  const int band = t / (GM * tiles_n);
+  const int first = band * GM;
+  const int rows = tiles_m - first < GM ? tiles_m - first : GM;
+  const int r = t - band * GM * tiles_n;
+  tm = first + r % rows;
+  tn = r / rows;
+}
+
 __device__ __forceinline__ uint32_t perm_b32(uint32_t hi, uint32_t lo, uint32_t sel) {
   return __builtin_amdgcn_perm(hi, lo, sel);
 }
@@ -360,10 +381,8 @@ __device__ __forceinline__ void gemm_tile(Params& p, const int tile, char* smem)
   const int wmn = wave % (WM * WN);
   const int wm = wmn / WN, wn = wmn % WN;
 
-  // Consecutive workgroups walk down a column of tiles, so they share the
-  // B tile (the weights in the forward) through L2.
-  const int tm = tile % p.tiles_m;
-  const int tn = tile / p.tiles_m;
+  int tm, tn;
+  tile_of(tile, p.tiles_m, p.tiles_n, tm, tn);
   const int64_t m0 = static_cast<int64_t>(tm) * BM;
   const int64_t n0 = static_cast<int64_t>(tn) * BN;
 
