@@ -444,19 +444,18 @@ dlvm_status plan_gradient(const dlvm_model* m, const void* params, const void* x
     st = run.run(elementwise_info("split_softmax_xent", batch, C,
                                   double(batch) * C * (4.0 * hp.splits + es) + 4.0 * batch),
                  [&](hipStream_t s) {
-                   int n = 0;
                    return dlvm::launch_split_softmax_xent(
                        dt, hp.splits, batch, C, head.split_ws, batch * C, C, P(2 * L - 1), labels,
-                       scale, at<void>(ws, w.dz[L - 1]), ldc, partials, bad, &n, s);
+                       scale, at<void>(ws, w.dz[L - 1]), ldc, partials, bad, &np, s);
                  },
                  "softmax cross-entropy launch");
   } else {
+    // (the kernel chosen decides how many loss partials it writes)
     st = run.run(elementwise_info("softmax_xent", batch, C, double(batch) * C * (4.0 + es) + 4.0 * batch),
                  [&](hipStream_t s) {
-                   int n = 0;
                    return dlvm::launch_softmax_xent(dt, batch, C, at<float>(ws, w.logits), labels,
                                                     scale, at<void>(ws, w.dz[L - 1]), ldc, partials,
-                                                    bad, &n, s);
+                                                    bad, &np, s);
                  },
                  "softmax cross-entropy launch");
   }

@@ -201,65 +201,81 @@ __device__ __forceinline__ void store4<bf16_t>(bf16_t* p, float a, float b, floa
   uint2 o;
   o.x = static_cast<uint32_t>(f32_to_bf16(a)) | (static_cast<uint32_t>(f32_to_bf16(b)) << 16);
   o.y = static_cast<uint32_t>(f32_to_bf16(c)) | (static_cast<uint32_t>(f32_to_bf16(d)) << 16);
-  *reinterpret_cast<uint2*>(p) = o;
+  store_nt(reinterpret_cast<uint2*>(p), o);
 }
 
-template <typename TD, int NCH>
+template <typename TD, int NCH, int NR>
 __global__ __launch_bounds__(kBlock) void dlvm_softmax_xent_rows_kernel(
     int64_t rows, int64_t C, const float* __restrict__ Z, const int32_t* __restrict__ labels,
     float scale, TD* __restrict__ dZ, int64_t ld_dz, float* __restrict__ partials,
     int32_t* __restrict__ bad) {
+  // Each wavefront takes NR rows, all of whose loads are issued before the
+  // first reduction (more bytes in flight per wavefront, fewer wavefronts).
   __shared__ float red[kWaves];
   __shared__ int32_t nbad[kWaves];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int64_t row = static_cast<int64_t>(blockIdx.x) * kWaves + wave;
+  const int64_t row0 = (static_cast<int64_t>(blockIdx.x) * kWaves + wave) * NR;
+  const int64_t C4 = C / 4;
   float li = 0.0f;
   int32_t badrow = 0;
-  if (row < rows) {
-    const int64_t C4 = C / 4;
+  float4 v[NR][NCH];
+  int32_t y[NR];
+#pragma unroll
+  for (int q = 0; q < NR; ++q) {
+    const int64_t row = row0 + q;
+    y[q] = row < rows ? labels[row] : 0;
     const float4* __restrict__ z4 = reinterpret_cast<const float4*>(Z + row * C);
-    const int32_t y = labels[row];
-    float4 v[NCH];
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      const int64_t j = lane + 64 * c;
+      v[q][c] = (row < rows && j < C4)
+                    ? z4[j]
+                    : make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < NR; ++q) {
+    const int64_t row = row0 + q;
+    if (row >= rows) continue;  // uniform across the wavefront
     float m = -INFINITY;
     float zy = 0.0f;  // the label's logit, held by exactly one lane
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
-      const int64_t j = lane + 64 * c;
-      v[c] = j < C4 ? load_nt(z4 + j) : make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
-      m = fmaxf(m, fmaxf(fmaxf(v[c].x, v[c].y), fmaxf(v[c].z, v[c].w)));
-      const int64_t k = 4 * j;
-      zy = k == y ? v[c].x : k + 1 == y ? v[c].y : k + 2 == y ? v[c].z : k + 3 == y ? v[c].w : zy;
+      const float4 t = v[q][c];
+      m = fmaxf(m, fmaxf(fmaxf(t.x, t.y), fmaxf(t.z, t.w)));
+      const int64_t k = 4 * (lane + 64 * c);
+      zy = k == y[q] ? t.x : k + 1 == y[q] ? t.y : k + 2 == y[q] ? t.z : k + 3 == y[q] ? t.w : zy;
     }
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) {
       m = fmaxf(m, __shfl_xor(m, o, 64));
       zy += __shfl_xor(zy, o, 64);  // one nonzero term: exact
     }
-    float s = 0.0f;
+    float sum = 0.0f;
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
-      v[c].x = __expf(v[c].x - m);
-      v[c].y = __expf(v[c].y - m);
-      v[c].z = __expf(v[c].z - m);
-      v[c].w = __expf(v[c].w - m);
-      s += (v[c].x + v[c].y) + (v[c].z + v[c].w);
+      v[q][c].x = __expf(v[q][c].x - m);
+      v[q][c].y = __expf(v[q][c].y - m);
+      v[q][c].z = __expf(v[q][c].z - m);
+      v[q][c].w = __expf(v[q][c].w - m);
+      sum += (v[q][c].x + v[q][c].y) + (v[q][c].z + v[q][c].w);
     }
 #pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) s += __shfl_xor(s, o, 64);
-    const bool ok = y >= 0 && y < C;
-    badrow = ok ? 0 : 1;
-    li = ok ? (m + __logf(s)) - zy : NAN;
-    const float ps = scale / s;
+    for (int o = 32; o >= 1; o >>= 1) sum += __shfl_xor(sum, o, 64);
+    const bool ok = y[q] >= 0 && y[q] < C;
+    badrow += ok ? 0 : 1;
+    li += ok ? (m + __logf(sum)) - zy : NAN;
+    const float ps = scale / sum;
     TD* d = dZ + row * ld_dz;
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
       const int64_t j = lane + 64 * c;
       if (j < C4) {
         const int64_t k = 4 * j;
-        store4<TD>(d + k, ps * v[c].x - (k == y ? scale : 0.0f),
-                   ps * v[c].y - (k + 1 == y ? scale : 0.0f),
-                   ps * v[c].z - (k + 2 == y ? scale : 0.0f),
-                   ps * v[c].w - (k + 3 == y ? scale : 0.0f));
+        store4<TD>(d + k, ps * v[q][c].x - (k == y[q] ? scale : 0.0f),
+                   ps * v[q][c].y - (k + 1 == y[q] ? scale : 0.0f),
+                   ps * v[q][c].z - (k + 2 == y[q] ? scale : 0.0f),
+                   ps * v[q][c].w - (k + 3 == y[q] ? scale : 0.0f));
       }
     }
     for (int64_t j = C + lane; j < ld_dz; j += 64) d[j] = store_cast<TD>(0.0f);
@@ -510,7 +526,18 @@ __global__ __launch_bounds__(kBlock) void dlvm_splitk_reduce_kernel(
       const int64_t r = i / c4, c = (i - r * c4) * 4;
       const int64_t o = r * ld + c;
       float4 acc = load_nt(reinterpret_cast<const float4*>(part + o));
-      for (int q = 1; q < S; ++q) {
+      int q = 1;
+      for (; q + 3 < S; q += 4) {  // four slices in flight, added in slice order
+        float4 v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          v[u] = load_nt(reinterpret_cast<const float4*>(part + (q + u) * c_split + o));
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          acc.x += v[u].x; acc.y += v[u].y; acc.z += v[u].z; acc.w += v[u].w;
+        }
+      }
+      for (; q < S; ++q) {
         const float4 v = load_nt(reinterpret_cast<const float4*>(part + q * c_split + o));
         acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
       }
@@ -522,14 +549,30 @@ __global__ __launch_bounds__(kBlock) void dlvm_splitk_reduce_kernel(
       const int64_t r = i / cols, c = i - r * cols;
       const int64_t o = r * ld + c;
       float acc = part[o];
-      for (int q = 1; q < S; ++q) acc += part[q * c_split + o];
+      int q = 1;
+      for (; q + 3 < S; q += 4) {
+        float v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) v[u] = part[(q + u) * c_split + o];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) acc += v[u];
+      }
+      for (; q < S; ++q) acc += part[q * c_split + o];
       out[o] = acc;
     }
   }
   if (colsum != nullptr) {
     for (int64_t i = t0; i < nvec; i += stride) {
       float acc = cs_part[i];
-      for (int q = 1; q < S; ++q) acc += cs_part[q * cs_split + i];
+      int q = 1;
+      for (; q + 3 < S; q += 4) {
+        float v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) v[u] = cs_part[(q + u) * cs_split + i];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) acc += v[u];
+      }
+      for (; q < S; ++q) acc += cs_part[q * cs_split + i];
       colsum[i] = acc;
     }
   }
@@ -542,25 +585,29 @@ unsigned grid_for(int64_t work_items, int64_t cap) {
   return static_cast<unsigned>(b);
 }
 
+// Rows per wavefront of the register-resident kernel (its grid has
+// ceil(rows / (kWaves * NR)) blocks, each writing one loss partial).
+int softmax_rows_per_wave(int64_t chunks) { return chunks <= 4 ? 2 : 1; }
+
 template <typename TD>
 hipError_t launch_softmax_rows(int64_t chunks, int nb, int64_t rows, int64_t classes,
                                const float* logits, const int32_t* labels, float scale, TD* dlogits,
                                int64_t ld, float* partials, int32_t* bad, hipStream_t s) {
   const dim3 g(nb), b(kBlock);
   if (chunks <= 1)
-    launch_kernel(dlvm_softmax_xent_rows_kernel<TD, 1>, g, b, s, rows, classes, logits, labels,
+    launch_kernel(dlvm_softmax_xent_rows_kernel<TD, 1, 2>, g, b, s, rows, classes, logits, labels,
                   scale, dlogits, ld, partials, bad);
   else if (chunks <= 2)
-    launch_kernel(dlvm_softmax_xent_rows_kernel<TD, 2>, g, b, s, rows, classes, logits, labels,
+    launch_kernel(dlvm_softmax_xent_rows_kernel<TD, 2, 2>, g, b, s, rows, classes, logits, labels,
                   scale, dlogits, ld, partials, bad);
   else if (chunks <= 4)
-    launch_kernel(dlvm_softmax_xent_rows_kernel<TD, 4>, g, b, s, rows, classes, logits, labels,
+    launch_kernel(dlvm_softmax_xent_rows_kernel<TD, 4, 2>, g, b, s, rows, classes, logits, labels,
                   scale, dlogits, ld, partials, bad);
   else if (chunks <= 8)
-    launch_kernel(dlvm_softmax_xent_rows_kernel<TD, 8>, g, b, s, rows, classes, logits, labels,
+    launch_kernel(dlvm_softmax_xent_rows_kernel<TD, 8, 1>, g, b, s, rows, classes, logits, labels,
                   scale, dlogits, ld, partials, bad);
   else
-    launch_kernel(dlvm_softmax_xent_rows_kernel<TD, 16>, g, b, s, rows, classes, logits, labels,
+    launch_kernel(dlvm_softmax_xent_rows_kernel<TD, 16, 1>, g, b, s, rows, classes, logits, labels,
                   scale, dlogits, ld, partials, bad);
   return hipGetLastError();
 }
@@ -573,19 +620,22 @@ hipError_t launch_softmax_xent(int dtype, int64_t rows, int64_t classes, const f
                                const int32_t* labels, float scale, void* dlogits,
                                int64_t ld_dlogits, float* partials, int32_t* bad, int* n_partials,
                                hipStream_t s) {
-  const int nb = softmax_xent_partials(rows);
-  *n_partials = nb;
+  int nb = softmax_xent_partials(rows);
   const bool vec = classes % 4 == 0 && ld_dlogits % 4 == 0 &&
                    ((reinterpret_cast<uintptr_t>(logits) | reinterpret_cast<uintptr_t>(dlogits)) &
                     15u) == 0;
   const int64_t chunks = (classes / 4 + 63) / 64;  // 16-byte chunks per lane
   if (vec && chunks <= 16) {
+    const int nr = softmax_rows_per_wave(chunks);
+    nb = static_cast<int>((rows + kWaves * nr - 1) / (kWaves * nr));  // <= softmax_xent_partials
+    *n_partials = nb;
     if (dtype == F32)
       return launch_softmax_rows<float>(chunks, nb, rows, classes, logits, labels, scale,
                                         static_cast<float*>(dlogits), ld_dlogits, partials, bad, s);
     return launch_softmax_rows<bf16_t>(chunks, nb, rows, classes, logits, labels, scale,
                                        static_cast<bf16_t*>(dlogits), ld_dlogits, partials, bad, s);
   }
+  *n_partials = nb;
   if (dtype == F32)
     launch_kernel(dlvm_softmax_xent_kernel<float>, dim3(nb), dim3(kBlock), s, rows,
                        classes, logits, labels, scale, static_cast<float*>(dlogits), ld_dlogits,
