@@ -44,6 +44,10 @@ def parse():
     ap.add_argument("--workload", default="c2", choices=sorted(workloads.WORKLOADS))
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="budget of the oracle CPU baseline (0 disables it)")
+    ap.add_argument("--entry", default="gradient", choices=["gradient", "vjp"],
+                    help="gradient: dlvm_gradient (+ dlvm_sgd_step); vjp: the seedable gradient "
+                         "of the logits (dlvm_vjp) with a fixed random seed, timed on its own "
+                         "(no per-launch roofline)")
     ap.add_argument("--graph", action="store_true",
                     help="replay a captured step graph instead of enqueueing every step's "
                          "launches from the host")
@@ -155,6 +159,34 @@ def cpu_baseline(wl, budget_s: float) -> dict | None:
             "kind": "oracle", "sample": sample}
 
 
+def vjp_bench(args, wl, m, P, xd, dP, dx, ws, stream, steps, warmup):
+    """Steps of the seedable gradient of the logits (dlvm_vjp) only."""
+    import torch
+    if wl.loss != "softmax_ce":
+        raise SystemExit("--entry vjp needs a softmax workload")
+    B, C = wl.batch, wl.widths[-1]
+    g = torch.Generator(device="cpu").manual_seed(7)
+    seed = (torch.randn((B, C), generator=g) / B).to("cuda:0")
+    for _ in range(warmup):
+        m.vjp(P, xd, seed, B, dP, dx, ws, stream)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        m.vjp(P, xd, seed, B, dP, dx, ws, stream)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    sps = steps / elapsed
+    # the output layer's own product is dead in the seedable gradient
+    flops = wl.flops() - 2 * B * wl.widths[-2] * C
+    print(json.dumps({"metric": METRIC, "entry": "vjp", "value": round(sps, 3), "unit": "steps/s",
+                      "n_gpus": 1, "steps": steps, "warmup": warmup,
+                      "ms_per_step": round(elapsed / steps * 1e3, 4), "higher_is_better": True,
+                      "dtype": wl.dtype, "data": "synthetic",
+                      "config": {"workload": f"{wl.name}: {wl.title}", "global_batch": B},
+                      "tflops": round(flops * sps / 1e12, 3),
+                      "mfma_frac": round(flops * sps / 1e12 / PEAK_TFLOPS[wl.dtype], 4)}), flush=True)
+
+
 def main():
     args = parse()
     if args.copy_calibration:
@@ -196,6 +228,9 @@ def main():
         m.gradient(P, xd, yd, B, loss, dP, dx, ws, stream)
         if wl.sgd:
             m.sgd_step(P, master, dP, wl.lr, stream)
+
+    if args.entry == "vjp":
+        return vjp_bench(args, wl, m, P, xd, dP, dx, ws, stream, steps, warmup)
 
     # A step is the same launches either way; with --graph they are captured
     # once into a HIP graph and replayed.

@@ -130,6 +130,19 @@ dlvm_status dlvm_gradient(const dlvm_model* m, const void* params, const void* x
                           float* dparams, float* dx, void* ws, size_t ws_bytes,
                           void* stream);
 
+/* The seedable gradient function (Fig. 3's "seedable" declaration,
+ * [gradient @mlp wrt params (, x) seedable]) of a softmax network's logits,
+ * without the loss: given `seed`, float32 [batch, classes] (the adjoint of the
+ * logits, caller's device memory), writes dparams = seed-weighted gradient of
+ * the logits wrt the parameters (float32, flat layout, padding set to zero)
+ * and, iff wrt_x, dx (float32 [batch, widths[0]]). The hidden layers' forward
+ * is recomputed; the output layer's own product is dead (its value is not
+ * kept) and not computed. No loss, no device flags. DLVM_ERR_UNSUPPORTED for
+ * CHAIN8 models. Workspace as for dlvm_gradient. */
+dlvm_status dlvm_vjp(const dlvm_model* m, const void* params, const void* x, const float* seed,
+                     int64_t batch, float* dparams, float* dx, void* ws, size_t ws_bytes,
+                     void* stream);
+
 /* Plain SGD over the whole flat buffer in one launch: params -= lr * dparams.
  * F32 models update params in place and take master == NULL. BF16 models
  * update the float32 `master` copy and write params = bf16(master). */

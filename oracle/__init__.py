@@ -15,5 +15,5 @@ from .ad import adce, count_ops, differentiate, simplify_algebra  # noqa: F401
 from .bf16 import bf16_bits, round_to_bf16  # noqa: F401
 from .ir import Function, evaluate  # noqa: F401
 from .mlp import (MlpSpec, apply_act, chain8, dense_forward, dense_vjp_input,  # noqa: F401
-                  dense_vjp_params, gemm, mlp_forward, mlp_gradient, sgd_bf16, sgd_f32,
-                  softmax_xent)
+                  dense_vjp_params, gemm, mlp_forward, mlp_gradient, mlp_vjp, sgd_bf16,
+                  sgd_f32, softmax_xent)

@@ -20,6 +20,9 @@ Functions written here:
 * ``chain_loss(x, W, b) -> (loss, e)``: one dense layer without bias, then the
   eight-operator element-wise chain ``add bias, tanh, x0.5, +1, sigmoid,
   x x_skip, square, mean`` with ``x_skip = x``.
+* ``mlp(x, W1, b1, ..., WL, bL) -> logits``: the same layers without the loss;
+  ``mlp_vjp`` evaluates its seedable gradient declaration (the adjoint of the
+  logits given as the seed, Fig. 3).
 * ``softmax_xent(z, y)`` and ``chain8(z, b, x_skip)`` are the same losses on a
   given pre-activation tensor, for testing the loss kernels on their own.
 
@@ -160,6 +163,35 @@ def build_mlp_gradient(spec: MlpSpec, batch: int, wrt_x: bool) -> Function:
     return differentiate(f, wrt=wrt, keeping=(0,), of=0)
 
 
+@lru_cache(maxsize=64)
+def build_mlp_logits(spec: MlpSpec, batch: int) -> Function:
+    """``mlp(x, W1, b1, ..., WL, bL) -> logits``: the dense layers of ``mlp_loss``
+    without the loss (softmax cross-entropy networks only)."""
+    assert spec.loss == "softmax_ce"
+    f = Function("mlp")
+    x = f.arg((batch, spec.widths[0]), name="x")
+    h = x
+    for l, act in enumerate(spec.acts):
+        W = f.arg((spec.widths[l], spec.widths[l + 1]), name=f"W{l + 1}")
+        b = f.arg((1, spec.widths[l + 1]), name=f"b{l + 1}")
+        h = _act(f, act, f.add(f.dot(h, W, spec.accumulate), b))
+        if spec.dtype == "bf16" and spec.storage_casts and l < spec.n_layers - 1:
+            h = f.cast(h, "bf16")
+    f.ret(h)
+    return f
+
+
+@lru_cache(maxsize=64)
+def build_mlp_vjp(spec: MlpSpec, batch: int, wrt_x: bool) -> Function:
+    """Gradient declaration ``[gradient @mlp wrt params (, x) seedable]`` (Fig. 3's
+    seedable form): the seed, the adjoint of the logits, is the last argument."""
+    f = build_mlp_logits(spec, batch)
+    wrt = list(range(1, 1 + 2 * spec.n_layers))
+    if wrt_x:
+        wrt = [0] + wrt
+    return differentiate(f, wrt=wrt, seedable=True, of=0)
+
+
 def _storage(a, dtype: str) -> np.ndarray:
     """Values as the GPU stores them: float32, or float32 rounded to bf16."""
     a32 = np.asarray(a, dtype=np.float32)
@@ -174,7 +206,7 @@ def _args(spec: MlpSpec, x, params, y=None):
     for W, b in params:
         args.append(_storage(W, spec.dtype))
         args.append(_storage(np.reshape(b, (1, -1)), spec.dtype))
-    if spec.loss == "softmax_ce":
+    if spec.loss == "softmax_ce" and y is not None:
         y = np.asarray(y, dtype=np.int64).reshape(-1, 1)
         C = spec.widths[-1]
         assert y.min() >= 0 and y.max() < C, "labels must lie in [0, C)"
@@ -194,6 +226,20 @@ def mlp_forward(spec: MlpSpec, x, params, y=None):
     f = build_mlp_loss(spec, batch)
     loss, out = evaluate(f, _args(spec, x, params, y))
     return float(loss), out
+
+
+def mlp_vjp(spec: MlpSpec, x, params, seed, wrt_x: bool = False):
+    """Evaluate the seedable gradient of the logits: ([(dW, db)...], dx or None)
+    for the given adjoint ``seed`` [batch, classes] of the logits."""
+    batch = np.shape(x)[0]
+    g = build_mlp_vjp(spec, batch, bool(wrt_x))
+    args = _args(spec, x, params)
+    res = evaluate(g, args + [np.asarray(seed, np.float64)])
+    dx = None
+    if wrt_x:
+        dx, res = res[0], res[1:]
+    grads = [(res[2 * l], res[2 * l + 1].reshape(-1)) for l in range(spec.n_layers)]
+    return grads, dx
 
 
 def mlp_gradient(spec: MlpSpec, x, params, y=None, wrt_x: bool = False):

@@ -66,6 +66,7 @@ _SIGS = {
     "dlvm_forward": (_I32, [_P, _P, _P, _I64, _P, _P, ctypes.c_size_t, _P]),
     "dlvm_gradient": (_I32, [_P, _P, _P, _P, _I64, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "dlvm_sgd_step": (_I32, [_P, _P, _P, _P, _F, _P]),
+    "dlvm_vjp": (_I32, [_P, _P, _P, _P, _I64, _P, _P, _P, ctypes.c_size_t, _P]),
     "dlvm_check": (_I32, [_P, _P, _P]),
     "dlvm_last_error": (ctypes.c_char_p, []),
     "dlvm_dense_forward": (_I32, [_I32, _I32, _I32, _I64, _I64, _I64, _F, _P, _P, _P, _P, _P]),
@@ -212,6 +213,12 @@ class Model:
         _check(lib().dlvm_gradient(self._h, _ptr(params), _ptr(x), _ptr(labels), int(batch),
                                    _ptr(loss), _ptr(dparams), _ptr(dx), _ptr(ws),
                                    ws.numel() * ws.element_size(), _stream(stream)))
+
+    def vjp(self, params, x, seed, batch, dparams, dx, ws, stream=None) -> None:
+        """Seedable gradient of the logits (``dlvm_vjp``)."""
+        _check(lib().dlvm_vjp(self._h, _ptr(params), _ptr(x), _ptr(seed), int(batch),
+                              _ptr(dparams), _ptr(dx), _ptr(ws), ws.numel() * ws.element_size(),
+                              _stream(stream)))
 
     def sgd_step(self, params, master, dparams, lr: float, stream=None) -> None:
         _check(lib().dlvm_sgd_step(self._h, _ptr(params), _ptr(master), _ptr(dparams),

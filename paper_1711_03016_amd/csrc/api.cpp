@@ -361,6 +361,48 @@ class Launcher {
   int32_t index_;
 };
 
+// The adjoint of the dense layers, last first, from the adjoint of the output
+// layer's output in dz[L-1]: for each layer the products wrt its parameters
+// and wrt its input (the latter dead for the first layer unless x is
+// differentiated, section 3.1.4).
+dlvm_status plan_adjoint_layers(const dlvm_model* m, const void* params, const void* x,
+                                int64_t batch, float* dparams, float* dx, void* ws,
+                                const WsLayout& w, Launcher& run) {
+  const int L = m->L;
+  const int dt = m->dtype;
+  auto P = [&](int idx) { return param_ptr(m, params, m->offsets[idx]); };
+  auto G = [&](int idx) { return at<float>(dparams, static_cast<size_t>(m->offsets[idx]) * 4); };
+  dlvm_status st = DLVM_OK;
+  // Last layer first. On the padded class columns dZ_L and W_L
+  // are zero, so the products run over the padded width and the padding
+  // columns of dW_L come out zero.
+  for (int l = L - 1; l >= 0; --l) {
+    const void* hin = l == 0 ? x : at<void>(ws, w.H[l]);
+    const int64_t K = m->widths[l], N = m->widths[l + 1];
+    const int64_t Np = m->ldw[l];  // padded width (== N except the last layer)
+    void* dzl = at<void>(ws, w.dz[l]);
+    GemmDesc dw = gemm_tn(dt, batch, Np, K, hin, dzl, Np, G(2 * l), Np, G(2 * l + 1), N);
+    dw.split_ws = at<float>(ws, w.splitk);
+    dw.split_ws_elems = w.splitk_elems;
+    // The product wrt the input (dead for the first layer unless x is
+    // differentiated) reads the same adjoint: the two share one launch.
+    if (l > 0) {
+      GemmDesc d = gemm_nt(dt, dt, m->acts[l - 1], batch, Np, K, dzl, Np, P(2 * l), Np,
+                           at<void>(ws, w.H[l]), nullptr, at<void>(ws, w.dz[l - 1]));
+      d.kvalid = N;
+      if ((st = run.gemm_pair(dw, d)) != DLVM_OK) return st;
+    } else if (m->wrt_x) {
+      GemmDesc d = gemm_nt(dt, DLVM_F32, DLVM_ACT_NONE, batch, Np, K, dzl, Np, P(0), Np, nullptr,
+                           nullptr, dx);
+      d.kvalid = N;
+      if ((st = run.gemm_pair(dw, d)) != DLVM_OK) return st;
+    } else if ((st = run.gemm(dw)) != DLVM_OK) {
+      return st;
+    }
+  }
+  return DLVM_OK;
+}
+
 // The launches of one gradient call (section 3.1.3): forward keeping every
 // layer output, the loss adjoint, then the adjoint of each layer, last first.
 dlvm_status plan_gradient(const dlvm_model* m, const void* params, const void* x,
@@ -460,34 +502,46 @@ dlvm_status plan_gradient(const dlvm_model* m, const void* params, const void* x
                  "softmax cross-entropy launch");
   }
   if (st != DLVM_OK) return st;
-  // Adjoint sweep, last layer first. On the padded class columns dZ_L and W_L
-  // are zero, so the products run over the padded width and the padding
-  // columns of dW_L come out zero.
-  for (int l = L - 1; l >= 0; --l) {
-    const void* hin = l == 0 ? x : at<void>(ws, w.H[l]);
-    const int64_t K = m->widths[l], N = m->widths[l + 1];
-    const int64_t Np = m->ldw[l];  // padded width (== N except the last layer)
-    void* dzl = at<void>(ws, w.dz[l]);
-    GemmDesc dw = gemm_tn(dt, batch, Np, K, hin, dzl, Np, G(2 * l), Np, G(2 * l + 1), N);
-    dw.split_ws = at<float>(ws, w.splitk);
-    dw.split_ws_elems = w.splitk_elems;
-    // The product wrt the input (dead for the first layer unless x is
-    // differentiated) reads the same adjoint: the two share one launch.
-    if (l > 0) {
-      GemmDesc d = gemm_nt(dt, dt, m->acts[l - 1], batch, Np, K, dzl, Np, P(2 * l), Np,
-                           at<void>(ws, w.H[l]), nullptr, at<void>(ws, w.dz[l - 1]));
-      d.kvalid = N;
-      if ((st = run.gemm_pair(dw, d)) != DLVM_OK) return st;
-    } else if (m->wrt_x) {
-      GemmDesc d = gemm_nt(dt, DLVM_F32, DLVM_ACT_NONE, batch, Np, K, dzl, Np, P(0), Np, nullptr,
-                           nullptr, dx);
-      d.kvalid = N;
-      if ((st = run.gemm_pair(dw, d)) != DLVM_OK) return st;
-    } else if ((st = run.gemm(dw)) != DLVM_OK) {
-      return st;
-    }
-  }
+  if ((st = plan_adjoint_layers(m, params, x, batch, dparams, dx, ws, w, run)) != DLVM_OK)
+    return st;
   return finalize();
+}
+
+// The launches of one seedable gradient call (Fig. 3's seedable
+// declaration, wrt the parameters [and x]): the hidden layers' forward keeping
+// their outputs, the seed stored as the output layer's adjoint, the adjoint
+// sweep, the padding of dparams zeroed. The output layer's own product is
+// dead (its value is not kept) and is not computed.
+dlvm_status plan_vjp(const dlvm_model* m, const void* params, const void* x, const float* seed,
+                     int64_t batch, float* dparams, float* dx, void* ws, Launcher& run) {
+  const WsLayout w = ws_layout(m, batch);
+  const int L = m->L;
+  const int dt = m->dtype;
+  auto P = [&](int idx) { return param_ptr(m, params, m->offsets[idx]); };
+  dlvm_status st = DLVM_OK;
+  const void* h = x;
+  for (int l = 0; l < L - 1; ++l) {
+    const int64_t N = m->widths[l + 1];
+    void* dst = at<void>(ws, w.H[l + 1]);
+    if ((st = run.gemm(gemm_nn(dt, dt, m->acts[l], batch, N, m->widths[l], 1.0f, h, P(2 * l),
+                               m->ldw[l], P(2 * l + 1), dst, N))) != DLVM_OK)
+      return st;
+    h = dst;
+  }
+  const int64_t C = m->widths[L], ldc = m->ldw[L - 1];
+  st = run.run(elementwise_info("seed", batch, C, double(batch) * (4.0 * C + elem_size(dt) * ldc)),
+               [&](hipStream_t s) {
+                 return dlvm::launch_seed(dt, batch, C, ldc, seed, at<void>(ws, w.dz[L - 1]), s);
+               },
+               "seed launch");
+  if (st != DLVM_OK) return st;
+  if ((st = plan_adjoint_layers(m, params, x, batch, dparams, dx, ws, w, run)) != DLVM_OK) return st;
+  return run.run(elementwise_info("zero_padding", 0, 1, 4.0 * m->param_count),
+                 [&](hipStream_t s) {
+                   return dlvm::launch_finalize(nullptr, nullptr, 0, 1.0f, nullptr, nullptr, dparams,
+                                                m->gaps, s);
+                 },
+                 "padding launch");
 }
 
 // The launches of one forward call: nothing is kept; layer l's output goes to
@@ -706,6 +760,24 @@ dlvm_status dlvm_gradient(const dlvm_model* m, const void* params, const void* x
   st = plan_gradient(m, params, x, labels, batch, loss, dparams, dx, ws, run);
   m->n_grad_launches = run.launches();
   return st;
+}
+
+dlvm_status dlvm_vjp(const dlvm_model* m, const void* params, const void* x, const float* seed,
+                     int64_t batch, float* dparams, float* dx, void* ws, size_t ws_bytes,
+                     void* stream) {
+  if (m == nullptr || params == nullptr || x == nullptr || seed == nullptr || dparams == nullptr)
+    return fail(DLVM_ERR_INVALID_ARG, "null argument");
+  if (m->loss != DLVM_LOSS_SOFTMAX_CE)
+    return fail(DLVM_ERR_UNSUPPORTED, "the seedable gradient is defined for softmax networks' logits");
+  if (m->wrt_x && dx == nullptr) return fail(DLVM_ERR_INVALID_ARG, "dx is required when wrt_x");
+  if (!aligned16(params) || !aligned16(x) || !aligned16(dparams) || !aligned16(seed) ||
+      (dx && !aligned16(dx)))
+    return fail(DLVM_ERR_MISALIGNED, "device pointers must be 16-byte aligned");
+  dlvm_status st = check_batch(m, batch);
+  if (st != DLVM_OK) return st;
+  if ((st = check_ws(m, batch, ws, ws_bytes)) != DLVM_OK) return st;
+  Launcher run(m, static_cast<hipStream_t>(stream), nullptr, 0);
+  return plan_vjp(m, params, x, seed, batch, dparams, dx, ws, run);
 }
 
 dlvm_status dlvm_sgd_step(const dlvm_model* m, void* params, float* master, const float* dparams,

@@ -390,8 +390,9 @@ __global__ __launch_bounds__(kBlock) void dlvm_chain8_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// Loss finalisation: fixed-order sum of the partials, times the seed scale.
-// Also zeroes the padding gaps of the flat gradient buffer.
+// Loss finalisation: fixed-order sum of the partials, times the seed scale
+// (skipped when out is null). Also zeroes the padding gaps of the flat
+// gradient buffer.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kBlock) void dlvm_finalize_kernel(const float* __restrict__ partials,
                                                                const int32_t* __restrict__ bad,
@@ -409,7 +410,7 @@ __global__ __launch_bounds__(kBlock) void dlvm_finalize_kernel(const float* __re
   }
   const float t = block_sum(v, red);
   const float tb = block_sum(nb, redb);
-  if (threadIdx.x == 0) {
+  if (threadIdx.x == 0 && out != nullptr) {
     const float loss = t * scale;
     out[0] = loss;
     if (flags != nullptr) {
@@ -420,6 +421,23 @@ __global__ __launch_bounds__(kBlock) void dlvm_finalize_kernel(const float* __re
   if (zero_base != nullptr) {
     for (int g = 0; g < gaps.n; ++g)
       for (int i = threadIdx.x; i < gaps.len[g]; i += kBlock) zero_base[gaps.off[g] + i] = 0.0f;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// The seed of a seedable gradient (the adjoint of the output layer's output),
+// float32 [rows, C], stored as the layer's adjoint: storage dtype, row stride
+// ld >= C, columns [C, ld) zero.
+// ---------------------------------------------------------------------------
+template <typename TD>
+__global__ __launch_bounds__(kBlock) void dlvm_seed_kernel(int64_t rows, int64_t C, int64_t ld,
+                                                           const float* __restrict__ seed,
+                                                           TD* __restrict__ dz) {
+  const int64_t n = rows * ld;
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < n;
+       i += static_cast<int64_t>(gridDim.x) * kBlock) {
+    const int64_t r = i / ld, c = i - r * ld;
+    dz[i] = store_cast<TD>(c < C ? seed[r * C + c] : 0.0f);
   }
 }
 
@@ -748,6 +766,18 @@ hipError_t launch_split_softmax_xent(int dtype, int splits, int64_t rows, int64_
   return launch_split_softmax_typed<bf16_t, bf16_t>(
       splits, rows, classes, part, c_split, ld_part, static_cast<const bf16_t*>(bias), labels,
       scale, static_cast<bf16_t*>(dlogits), ld_dlogits, partials, bad, nb, s);
+}
+
+hipError_t launch_seed(int dtype, int64_t rows, int64_t classes, int64_t ld, const float* seed,
+                       void* dz, hipStream_t s) {
+  const unsigned nb = grid_for(rows * ld, 4096);
+  if (dtype == F32)
+    launch_kernel(dlvm_seed_kernel<float>, dim3(nb), dim3(kBlock), s, rows, classes, ld, seed,
+                  static_cast<float*>(dz));
+  else
+    launch_kernel(dlvm_seed_kernel<bf16_t>, dim3(nb), dim3(kBlock), s, rows, classes, ld, seed,
+                  static_cast<bf16_t*>(dz));
+  return hipGetLastError();
 }
 
 }  // namespace dlvm

@@ -113,8 +113,8 @@ int chain8_partials(int64_t rows, int64_t cols);
 
 // Sum `n` partials in a fixed order, multiply by `scale`, write *out. Writes
 // flags[0] = (any bad label counted in `bad`, which may be null) and
-// flags[1] = (loss not finite) on every call. Zeroes the `gaps` ranges of
-// `zero_base` (may be null).
+// flags[1] = (loss not finite) on every call. With out == null only zeroes.
+// Zeroes the `gaps` ranges of `zero_base` (may be null).
 struct ZeroGaps {
   static constexpr int kMax = 64;
   int n;
@@ -127,6 +127,11 @@ hipError_t launch_finalize(const float* partials, const int32_t* bad, int n, flo
 
 hipError_t launch_sgd(int dtype, int64_t n, void* params, float* master, const float* grads,
                       float lr, hipStream_t s);
+
+// dz[r, c] (row stride ld, storage dtype) = seed[r, c] for c < classes, 0 for
+// classes <= c < ld.
+hipError_t launch_seed(int dtype, int64_t rows, int64_t classes, int64_t ld, const float* seed,
+                       void* dz, hipStream_t s);
 
 // Sum of the k-slices of a split product in slice order: out[r, c] (row
 // stride ld) = sum_s part[s * c_split + r * ld + c] for c < cols, and

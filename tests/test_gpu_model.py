@@ -361,3 +361,72 @@ def test_split_batch_reduction(dtype, widths, batch):
     again = _run(wl, x, params, y, wrt_x=False, forward=False)
     for (a, b), (c, d) in zip(got["grads"], again["grads"]):
         assert np.array_equal(a, c) and np.array_equal(b, d)
+
+
+@pytest.mark.parametrize("name,batch,wrt_x", [("c1", 16, True), ("c2", 256, False), ("c2", 37, True),
+                                              ("c3", 512, False), ("c3", 300, True)])
+def test_vjp_against_oracle(name, batch, wrt_x):
+    """The seedable gradient of the logits (dlvm_vjp) for a random seed, against
+    the oracle's seedable gradient declaration."""
+    import torch
+    from dataclasses import replace
+    wl = replace(workloads.WORKLOADS[name], batch=batch)
+    x, params, _ = workloads.make_inputs(wl, bias_scale=0.1)
+    seed = (np.random.default_rng([41, batch]).standard_normal((batch, wl.widths[-1])) /
+            batch).astype(np.float32)
+    dev = device()
+    m = dl.Model(wl.widths, wl.acts, wl.dtype, wl.loss, wrt_x, batch)
+    P = m.pack(params, dev, torch_dtype(wl.dtype))
+    ws = torch.empty(m.workspace_bytes(batch), dtype=torch.uint8, device=dev)
+    dP = torch.full((m.param_count(),), float("nan"), device=dev)
+    dx = torch.empty((batch, wl.widths[0]), device=dev) if wrt_x else None
+    m.vjp(P, to_dev(x, wl.dtype), to_dev(seed), batch, dP, dx, ws)
+    torch.cuda.synchronize()
+    rg, rdx = oracle.mlp_vjp(_spec(wl), x, params, seed, wrt_x=wrt_x)
+    tol = TOL[wl.dtype]
+    for (gw, gb), (rw, rb) in zip(m.unpack(dP), rg):
+        assert rel_l2(to_np(gw), rw) <= tol
+        assert rel_l2(to_np(gb), rb) <= tol
+    if wrt_x:
+        assert rel_l2(to_np(dx), rdx) <= tol
+    # the flat buffer's padding is zero
+    offs, lds = m.param_layout_lds()
+    used = torch.zeros(m.param_count(), dtype=torch.bool, device=dev)
+    for l in range(m.n_layers):
+        K, N = wl.widths[l], wl.widths[l + 1]
+        used[offs[2 * l]:offs[2 * l] + K * lds[l]] = True
+        used[offs[2 * l + 1]:offs[2 * l + 1] + N] = True
+    assert torch.count_nonzero(dP[~used]).item() == 0
+    pad = [Wp[:, wl.widths[l + 1]:] for l, (Wp, _) in enumerate(m.unpack(dP, padded=True))]
+    assert all(torch.count_nonzero(t).item() == 0 for t in pad)
+
+
+def test_vjp_with_loss_adjoint_matches_gradient():
+    """Seeding the logits with the loss adjoint (p - onehot)/B reproduces the
+    gradient call's parameter gradient (f32 network)."""
+    import torch
+    wl = workloads.WORKLOADS["c2"]
+    x, params, y = workloads.make_inputs(wl, bias_scale=0.1)
+    got = _run(wl, x, params, y)
+    z = got["forward"]
+    p = np.exp(z - z.max(axis=1, keepdims=True))
+    p /= p.sum(axis=1, keepdims=True)
+    seed = ((p - np.eye(wl.widths[-1])[y]) / wl.batch).astype(np.float32)
+    m, P, ws = got["model"], got["P"], got["ws"]
+    dP = torch.empty(m.param_count(), device=device())
+    m.vjp(P, to_dev(x), to_dev(seed), wl.batch, dP, None, ws)
+    torch.cuda.synchronize()
+    for (a, b), (c, d) in zip(m.unpack(dP), got["grads"]):
+        assert rel_l2(to_np(a), c) <= 1e-5
+        assert rel_l2(to_np(b), d) <= 1e-5
+
+
+def test_vjp_rejects_chain_models():
+    import torch
+    wl = workloads.WORKLOADS["c4"]
+    m = dl.Model((64, 64), ("none",), "f32", "chain8", True, 8)
+    A = torch.zeros(1 << 16, device=device())
+    ws = torch.empty(m.workspace_bytes(8), dtype=torch.uint8, device=device())
+    with pytest.raises(dl.DlvmError) as e:
+        m.vjp(A, A, A, 8, A, A, ws)
+    assert e.value.status == dl.ERR_UNSUPPORTED

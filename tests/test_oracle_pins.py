@@ -20,7 +20,7 @@ import workloads
 from oracle import MlpSpec
 from oracle.ad import adce, count_ops, differentiate, simplify_algebra
 from oracle.ir import I64, Function, Instr, evaluate
-from oracle.mlp import build_mlp_gradient, build_mlp_loss
+from oracle.mlp import build_mlp_gradient, build_mlp_logits, build_mlp_loss, build_mlp_vjp
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 
@@ -630,3 +630,76 @@ def test_float32_accumulation_mode():
     a, b = rng.standard_normal((5, 7)), rng.standard_normal((7, 3))
     got, = evaluate(f, [a, b])
     np.testing.assert_array_equal(got, (a.astype(np.float32) @ b.astype(np.float32)).astype(np.float64))
+
+
+# ---------------------------------------------------------------------------
+# The seedable gradient of the logits (Fig. 3's seedable declaration)
+# ---------------------------------------------------------------------------
+def _vjp_case(seed=31):
+    spec = MlpSpec((7, 6, 5, 4), ("tanh", "sigmoid", "none"))
+    r = np.random.default_rng(seed)
+    x = r.standard_normal((3, 7))
+    params = [(r.standard_normal((spec.widths[l], spec.widths[l + 1])) * 0.6,
+               r.standard_normal(spec.widths[l + 1]) * 0.3) for l in range(3)]
+    return spec, x, params, r
+
+
+def test_vjp_adjoint_identity_by_finite_differences():
+    """<seed, J v> = <VJP(seed), v> for a random direction v over x and every
+    parameter, J v taken by central finite differences of the logits."""
+    spec, x, params, r = _vjp_case()
+    S = r.standard_normal((3, 4))
+    vx = r.standard_normal(x.shape)
+    vp = [(r.standard_normal(W.shape), r.standard_normal(b.shape)) for W, b in params]
+    h = 1e-5
+
+    # float64 arguments straight into the IR functions (no storage rounding)
+    f = build_mlp_logits(spec, 3)
+    g = build_mlp_vjp(spec, 3, True)
+
+    def flat(t):
+        a = [x + t * vx]
+        for (W, b), (dW, db) in zip(params, vp):
+            a += [W + t * dW, (b + t * db).reshape(1, -1)]
+        return a
+
+    jv = (evaluate(f, flat(h))[0] - evaluate(f, flat(-h))[0]) / (2 * h)
+    lhs = float(np.sum(S * jv))
+    res = evaluate(g, flat(0.0) + [S])
+    dx, grads = res[0], [(res[1 + 2 * l], res[2 + 2 * l].reshape(-1)) for l in range(3)]
+    rhs = float(np.sum(dx * vx)) + sum(float(np.sum(gW * dW) + np.sum(gb * db))
+                                       for (gW, gb), (dW, db) in zip(grads, vp))
+    assert abs(lhs - rhs) <= 1e-7 * max(1.0, abs(lhs)), (lhs, rhs)
+
+
+def test_vjp_is_linear_in_the_seed():
+    spec, x, params, r = _vjp_case(32)
+    S1, S2 = r.standard_normal((3, 4)), r.standard_normal((3, 4))
+    g1, d1 = oracle.mlp_vjp(spec, x, params, S1, wrt_x=True)
+    g2, d2 = oracle.mlp_vjp(spec, x, params, S2, wrt_x=True)
+    g3, d3 = oracle.mlp_vjp(spec, x, params, 2.0 * S1 - 0.5 * S2, wrt_x=True)
+    np.testing.assert_allclose(d3, 2.0 * d1 - 0.5 * d2, rtol=1e-12, atol=1e-14)
+    for (a1, b1), (a2, b2), (a3, b3) in zip(g1, g2, g3):
+        np.testing.assert_allclose(a3, 2.0 * a1 - 0.5 * a2, rtol=1e-12, atol=1e-14)
+        np.testing.assert_allclose(b3, 2.0 * b1 - 0.5 * b2, rtol=1e-12, atol=1e-14)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_vjp_with_the_loss_adjoint_is_the_loss_gradient(dtype):
+    """Chain rule: the seed (softmax(z) - onehot(y)) / B, written from its closed
+    form, turns the logits' gradient into the loss gradient."""
+    spec = MlpSpec((8, 6, 5), ("relu", "none"), dtype=dtype)
+    r = np.random.default_rng(33)
+    x = r.standard_normal((4, 8)).astype(np.float32)
+    params = [(r.standard_normal((8, 6)).astype(np.float32), r.uniform(-.3, .3, 6).astype(np.float32)),
+              (r.standard_normal((6, 5)).astype(np.float32), r.uniform(-.3, .3, 5).astype(np.float32))]
+    y = np.array([0, 4, 2, 2])
+    _, z = oracle.mlp_forward(spec, x, params, y)
+    p = np.exp(z - z.max(axis=1, keepdims=True))
+    p /= p.sum(axis=1, keepdims=True)
+    seed = (p - np.eye(5)[y]) / 4
+    gv, _ = oracle.mlp_vjp(spec, x, params, seed)
+    _, gl, _ = oracle.mlp_gradient(spec, x, params, y)
+    for (a, b), (c, d) in zip(gv, gl):
+        np.testing.assert_allclose(a, c, rtol=1e-10, atol=1e-13)
+        np.testing.assert_allclose(b, d, rtol=1e-10, atol=1e-13)
