@@ -51,6 +51,10 @@ def parse():
     ap.add_argument("--graph", action="store_true",
                     help="replay a captured step graph instead of enqueueing every step's "
                          "launches from the host")
+    ap.add_argument("--checkpoint", type=int, default=1, metavar="K",
+                    help="keep only every K-th hidden layer output and recompute the rest in "
+                         "the adjoint sweep (1: keep all); the rate still counts the "
+                         "algorithmic flops only")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (5 times) and exit: the "
                          "reference kernel for scaling the FETCH_SIZE / WRITE_SIZE counters")
@@ -211,7 +215,8 @@ def main():
     # inputs, resident in device memory before timing
     x, params, y = workloads.make_inputs(wl)
     B = wl.batch
-    m = dl.Model(wl.widths, wl.acts, wl.dtype, wl.loss, wl.wrt_x, B)
+    m = dl.Model(wl.widths, wl.acts, wl.dtype, wl.loss, wl.wrt_x, B,
+                 checkpoint_every=args.checkpoint)
     P = m.pack(params, dev, tdt)
     master = m.pack(params, dev, torch.float32) if wl.dtype == "bf16" and wl.sgd else None
     del params
@@ -314,8 +319,10 @@ def main():
         "dtype": wl.dtype,
         "data": "synthetic",
         "config": {"workload": f"{wl.name}: {wl.title}", "global_batch": B,
-                   "widths": list(wl.widths), "loss": wl.loss, "parallelism": "none"},
+                   "widths": list(wl.widths), "loss": wl.loss, "parallelism": "none",
+                   **({"checkpoint_every": args.checkpoint} if args.checkpoint > 1 else {})},
         "launch": "eager" if graph is None else "hip_graph",
+        "workspace_bytes": int(ws.numel()),
         "tflops": round(tflops, 3),
         "mfma_frac": round(tflops / PEAK_TFLOPS[wl.dtype], 4),
         "roofline": roof,

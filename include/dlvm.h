@@ -67,6 +67,11 @@ typedef struct dlvm_mlp_desc {
   int32_t loss;            /* DLVM_LOSS_SOFTMAX_CE, or DLVM_LOSS_CHAIN8 (L == 1, widths[0] == widths[1]) */
   int32_t wrt_x;           /* 1: dlvm_gradient also returns dL/dx (required for CHAIN8) */
   int64_t batch_max;       /* largest batch any call will use */
+  int32_t checkpoint_every; /* 0 or 1: keep every hidden layer output for the adjoint sweep;
+                             * k in [2, n_layers]: keep only H_l with l % k == 0 and
+                             * recompute the others, one segment at a time, during the
+                             * sweep (checkpointing, section 3.1.3). Results are bitwise
+                             * the same for every k; the workspace shrinks. */
 } dlvm_mlp_desc;
 
 typedef struct dlvm_model dlvm_model;

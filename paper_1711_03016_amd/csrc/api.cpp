@@ -48,6 +48,7 @@ struct dlvm_model {
   int32_t loss = DLVM_LOSS_SOFTMAX_CE;
   int32_t wrt_x = 0;
   int64_t batch_max = 0;
+  int32_t ckpt = 1;              // keep every ckpt-th hidden activation (1: all)
   std::vector<int64_t> offsets;  // element offsets: W_l, b_l interleaved
   std::vector<int64_t> ldw;      // row stride of W_l (N_l, or N_L rounded up to 8)
   int64_t param_count = 0;
@@ -88,7 +89,9 @@ struct WsLayout {
   size_t flags = 0;         // int32[4]: [0] label out of range, [1] non-finite loss
   size_t partials = 0;      // float32 loss partials
   size_t bad = 0;           // int32 bad-label counts, one per loss partial
-  std::vector<size_t> H;    // H[l], l = 1 .. L-1: saved layer outputs (storage dtype)
+  std::vector<size_t> H;    // H[l], l = 1 .. L-1: where layer output H_l lives (storage dtype):
+                            // its own buffer if l is a multiple of ckpt (a checkpoint), else
+                            // segment slot l % ckpt - 1, shared by the segments in turn
   size_t logits = 0;        // float32 [B, widths[L]] (logits, or z for the chain)
   std::vector<size_t> dz;   // dz[l], l = 0 .. L-1: adjoint of layer l's pre-activation output,
                             // [B, ldw[l]] (storage dtype; float32 for the chain)
@@ -127,9 +130,23 @@ WsLayout ws_layout(const dlvm_model* m, int64_t B) {
   off = align_up(off + static_cast<size_t>(np) * 4);
   const size_t es = elem_size(m->dtype);
   w.H.assign(m->L + 1, 0);
+  const int k = m->ckpt;
+  int64_t maxw = 0;
   for (int l = 1; l < m->L; ++l) {
-    w.H[l] = off;
-    off = align_up(off + static_cast<size_t>(B) * m->widths[l] * es);
+    if (l % k == 0) {
+      w.H[l] = off;
+      off = align_up(off + static_cast<size_t>(B) * m->widths[l] * es);
+    } else {
+      maxw = std::max<int64_t>(maxw, m->widths[l]);
+    }
+  }
+  if (maxw > 0) {
+    for (int j = 0; j < k - 1; ++j) {
+      const size_t slot = off;
+      off = align_up(off + static_cast<size_t>(B) * maxw * es);
+      for (int l = 1; l < m->L; ++l)
+        if (l % k == j + 1) w.H[l] = slot;
+    }
   }
   w.logits = off;
   off = align_up(off + static_cast<size_t>(B) * m->widths[m->L] * 4);
@@ -365,6 +382,36 @@ class Launcher {
 // layer's output in dz[L-1]: for each layer the products wrt its parameters
 // and wrt its input (the latter dead for the first layer unless x is
 // differentiated, section 3.1.4).
+// Forward product of layer l (0-based): H_{l+1} = act_l(H_l . W_l + b_l), from
+// where H_l lives (x for l = 0) to where H_{l+1} lives.
+dlvm_status plan_hidden_layer(const dlvm_model* m, const void* params, const void* x,
+                              int64_t batch, void* ws, const WsLayout& w, int l, Launcher& run) {
+  const int dt = m->dtype;
+  const void* in = l == 0 ? x : at<void>(ws, w.H[l]);
+  return run.gemm(gemm_nn(dt, dt, m->acts[l], batch, m->widths[l + 1], m->widths[l], 1.0f, in,
+                          param_ptr(m, params, m->offsets[2 * l]), m->ldw[l],
+                          param_ptr(m, params, m->offsets[2 * l + 1]), at<void>(ws, w.H[l + 1]),
+                          m->widths[l + 1]));
+}
+
+// The hidden layers' forward (H_1 .. H_{L-1}, each written where it lives).
+dlvm_status plan_hidden_forward(const dlvm_model* m, const void* params, const void* x,
+                                int64_t batch, void* ws, const WsLayout& w, Launcher& run) {
+  for (int l = 0; l < m->L - 1; ++l) {
+    const dlvm_status st = plan_hidden_layer(m, params, x, batch, ws, w, l, run);
+    if (st != DLVM_OK) return st;
+  }
+  return DLVM_OK;
+}
+
+// First layer of the segment whose outputs the segment slots hold after the
+// hidden layers' forward (-1: no slots).
+int resident_segment(const dlvm_model* m) {
+  for (int l = m->L - 1; l >= 1; --l)
+    if (l % m->ckpt != 0) return l - l % m->ckpt;
+  return -1;
+}
+
 dlvm_status plan_adjoint_layers(const dlvm_model* m, const void* params, const void* x,
                                 int64_t batch, float* dparams, float* dx, void* ws,
                                 const WsLayout& w, Launcher& run) {
@@ -373,10 +420,20 @@ dlvm_status plan_adjoint_layers(const dlvm_model* m, const void* params, const v
   auto P = [&](int idx) { return param_ptr(m, params, m->offsets[idx]); };
   auto G = [&](int idx) { return at<float>(dparams, static_cast<size_t>(m->offsets[idx]) * 4); };
   dlvm_status st = DLVM_OK;
+  // Checkpointing (section 3.1.3): layer l's adjoint needs H_l. A layer output
+  // that is not a checkpoint is recomputed, with the rest of its segment, from
+  // the segment's checkpoint the first time the sweep needs it.
+  int resident = resident_segment(m);
   // Last layer first. On the padded class columns dZ_L and W_L
   // are zero, so the products run over the padded width and the padding
   // columns of dW_L come out zero.
   for (int l = L - 1; l >= 0; --l) {
+    if (l > 0 && l % m->ckpt != 0 && l - l % m->ckpt != resident) {
+      const int c = l - l % m->ckpt;
+      for (int j = c; j < l; ++j)  // H_{c+1} .. H_l from H_c
+        if ((st = plan_hidden_layer(m, params, x, batch, ws, w, j, run)) != DLVM_OK) return st;
+      resident = c;
+    }
     const void* hin = l == 0 ? x : at<void>(ws, w.H[l]);
     const int64_t K = m->widths[l], N = m->widths[l + 1];
     const int64_t Np = m->ldw[l];  // padded width (== N except the last layer)
@@ -459,16 +516,10 @@ dlvm_status plan_gradient(const dlvm_model* m, const void* params, const void* x
     return finalize();
   }
 
-  // Forward, keeping every layer output.
-  const void* h = x;
-  for (int l = 0; l < L - 1; ++l) {
-    const int64_t N = m->widths[l + 1];
-    void* dst = at<void>(ws, w.H[l + 1]);
-    if ((st = run.gemm(gemm_nn(dt, dt, m->acts[l], batch, N, m->widths[l], 1.0f, h, P(2 * l),
-                               m->ldw[l], P(2 * l + 1), dst, N))) != DLVM_OK)
-      return st;
-    h = dst;
-  }
+  // Forward, keeping the layer outputs (every one, or the checkpoints and the
+  // last segment).
+  if ((st = plan_hidden_forward(m, params, x, batch, ws, w, run)) != DLVM_OK) return st;
+  const void* h = L > 1 ? at<void>(ws, w.H[L - 1]) : x;
   const int64_t C = m->widths[L];
   const int64_t ldc = m->ldw[L - 1];  // dZ_L rows are padded like W_L's
   scale = static_cast<float>(1.0 / static_cast<double>(batch));
@@ -519,15 +570,7 @@ dlvm_status plan_vjp(const dlvm_model* m, const void* params, const void* x, con
   const int dt = m->dtype;
   auto P = [&](int idx) { return param_ptr(m, params, m->offsets[idx]); };
   dlvm_status st = DLVM_OK;
-  const void* h = x;
-  for (int l = 0; l < L - 1; ++l) {
-    const int64_t N = m->widths[l + 1];
-    void* dst = at<void>(ws, w.H[l + 1]);
-    if ((st = run.gemm(gemm_nn(dt, dt, m->acts[l], batch, N, m->widths[l], 1.0f, h, P(2 * l),
-                               m->ldw[l], P(2 * l + 1), dst, N))) != DLVM_OK)
-      return st;
-    h = dst;
-  }
+  if ((st = plan_hidden_forward(m, params, x, batch, ws, w, run)) != DLVM_OK) return st;
   const int64_t C = m->widths[L], ldc = m->ldw[L - 1];
   st = run.run(elementwise_info("seed", batch, C, double(batch) * (4.0 * C + elem_size(dt) * ldc)),
                [&](hipStream_t s) {
@@ -620,6 +663,8 @@ dlvm_status dlvm_create(const dlvm_mlp_desc* desc, dlvm_model** out) {
     if (!valid_act(desc->acts[l])) return fail(DLVM_ERR_INVALID_ARG, "unknown activation");
   if (desc->acts[L - 1] != DLVM_ACT_NONE)
     return fail(DLVM_ERR_INVALID_ARG, "the last layer must have no activation");
+  if (desc->checkpoint_every < 0 || desc->checkpoint_every > L)
+    return fail(DLVM_ERR_INVALID_ARG, "checkpoint_every must be in [0, n_layers]");
   if (desc->loss == DLVM_LOSS_CHAIN8) {
     if (L != 1 || desc->widths[0] != desc->widths[1])
       return fail(DLVM_ERR_UNSUPPORTED, "the chain loss needs one layer with in == out");
@@ -640,6 +685,7 @@ dlvm_status dlvm_create(const dlvm_mlp_desc* desc, dlvm_model** out) {
   m->loss = desc->loss;
   m->wrt_x = desc->wrt_x ? 1 : 0;
   m->batch_max = desc->batch_max;
+  m->ckpt = desc->checkpoint_every > 1 ? desc->checkpoint_every : 1;
   // Flat layout: every tensor starts on a 256-byte boundary in every view
   // (storage dtype and float32 share element offsets: 128 elements is 256
   // bytes of bf16 and 512 bytes of float32).

@@ -29,11 +29,11 @@ def test_every_declared_function_is_exported():
         assert n in names
 
 
-def _desc(widths, acts, dtype=0, loss=0, wrt_x=0, batch_max=8):
+def _desc(widths, acts, dtype=0, loss=0, wrt_x=0, batch_max=8, ckpt=1):
     L = len(widths) - 1
     w = (ctypes.c_int32 * len(widths))(*widths)
     a = (ctypes.c_int32 * max(L, 1))(*acts)
-    return dl._Desc(L, w, a, dtype, loss, wrt_x, batch_max), (w, a)
+    return dl._Desc(L, w, a, dtype, loss, wrt_x, batch_max, ckpt), (w, a)
 
 
 @pytest.mark.parametrize("widths,acts,dtype,loss,wrt_x,batch_max,status", [
@@ -98,6 +98,51 @@ def test_layout_and_plan(name):
     tn = [p for p in plan if p["name"].startswith("gemm_tn")]
     assert len(nt) + len(pair) == wl.n_layers - 1 + (1 if wl.wrt_x else 0)
     assert len(tn) + len(pair) == wl.n_layers
+
+
+@pytest.mark.parametrize("ckpt,status", [(0, dl.OK), (1, dl.OK), (3, dl.OK), (4, dl.OK),
+                                         (5, dl.ERR_INVALID_ARG), (-1, dl.ERR_INVALID_ARG)])
+def test_checkpoint_every_is_validated(ckpt, status):
+    d, keep = _desc((8, 8, 8, 8, 4), (3, 3, 3, 0), ckpt=ckpt)
+    h = ctypes.c_void_p()
+    assert dl.lib().dlvm_create(ctypes.byref(d), ctypes.byref(h)) == status
+    if status == dl.OK:
+        dl.lib().dlvm_destroy(h)
+
+
+@pytest.mark.parametrize("k", [2, 3, 4, 8])
+def test_checkpoint_plan(k):
+    """Checkpointing (section 3.1.3): the sweep recomputes the hidden layer
+    outputs that are not kept, once per segment; the workspace holds the
+    checkpoints plus k-1 segment slots."""
+    wl = workloads.WORKLOADS["c5"]
+    L, B = wl.n_layers, 256
+    full = dl.Model(wl.widths, wl.acts, wl.dtype, wl.loss, wl.wrt_x, B)
+    ck = dl.Model(wl.widths, wl.acts, wl.dtype, wl.loss, wl.wrt_x, B, checkpoint_every=k)
+    p_full, p_ck = full.plan(B), ck.plan(B)
+    nn_full = [p for p in p_full if p["name"].startswith("gemm_nn")]
+    nn_ck = [p for p in p_ck if p["name"].startswith("gemm_nn")]
+    # hidden outputs H_1 .. H_{L-1}; the resident (last) segment is not redone
+    hidden = list(range(1, L))
+    last_seg = max(l - l % k for l in hidden if l % k) if any(l % k for l in hidden) else None
+    redo = 0
+    for l in hidden:
+        if l % k == 0:
+            continue
+        c = l - l % k
+        if c != last_seg and (l + 1 >= L or (l + 1) % k == 0):
+            redo += l - c   # the segment's layers c .. l-1, once
+    assert len(nn_ck) - len(nn_full) == redo
+    w = wl.widths
+    extra = sum(p["flops"] for p in nn_ck[len(nn_full):])
+    assert sum(p["flops"] for p in p_ck) - sum(p["flops"] for p in p_full) == extra
+    kept = sum(1 for l in hidden if l % k == 0)
+    slots = (k - 1) if any(l % k for l in hidden) else 0
+    saved = len(hidden) - kept - slots
+    es = 2
+    assert full.workspace_bytes(B) - ck.workspace_bytes(B) >= saved * B * w[1] * es
+    if saved > 0:
+        assert ck.workspace_bytes(B) < full.workspace_bytes(B)
 
 
 def test_gradient_argument_errors_are_host_side():

@@ -421,6 +421,62 @@ def test_vjp_with_loss_adjoint_matches_gradient():
         assert rel_l2(to_np(b), d) <= 1e-5
 
 
+def _grad_with_ckpt(wl, x, params, y, k, wrt_x, seed=None):
+    import torch
+    B = x.shape[0]
+    dev = device()
+    m = dl.Model(wl.widths, wl.acts, wl.dtype, wl.loss, wrt_x, B, checkpoint_every=k)
+    P = m.pack(params, dev, torch_dtype(wl.dtype))
+    ws = torch.full((m.workspace_bytes(B),), 0xFF, dtype=torch.uint8, device=dev)
+    dP = torch.full((m.param_count(),), float("nan"), device=dev)
+    dx = torch.empty((B, wl.widths[0]), device=dev) if wrt_x else None
+    loss = torch.zeros(1, device=dev)  # dlvm_vjp writes no loss
+    if seed is None:
+        yd = torch.from_numpy(np.asarray(y, np.int32)).to(dev)
+        m.gradient(P, to_dev(x, wl.dtype), yd, B, loss, dP, dx, ws)
+    else:
+        m.vjp(P, to_dev(x, wl.dtype), to_dev(seed), B, dP, dx, ws)
+    torch.cuda.synchronize()
+    return loss.cpu(), dP.cpu(), None if dx is None else dx.cpu()
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("entry", ["gradient", "vjp"])
+def test_checkpointing_is_bitwise_neutral(dtype, entry):
+    """Checkpointing (section 3.1.3) recomputes dropped layer outputs with the
+    same deterministic kernels: loss, parameter and input gradients are bitwise
+    those of the keep-everything plan, for every segment length."""
+    import torch
+    from dataclasses import replace
+    wl = replace(workloads.WORKLOADS["c5"], widths=(96,) + (136,) * 8 + (10,), dtype=dtype,
+                 batch=300)
+    x, params, y = workloads.make_inputs(wl, bias_scale=0.1)
+    seed = None
+    if entry == "vjp":
+        seed = (np.random.default_rng(5).standard_normal((wl.batch, 10)) / wl.batch).astype(np.float32)
+    ref = _grad_with_ckpt(wl, x, params, y, 1, True, seed)
+    assert not torch.isnan(ref[1]).any()
+    for k in (2, 3, 4, 8, 9):
+        got = _grad_with_ckpt(wl, x, params, y, k, True, seed)
+        for a, b in zip(got, ref):
+            assert torch.equal(a, b), k
+
+
+def test_checkpointing_c5_against_oracle():
+    """The c5 network (8 hidden layers of 4096) with only every third hidden
+    output kept, against the oracle at a reduced batch."""
+    wl = workloads.WORKLOADS["c5"]
+    x, params, y = workloads.make_inputs(wl, batch=64, bias_scale=0.05)
+    loss, dP, _ = _grad_with_ckpt(wl, x, params, y, 3, False)
+    rl, rg, _ = oracle.mlp_gradient(_spec(wl), x, params, y)
+    m = dl.Model(wl.widths, wl.acts, wl.dtype, wl.loss, False, 64)
+    tols = _order_tolerances(wl, x, params, y, rg)
+    assert abs(loss.item() - rl) <= TOL["bf16"] * abs(rl)
+    for (gw, gb), (rw, rb), (tw, tb) in zip(m.unpack(dP), rg, tols):
+        assert rel_l2(to_np(gw), rw) <= tw
+        assert rel_l2(to_np(gb), rb) <= tb
+
+
 def test_vjp_rejects_chain_models():
     import torch
     wl = workloads.WORKLOADS["c4"]
