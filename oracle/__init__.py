@@ -17,3 +17,4 @@ from .ir import Function, evaluate  # noqa: F401
 from .mlp import (MlpSpec, apply_act, chain8, dense_forward, dense_vjp_input,  # noqa: F401
                   dense_vjp_params, gemm, mlp_forward, mlp_gradient, mlp_vjp, sgd_bf16,
                   sgd_f32, softmax_xent)
+from .rnn import RnnSpec, rnn_forward, rnn_vjp  # noqa: F401

@@ -703,3 +703,121 @@ def test_vjp_with_the_loss_adjoint_is_the_loss_gradient(dtype):
     for (a, b), (c, d) in zip(gv, gl):
         np.testing.assert_allclose(a, c, rtol=1e-10, atol=1e-13)
         np.testing.assert_allclose(b, d, rtol=1e-10, atol=1e-13)
+
+
+# --------------------------------------------------------------------------
+# The recurrent cell (§3.1.2): oracle.rnn_forward / oracle.rnn_vjp
+# --------------------------------------------------------------------------
+def _rnn_case(T, Kx, H, B, seed=3):
+    from dataclasses import replace
+    wl = replace(workloads.RNN_WORKLOADS["r1"], steps=T, in_width=Kx, hidden=H, dtype="f32")
+    return workloads.make_rnn_inputs(wl, batch=B, seed=seed)
+
+
+@pytest.mark.parametrize("act", ["tanh", "relu"])
+def test_rnn_against_torch_rnn(act):
+    """torch.nn.RNN (float64, CPU) computes h_t = act(x_t W_ih^T + b_ih + h_{t-1}
+    W_hh^T + b_hh): an independent implementation of the same recurrence and of
+    its gradient (library autograd)."""
+    import torch
+    T, Kx, H, B = 5, 7, 6, 4
+    xs, h0, W, U, b, dhs = _rnn_case(T, Kx, H, B)
+    spec = oracle.RnnSpec(T, Kx, H, act, "f32")
+    hs = oracle.rnn_forward(spec, xs, h0, W, U, b)
+    dW, dU, db, dxs, dh0 = oracle.rnn_vjp(spec, xs, h0, W, U, b, dhs, wrt_x=True, wrt_h0=True)
+    f64 = lambda a: torch.from_numpy(np.asarray(a, np.float64))  # noqa: E731
+    rnn = torch.nn.RNN(Kx, H, nonlinearity=act, bias=True).double()
+    with torch.no_grad():
+        rnn.weight_ih_l0.copy_(f64(W).T)
+        rnn.weight_hh_l0.copy_(f64(U).T)
+        rnn.bias_ih_l0.copy_(f64(b))
+        rnn.bias_hh_l0.zero_()
+    x = f64(xs).requires_grad_()
+    h = f64(h0)[None].clone().requires_grad_()
+    out, _ = rnn(x, h)
+    np.testing.assert_allclose(hs[1:], out.detach().numpy(), rtol=1e-12, atol=1e-13)
+    np.testing.assert_array_equal(hs[0], np.asarray(h0, np.float64))
+    (out * f64(dhs)).sum().backward()
+    np.testing.assert_allclose(dW, rnn.weight_ih_l0.grad.numpy().T, rtol=1e-10, atol=1e-13)
+    np.testing.assert_allclose(dU, rnn.weight_hh_l0.grad.numpy().T, rtol=1e-10, atol=1e-13)
+    np.testing.assert_allclose(db, rnn.bias_ih_l0.grad.numpy(), rtol=1e-10, atol=1e-13)
+    np.testing.assert_allclose(dxs, x.grad.numpy(), rtol=1e-10, atol=1e-13)
+    np.testing.assert_allclose(dh0, h.grad.numpy()[0], rtol=1e-10, atol=1e-13)
+
+
+def test_rnn_linear_scalar_closed_form():
+    """act = none, Kx = H = 1: h_T = u^T h0 + sum_t u^(T-1-t) (x_t w + b), and with
+    the seed on h_T alone dL/du = T u^(T-1) h0 + sum_t (T-1-t) u^(T-2-t) c_t,
+    dL/dw = sum_t u^(T-1-t) x_t, dL/db = sum_t u^(T-1-t), dL/dh0 = u^T."""
+    T, B = 6, 3
+    rng = np.random.default_rng(11)
+    xs = rng.standard_normal((T, B, 1)).astype(np.float32)
+    h0 = rng.standard_normal((B, 1)).astype(np.float32)
+    w, u, bb = np.float32(0.7), np.float32(-0.8), np.float32(0.3)
+    dhs = np.zeros((T, B, 1), np.float32)
+    dhs[-1] = 1.0
+    spec = oracle.RnnSpec(T, 1, 1, "none", "f32")
+    W, U, b = np.array([[w]]), np.array([[u]]), np.array([bb])
+    hs = oracle.rnn_forward(spec, xs, h0, W, U, b)
+    u64, w64, b64 = float(u), float(w), float(bb)
+    x64, h64 = xs[:, :, 0].astype(np.float64), h0[:, 0].astype(np.float64)
+    c = x64 * w64 + b64                                               # c_t [T, B]
+    hT = u64 ** T * h64 + sum(u64 ** (T - 1 - t) * c[t] for t in range(T))
+    np.testing.assert_allclose(hs[-1][:, 0], hT, rtol=1e-13)
+    dW, dU, db, dxs, dh0 = oracle.rnn_vjp(spec, xs, h0, W, U, b, dhs, wrt_x=True, wrt_h0=True)
+    du = np.sum(T * u64 ** (T - 1) * h64 +
+                sum((T - 1 - t) * u64 ** (T - 2 - t) * c[t] for t in range(T - 1)))
+    dw = np.sum(sum(u64 ** (T - 1 - t) * x64[t] for t in range(T)))
+    np.testing.assert_allclose(dU[0, 0], du, rtol=1e-12)
+    np.testing.assert_allclose(dW[0, 0], dw, rtol=1e-12)
+    np.testing.assert_allclose(db[0], B * sum(u64 ** (T - 1 - t) for t in range(T)), rtol=1e-12)
+    np.testing.assert_allclose(dh0[:, 0], np.full(B, u64 ** T), rtol=1e-12)
+    np.testing.assert_allclose(dxs[:, :, 0], np.array([[w64 * u64 ** (T - 1 - t)] * B
+                                                       for t in range(T)]), rtol=1e-12)
+
+
+def test_rnn_sigmoid_single_step_and_adjoint_identity():
+    """Sigmoid cells (not in torch.nn.RNN): one step from h0 = 0 is the dense
+    layer sigmoid(x W + b) (library sigmoid), and the VJP satisfies the adjoint
+    identity <vjp(s), v> = d/de <s, h(theta + e v)> against central differences
+    of the forward."""
+    import torch
+    T, Kx, H, B = 4, 5, 6, 3
+    xs, h0, W, U, b, dhs = _rnn_case(T, Kx, H, B, seed=9)
+    spec1 = oracle.RnnSpec(1, Kx, H, "sigmoid", "f32")
+    hs1 = oracle.rnn_forward(spec1, xs[:1], np.zeros_like(h0), W, U, b)
+    ref = torch.sigmoid(torch.from_numpy(xs[0].astype(np.float64)) @
+                        torch.from_numpy(W.astype(np.float64)) + torch.from_numpy(b.astype(np.float64)))
+    np.testing.assert_allclose(hs1[1], ref.numpy(), rtol=1e-13)
+
+    spec = oracle.RnnSpec(T, Kx, H, "sigmoid", "f32")
+    dW, dU, db, dxs, dh0 = oracle.rnn_vjp(spec, xs, h0, W, U, b, dhs, wrt_x=True, wrt_h0=True)
+    rng = np.random.default_rng(4)
+    # float64 perturbations: evaluate the IR directly on float64 arguments
+    f = oracle.rnn.build_rnn(spec, B)
+    base = [np.asarray(xs[t], np.float64) for t in range(T)] + \
+        [np.asarray(a, np.float64) for a in (h0, W, U, np.reshape(b, (1, -1)))]
+    vs = [rng.standard_normal(a.shape) for a in base]
+
+    def L(e):
+        outs = evaluate(f, [a + e * v for a, v in zip(base, vs)])
+        return sum(float(np.sum(np.asarray(dhs[t], np.float64) * outs[t])) for t in range(T))
+
+    eps = 1e-5
+    fd = (L(eps) - L(-eps)) / (2 * eps)
+    grads = [dxs[t] for t in range(T)] + [dh0, dW, dU, db.reshape(1, -1)]
+    ad = sum(float(np.sum(g * v)) for g, v in zip(grads, vs))
+    assert abs(fd - ad) <= 1e-7 * max(1.0, abs(ad)), (fd, ad)
+
+
+def test_rnn_bf16_states_are_stored_as_bf16():
+    """With bf16 storage every state the oracle returns is a bf16 number, and
+    without the casts it is the exact function of the rounded inputs."""
+    T, Kx, H, B = 3, 8, 8, 4
+    xs, h0, W, U, b, dhs = _rnn_case(T, Kx, H, B)
+    hs = oracle.rnn_forward(oracle.RnnSpec(T, Kx, H, "tanh", "bf16"), xs, h0, W, U, b)
+    np.testing.assert_array_equal(oracle.round_to_bf16(hs.astype(np.float32)), hs)
+    exact = oracle.rnn_forward(oracle.RnnSpec(T, Kx, H, "tanh", "bf16", storage_casts=False),
+                               xs, h0, W, U, b)
+    assert not np.array_equal(exact, hs)
+    assert np.max(np.abs(exact - hs)) < 0.05

@@ -185,3 +185,66 @@ def scaled(wl: Workload, width_div: int = 1, batch: int | None = None) -> Worklo
             w[i] = max(1, w[i] // width_div)
     from dataclasses import replace
     return replace(wl, widths=tuple(w), batch=wl.batch if batch is None else batch)
+
+
+# ---------------------------------------------------------------------------
+# Recurrent cell (the RNN example of linear-algebra fusion): seeded inputs.
+# ---------------------------------------------------------------------------
+@dataclass(frozen=True)
+class RnnWorkload:
+    """T steps of hs[t+1] = act(xs[t] . W + hs[t] . U + b) and their seeded
+    backward pass. Inputs x ~ N(0, 1), h0 ~ U(-0.5, 0.5); the stacked [W; U]
+    has fan-in Kx + H and is drawn N(0, 1 / (Kx + H)) (pre-activations of
+    unit variance); b ~ U(-0.1, 0.1); the output adjoints dhs ~ N(0, 1) / B
+    (what a loss averaged over the batch hands back)."""
+
+    name: str
+    title: str
+    steps: int
+    in_width: int
+    hidden: int
+    act: str
+    dtype: str
+    batch: int
+    sgd: bool = True
+    lr: float = 0.01
+    wrt_x: bool = True
+    wrt_h0: bool = True
+
+    def flops(self, batch: int | None = None) -> int:
+        """Algorithmic GEMM flops of one forward + backward pass.
+
+        Forward: T products [B, Kx + H] x [Kx + H, H]. Backward: T - 1
+        recurrent products [B, H] x [H, H] (+1 for dh0), the weight gradient
+        [Kx + H, T B] x [T B, H], and dxs [T B, H] x [H, Kx] when declared.
+        """
+        B = self.batch if batch is None else batch
+        T, Kx, H = self.steps, self.in_width, self.hidden
+        fl = T * 2 * B * H * (Kx + H)
+        fl += (T - 1 + (1 if self.wrt_h0 else 0)) * 2 * B * H * H
+        fl += 2 * (Kx + H) * H * T * B
+        if self.wrt_x:
+            fl += 2 * T * B * H * Kx
+        return fl
+
+
+RNN_WORKLOADS = {
+    "r1": RnnWorkload(
+        "r1", "RNN cell bf16 tanh, T=32 steps, x 1024 -> h 1024, batch 1024, BPTT + SGD",
+        32, 1024, 1024, "tanh", "bf16", 1024),
+}
+
+
+def make_rnn_inputs(wl: RnnWorkload, batch: int | None = None, seed: int | None = None):
+    """(xs [T, B, Kx], h0 [B, H], W [Kx, H], U [H, H], b [H], dhs [T, B, H]), float32."""
+    seed = SEED_BASE if seed is None else seed
+    B = wl.batch if batch is None else batch
+    T, Kx, H = wl.steps, wl.in_width, wl.hidden
+    xs = _draw(_rng(seed, 201), (T, B, Kx), ("normal_var", 1.0))
+    h0 = _draw(_rng(seed, 202), (B, H), ("uniform", -0.5, 0.5))
+    var = ("normal_var", 1.0 / (Kx + H))
+    W = _draw(_rng(seed, 203), (Kx, H), var)
+    U = _draw(_rng(seed, 204), (H, H), var)
+    b = _draw(_rng(seed, 205), (H,), ("uniform", -0.1, 0.1))
+    dhs = _draw(_rng(seed, 206), (T, B, H), ("normal_var", 1.0)) / np.float32(B)
+    return xs, h0, W, U, b, dhs
