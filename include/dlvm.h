@@ -155,6 +155,58 @@ dlvm_status dlvm_sgd_step(const dlvm_model* m, void* params, float* master,
                           const float* dparams, float lr, void* stream);
 
 /* ---------------------------------------------------------------------------
+ * Recurrent network (section 3.1.2's RNN cell, linear-algebra fusion of a
+ * polynomial of products)
+ * ------------------------------------------------------------------------- */
+
+/* The cell h_t = f(W x_{t-1} + U h_{t-1} + b) unrolled over `steps`, in
+ * row-major batch form: hs[t+1] = act(xs[t].W + hs[t].U + b), t = 0..T-1.
+ * Each step is ONE matrix product over the concatenated contraction
+ * [xs[t] hs[t]].[W; U] with the bias add and activation fused (section
+ * 3.1.2); the parameters are stored concatenated in the first place (the
+ * interprocedural form of the fusion): the flat buffer (dlvm_param_count,
+ * dlvm_param_layout with offsets[0] = [W; U], offsets[1] = b, lds[0] = hidden)
+ * holds [W; U] as one [in_width + hidden, hidden] row-major matrix (W's rows
+ * first) and b [hidden]. The operand [xs[t] hs[t]] is not materialised. */
+typedef struct dlvm_rnn_desc {
+  int32_t dtype;       /* DLVM_F32 or DLVM_BF16 (storage of xs, hs, params, dhs) */
+  int32_t act;         /* DLVM_ACT_* of the cell */
+  int64_t steps;       /* T in [1, 4096] */
+  int64_t in_width;    /* Kx >= 1 */
+  int64_t hidden;      /* H >= 1 */
+  int64_t batch_max;   /* largest batch any call will use */
+  int32_t wrt_x;       /* 1: dlvm_rnn_backward also returns dL/dxs */
+  int32_t wrt_h0;      /* 1: dlvm_rnn_backward also returns dL/dh0 */
+} dlvm_rnn_desc;
+
+/* Create a recurrent model handle (host only). dlvm_destroy, dlvm_param_count,
+ * dlvm_param_layout, dlvm_workspace_bytes, dlvm_sgd_step, dlvm_plan_size /
+ * dlvm_plan_entry (a step is a forward call, a backward call and the update)
+ * and the timing probe take it; dlvm_forward, dlvm_gradient, dlvm_vjp and
+ * dlvm_step_graph_create return DLVM_ERR_UNSUPPORTED for it. */
+dlvm_status dlvm_rnn_create(const dlvm_rnn_desc* desc, dlvm_model** out);
+
+/* Forward over the T steps: xs [T, batch, Kx] and hs [T + 1, batch, H] in the
+ * storage dtype, caller's device memory; the caller writes the initial state
+ * into hs[0], the call writes hs[1..T] (T launches, one fused product each).
+ * hs is what dlvm_rnn_backward needs (the adjoint uses the saved outputs). */
+dlvm_status dlvm_rnn_forward(const dlvm_model* m, const void* params, const void* xs,
+                             int64_t batch, void* hs, void* stream);
+
+/* Seedable gradient of the T outputs (backpropagation through time, the
+ * adjoint of the unrolled cell, section 3.1.3): dhs [T, batch, H] (storage
+ * dtype) holds the adjoints of hs[1..T] (dhs[t] for hs[t+1]; zeros where a
+ * step's output does not reach the loss); xs and hs as written by
+ * dlvm_rnn_forward with the same params. Writes dparams (float32, flat
+ * layout: d[W; U], db; padding zero), and iff wrt_x dxs (float32 [T, batch,
+ * Kx]), iff wrt_h0 dh0 (float32 [batch, H]); neither is computed otherwise
+ * (dead code elimination, section 3.1.4). The weight gradient over all steps
+ * is one contraction over T * batch rows. `ws` needs dlvm_workspace_bytes. */
+dlvm_status dlvm_rnn_backward(const dlvm_model* m, const void* params, const void* xs,
+                              const void* hs, const void* dhs, int64_t batch, float* dparams,
+                              float* dxs, float* dh0, void* ws, size_t ws_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
  * Captured training step (HIP graph)
  * ------------------------------------------------------------------------- */
 
@@ -236,6 +288,15 @@ dlvm_status dlvm_dense_forward(int32_t dtype, int32_t out_dtype, int32_t act,
                                int64_t M, int64_t N, int64_t K, float alpha,
                                const void* X, const void* W, const void* bias,
                                void* H, void* stream);
+
+/* One recurrent cell as one fused product (section 3.1.2): Hout[M,N] =
+ * act(X[M,Kx].WU[0:Kx,:] + H[M,Kh].WU[Kx:Kx+Kh,:] + bias[N]), i.e. the product
+ * of the concatenation [X H] (read in place from the two buffers, never
+ * copied) with WU [Kx + Kh, N]. All tensors contiguous row-major, `dtype`
+ * (F32 or BF16) for inputs and output; bias may be NULL. */
+dlvm_status dlvm_rnn_cell_forward(int32_t dtype, int32_t act, int64_t M, int64_t Kx,
+                                  int64_t Kh, int64_t N, const void* X, const void* H,
+                                  const void* WU, const void* bias, void* Hout, void* stream);
 
 /* Adjoint of the dense layer with respect to its input (adjoint of dot:
  * dX = dY.W^T, transpose never materialised), fused with the adjoint of the

@@ -44,6 +44,19 @@ class _Desc(ctypes.Structure):
     ]
 
 
+class _RnnDesc(ctypes.Structure):
+    _fields_ = [
+        ("dtype", ctypes.c_int32),
+        ("act", ctypes.c_int32),
+        ("steps", ctypes.c_int64),
+        ("in_width", ctypes.c_int64),
+        ("hidden", ctypes.c_int64),
+        ("batch_max", ctypes.c_int64),
+        ("wrt_x", ctypes.c_int32),
+        ("wrt_h0", ctypes.c_int32),
+    ]
+
+
 class LaunchInfo(ctypes.Structure):
     _fields_ = [
         ("name", ctypes.c_char * 48),
@@ -85,6 +98,10 @@ _SIGS = {
     "dlvm_probe_disarm": (_I32, [_P]),
     "dlvm_step_graph_create": (_I32, [_P, _P, _P, _P, _P, _I64, _P, _P, _P, _P, ctypes.c_size_t,
                                       _I32, _F, ctypes.POINTER(_P)]),
+    "dlvm_rnn_create": (_I32, [ctypes.POINTER(_RnnDesc), ctypes.POINTER(_P)]),
+    "dlvm_rnn_forward": (_I32, [_P, _P, _P, _I64, _P, _P]),
+    "dlvm_rnn_backward": (_I32, [_P, _P, _P, _P, _P, _I64, _P, _P, _P, _P, ctypes.c_size_t, _P]),
+    "dlvm_rnn_cell_forward": (_I32, [_I32, _I32, _I64, _I64, _I64, _I64, _P, _P, _P, _P, _P, _P]),
     "dlvm_graph_launch": (_I32, [_P, _P]),
     "dlvm_graph_destroy": (None, [_P]),
 }
@@ -265,6 +282,55 @@ class Model:
         return int(lib().dlvm_check(self._h, _ptr(ws), _stream(stream)))
 
 
+class Rnn(Model):
+    """A handle on a recurrent network (see ``dlvm_rnn_create``): T steps of the
+    cell ``hs[t+1] = act(xs[t] . W + hs[t] . U + b)``, one fused product each.
+
+    The flat parameter buffer holds the stacked ``[W; U]`` ([Kx + H, H]) and
+    ``b``; ``pack_cell`` / ``split_cell`` convert from and to (W, U, b).
+    """
+
+    def __init__(self, steps: int, in_width: int, hidden: int, act: str = "tanh",
+                 dtype: str = "f32", wrt_x: bool = False, wrt_h0: bool = False,
+                 batch_max: int = 1):
+        self.steps, self.in_width, self.hidden = int(steps), int(in_width), int(hidden)
+        self.widths = (self.in_width + self.hidden, self.hidden)
+        self.acts = (act,)
+        self.dtype = dtype
+        self.loss = None
+        self.wrt_x, self.wrt_h0 = bool(wrt_x), bool(wrt_h0)
+        self.batch_max = int(batch_max)
+        self.checkpoint_every = 1
+        desc = _RnnDesc(DTYPES[dtype], ACTS[act], self.steps, self.in_width, self.hidden,
+                        self.batch_max, int(self.wrt_x), int(self.wrt_h0))
+        h = _P()
+        _check(lib().dlvm_rnn_create(ctypes.byref(desc), ctypes.byref(h)))
+        self._h = h
+
+    def pack_cell(self, W, U, b, device, torch_dtype):
+        """A flat parameter tensor holding [W; U] and b."""
+        import numpy as np
+        WU = np.concatenate([np.asarray(W), np.asarray(U)], axis=0)
+        return self.pack([(WU, np.asarray(b))], device, torch_dtype)
+
+    def split_cell(self, flat):
+        """Views (W [Kx, H], U [H, H], b [H]) into a flat parameter or gradient tensor."""
+        (WU, b), = self.unpack(flat)
+        return WU[:self.in_width], WU[self.in_width:], b
+
+    def forward(self, params, xs, batch, hs, stream=None) -> None:
+        """hs[1..T] from xs [T, batch, Kx] and hs[0] ([T + 1, batch, H] buffer)."""
+        _check(lib().dlvm_rnn_forward(self._h, _ptr(params), _ptr(xs), int(batch), _ptr(hs),
+                                      _stream(stream)))
+
+    def backward(self, params, xs, hs, dhs, batch, dparams, dxs, dh0, ws, stream=None) -> None:
+        """d[W; U], db (and dxs, dh0 when declared) for the output adjoints dhs."""
+        _check(lib().dlvm_rnn_backward(self._h, _ptr(params), _ptr(xs), _ptr(hs), _ptr(dhs),
+                                       int(batch), _ptr(dparams), _ptr(dxs), _ptr(dh0),
+                                       _ptr(ws), ws.numel() * ws.element_size(),
+                                       _stream(stream)))
+
+
 class StepGraph:
     """A captured training step; ``launch()`` enqueues one replay."""
 
@@ -289,6 +355,11 @@ def dense_forward(dtype, out_dtype, act, M, N, K, alpha, X, W, bias, H, stream=N
     _check(lib().dlvm_dense_forward(DTYPES[dtype], DTYPES[out_dtype], ACTS[act], M, N, K,
                                     float(alpha), _ptr(X), _ptr(W), _ptr(bias), _ptr(H),
                                     _stream(stream)))
+
+
+def rnn_cell_forward(dtype, act, M, Kx, Kh, N, X, H, WU, bias, Hout, stream=None):
+    _check(lib().dlvm_rnn_cell_forward(DTYPES[dtype], ACTS[act], M, Kx, Kh, N, _ptr(X), _ptr(H),
+                                       _ptr(WU), _ptr(bias), _ptr(Hout), _stream(stream)))
 
 
 def dense_backward_data(dtype, out_dtype, act_prev, M, N, K, dY, W, Hprev, R, dX, stream=None):

@@ -49,6 +49,13 @@ struct dlvm_model {
   int32_t wrt_x = 0;
   int64_t batch_max = 0;
   int32_t ckpt = 1;              // keep every ckpt-th hidden activation (1: all)
+  // Recurrent networks (kind 1): T steps of the cell
+  // hs[t+1] = act(xs[t] . W + hs[t] . U + b); L = 1 and widths = {Kx + H, H},
+  // the one "layer" being the stacked [W; U] and b.
+  int32_t kind = 0;              // 0: dense network, 1: recurrent network
+  int64_t rnn_T = 0, rnn_Kx = 0, rnn_H = 0;
+  int32_t wrt_h0 = 0;
+  mutable int32_t n_fwd_launches = 0;  // launches of a recurrent forward call
   std::vector<int64_t> offsets;  // element offsets: W_l, b_l interleaved
   std::vector<int64_t> ldw;      // row stride of W_l (N_l, or N_L rounded up to 8)
   int64_t param_count = 0;
@@ -190,10 +197,12 @@ dlvm_status check_batch(const dlvm_model* m, int64_t batch) {
   return DLVM_OK;
 }
 
+size_t ws_total(const dlvm_model* m, int64_t batch);
+
 dlvm_status check_ws(const dlvm_model* m, int64_t batch, const void* ws, size_t ws_bytes) {
   if (ws == nullptr) return fail(DLVM_ERR_WORKSPACE, "workspace is null");
   if (!aligned16(ws)) return fail(DLVM_ERR_MISALIGNED, "workspace is not 16-byte aligned");
-  if (ws_bytes < ws_layout(m, batch).total)
+  if (ws_bytes < ws_total(m, batch))
     return fail(DLVM_ERR_WORKSPACE, "workspace is smaller than dlvm_workspace_bytes");
   return DLVM_OK;
 }
@@ -624,6 +633,183 @@ dlvm_status plan_forward(const dlvm_model* m, const void* params, const void* x,
   return DLVM_OK;
 }
 
+// ---------------------------------------------------------------------------
+// Recurrent network: the cell h_t = f(W x_{t-1} + U h_{t-1} + b) of section
+// 3.1.2, unrolled over T steps (row-major batch form:
+// hs[t+1] = act(xs[t] . W + hs[t] . U + b)), with its linear-algebra fusion:
+// the polynomial of two products and two additions is one product over the
+// concatenated contraction [xs[t] hs[t]] . [W; U] + b. The parameters are
+// stored concatenated in the first place (the interprocedural form of the
+// fusion): [W; U] is one [Kx + H, H] matrix of the flat buffer. The operand
+// [xs[t] hs[t]] is never materialised: the product reads its first Kx
+// columns from xs[t] and the rest from hs[t] (a two-phase contraction).
+// ---------------------------------------------------------------------------
+struct RnnWs {
+  size_t dz = 0;          // [T, B, H] storage dtype: adjoints of the pre-activations
+  size_t splitk = 0;      // float32 partials of the split products wrt the weights
+  int64_t splitk_elems = 0;
+  size_t total = 0;
+};
+
+// The two products wrt the weights: d[W] = xs^T dz (+ db) and d[U] = hs^T dz
+// over all T * B rows at once.
+GemmDesc rnn_dw(const dlvm_model* m, int64_t B, const void* xs, const void* dz, float* dWU,
+                float* db) {
+  return gemm_tn(m->dtype, m->rnn_T * B, m->rnn_H, m->rnn_Kx, xs, dz, m->rnn_H, dWU, m->rnn_H,
+                 db, m->rnn_H);
+}
+GemmDesc rnn_du(const dlvm_model* m, int64_t B, const void* hs, const void* dz, float* dU) {
+  return gemm_tn(m->dtype, m->rnn_T * B, m->rnn_H, m->rnn_H, hs, dz, m->rnn_H, dU, m->rnn_H,
+                 nullptr, m->rnn_H);
+}
+
+RnnWs rnn_ws_layout(const dlvm_model* m, int64_t B) {
+  RnnWs w;
+  size_t off = 0;
+  w.dz = off;
+  off = align_up(off + static_cast<size_t>(m->rnn_T * B * m->rnn_H) * elem_size(m->dtype));
+  w.splitk = off;
+  w.splitk_elems = std::max(dlvm::split_ws_elems(rnn_dw(m, B, nullptr, nullptr, nullptr, nullptr)),
+                            dlvm::split_ws_elems(rnn_du(m, B, nullptr, nullptr, nullptr)));
+  off = align_up(off + static_cast<size_t>(w.splitk_elems) * 4);
+  w.total = off;
+  return w;
+}
+
+size_t ws_total(const dlvm_model* m, int64_t batch) {
+  return m->kind == 1 ? rnn_ws_layout(m, batch).total : ws_layout(m, batch).total;
+}
+
+// Row block t of a [*, B, width] sequence tensor.
+template <typename T>
+T* seq_at(T* base, int64_t t, int64_t B, int64_t width, size_t es) {
+  return at<T>(base, static_cast<size_t>(t * B * width) * es);
+}
+
+// The T fused cell products of a forward call.
+dlvm_status plan_rnn_forward(const dlvm_model* m, const void* params, const void* xs, int64_t B,
+                             void* hs, Launcher& run) {
+  const int dt = m->dtype;
+  const size_t es = elem_size(dt);
+  const int64_t Kx = m->rnn_Kx, H = m->rnn_H;
+  const void* WU = param_ptr(m, params, m->offsets[0]);
+  const void* bias = param_ptr(m, params, m->offsets[1]);
+  for (int64_t t = 0; t < m->rnn_T; ++t) {
+    GemmDesc d = gemm_nn(dt, dt, m->acts[0], B, H, Kx + H, 1.0f, seq_at(xs, t, B, Kx, es), WU, H,
+                         bias, seq_at(hs, t + 1, B, H, es), H);
+    d.lda = Kx;
+    d.A2 = seq_at(hs, t, B, H, es);
+    d.lda2 = H;
+    d.K1 = Kx;
+    const dlvm_status st = run.gemm(d);
+    if (st != DLVM_OK) return st;
+  }
+  return DLVM_OK;
+}
+
+// The launches of a backward call (backpropagation through time, the
+// adjoint of the unrolled cell, section 3.1.3), with dz[t] the adjoint of
+// cell t's pre-activation and dhs[t] the seed (direct adjoint) of hs[t+1]:
+//   dz[T-1] = dhs[T-1] * act'(hs[T])
+//   dz[t-1] = (dz[t] . U^T + dhs[t-1]) * act'(hs[t])      t = T-1 .. 1
+//   dh0 = dz[0] . U^T                                      (iff wrt_h0)
+//   [dW; dU] = [xs hs[0..T-1]]^T . dz, db = colsum(dz)    (all steps in one contraction)
+//   dxs = dz . W^T                                         (iff wrt_x)
+// The adjoint of the concatenation is the split of the product's output into
+// its W and U rows; d[W] and dxs share dz and run as one launch when they can.
+dlvm_status plan_rnn_backward(const dlvm_model* m, const void* params, const void* xs,
+                              const void* hs, const void* dhs, int64_t B, float* dparams,
+                              float* dxs, float* dh0, void* ws, Launcher& run) {
+  const RnnWs w = rnn_ws_layout(m, B);
+  const int dt = m->dtype;
+  const size_t es = elem_size(dt);
+  const int64_t T = m->rnn_T, Kx = m->rnn_Kx, H = m->rnn_H;
+  const int act = m->acts[0];
+  const void* WU = param_ptr(m, params, m->offsets[0]);
+  const void* U = at<const void>(WU, static_cast<size_t>(Kx * H) * es);
+  float* dWU = at<float>(dparams, static_cast<size_t>(m->offsets[0]) * 4);
+  float* db = at<float>(dparams, static_cast<size_t>(m->offsets[1]) * 4);
+  void* dz = at<void>(ws, w.dz);
+  dlvm_status st = run.run(
+      elementwise_info("act_adjoint", B, H, 3.0 * double(B) * H * es), [&](hipStream_t s) {
+        return dlvm::launch_act_adjoint(dt, act, B * H, seq_at(dhs, T - 1, B, H, es),
+                                        seq_at(hs, T, B, H, es), seq_at(dz, T - 1, B, H, es), s);
+      },
+      "activation adjoint launch");
+  if (st != DLVM_OK) return st;
+  for (int64_t t = T - 1; t >= 1; --t) {
+    GemmDesc d = gemm_nt(dt, dt, act, B, H, H, seq_at(dz, t, B, H, es), H, U, H,
+                         seq_at(hs, t, B, H, es), seq_at(dhs, t - 1, B, H, es),
+                         seq_at(dz, t - 1, B, H, es));
+    d.res_pre = true;
+    if ((st = run.gemm(d)) != DLVM_OK) return st;
+  }
+  if (m->wrt_h0 &&
+      (st = run.gemm(gemm_nt(dt, DLVM_F32, DLVM_ACT_NONE, B, H, H, dz, H, U, H, nullptr, nullptr,
+                             dh0))) != DLVM_OK)
+    return st;
+  GemmDesc dw = rnn_dw(m, B, xs, dz, dWU, db);
+  GemmDesc du = rnn_du(m, B, hs, dz, dWU + Kx * H);
+  for (GemmDesc* d : {&dw, &du}) {
+    d->split_ws = at<float>(ws, w.splitk);
+    d->split_ws_elems = w.splitk_elems;
+  }
+  if (m->wrt_x) {
+    st = run.gemm_pair(dw, gemm_nt(dt, DLVM_F32, DLVM_ACT_NONE, T * B, H, Kx, dz, H, WU, H,
+                                   nullptr, nullptr, dxs));
+  } else {
+    st = run.gemm(dw);
+  }
+  if (st != DLVM_OK) return st;
+  if ((st = run.gemm(du)) != DLVM_OK) return st;
+  return run.run(elementwise_info("zero_padding", 0, 1, 4.0 * m->param_count),
+                 [&](hipStream_t s) {
+                   return dlvm::launch_finalize(nullptr, nullptr, 0, 1.0f, nullptr, nullptr, dparams,
+                                                m->gaps, s);
+                 },
+                 "padding launch");
+}
+
+// The launches of one training step up to the update, without running them:
+// a gradient call (dense networks), or a forward and a backward call
+// (recurrent networks).
+void plan_step(const dlvm_model* m, int64_t batch, std::vector<LaunchInfo>* plan) {
+  Launcher dry(m, nullptr, plan, 0);
+  if (m->kind == 1) {
+    plan_rnn_forward(m, nullptr, nullptr, batch, nullptr, dry);
+    plan_rnn_backward(m, nullptr, nullptr, nullptr, nullptr, batch, nullptr, nullptr, nullptr,
+                      nullptr, dry);
+  } else {
+    plan_gradient(m, nullptr, nullptr, nullptr, batch, nullptr, nullptr, nullptr, nullptr, dry);
+  }
+}
+
+// The flat parameter layout of m->widths / m->ldw (every tensor on a 256-byte
+// boundary in every view; the gaps between tensors are recorded).
+void build_layout(dlvm_model* m) {
+  // storage dtype and float32 share element offsets: 128 elements is 256
+  // bytes of bf16 and 512 bytes of float32
+  const int64_t step = 128;
+  int64_t off = 0;
+  m->gaps.n = 0;
+  m->offsets.clear();
+  for (int l = 0; l < m->L; ++l) {
+    for (int t = 0; t < 2; ++t) {
+      const int64_t n = t == 0 ? int64_t(m->widths[l]) * m->ldw[l] : m->widths[l + 1];
+      m->offsets.push_back(off);
+      const int64_t end = off + n;
+      const int64_t next = (end + step - 1) / step * step;
+      if (next > end) {
+        m->gaps.off[m->gaps.n] = end;
+        m->gaps.len[m->gaps.n] = static_cast<int32_t>(next - end);
+        ++m->gaps.n;
+      }
+      off = next;
+    }
+  }
+  m->param_count = off;
+}
+
 LaunchInfo sgd_info(const dlvm_model* m) {
   const double per = m->dtype == DLVM_BF16 ? 14.0 : 12.0;  // master/params, grads, (shadow)
   return elementwise_info(m->dtype == DLVM_BF16 ? "sgd_bf16" : "sgd_f32", m->param_count, 1,
@@ -686,36 +872,56 @@ dlvm_status dlvm_create(const dlvm_mlp_desc* desc, dlvm_model** out) {
   m->wrt_x = desc->wrt_x ? 1 : 0;
   m->batch_max = desc->batch_max;
   m->ckpt = desc->checkpoint_every > 1 ? desc->checkpoint_every : 1;
-  // Flat layout: every tensor starts on a 256-byte boundary in every view
-  // (storage dtype and float32 share element offsets: 128 elements is 256
-  // bytes of bf16 and 512 bytes of float32).
-  const int64_t step = 128;
-  int64_t off = 0;
-  m->gaps.n = 0;
   // The class dimension of a softmax network's last weight matrix is padded
   // to a multiple of 8 (zero columns), so every row is 16-byte aligned.
   for (int l = 0; l < L; ++l) {
     const int64_t n = m->widths[l + 1];
     m->ldw.push_back(m->loss == DLVM_LOSS_SOFTMAX_CE && l == L - 1 ? (n + 7) / 8 * 8 : n);
   }
-  for (int l = 0; l < L; ++l) {
-    for (int t = 0; t < 2; ++t) {
-      const int64_t n = t == 0 ? int64_t(m->widths[l]) * m->ldw[l] : m->widths[l + 1];
-      m->offsets.push_back(off);
-      const int64_t end = off + n;
-      const int64_t next = (end + step - 1) / step * step;
-      if (next > end) {
-        m->gaps.off[m->gaps.n] = end;
-        m->gaps.len[m->gaps.n] = static_cast<int32_t>(next - end);
-        ++m->gaps.n;
-      }
-      off = next;
-    }
-  }
-  m->param_count = off;
+  build_layout(m);
+  std::vector<LaunchInfo> plan;
+  plan_step(m, 1, &plan);
+  m->n_grad_launches = static_cast<int32_t>(plan.size());
+  *out = m;
+  return DLVM_OK;
+}
+
+dlvm_status dlvm_rnn_create(const dlvm_rnn_desc* desc, dlvm_model** out) {
+  if (out == nullptr || desc == nullptr) return fail(DLVM_ERR_INVALID_ARG, "null argument");
+  *out = nullptr;
+  if (!valid_dtype(desc->dtype)) return fail(DLVM_ERR_INVALID_ARG, "unknown dtype");
+  if (!valid_act(desc->act)) return fail(DLVM_ERR_INVALID_ARG, "unknown activation");
+  if (desc->steps < 1 || desc->steps > 4096) return fail(DLVM_ERR_INVALID_ARG, "steps must be in [1, 4096]");
+  if (desc->in_width < 1 || desc->in_width > (1 << 20) || desc->hidden < 1 || desc->hidden > (1 << 20))
+    return fail(DLVM_ERR_INVALID_ARG, "in_width and hidden must be in [1, 2^20]");
+  if (desc->batch_max < 1 || desc->batch_max > (int64_t(1) << 24))
+    return fail(DLVM_ERR_INVALID_ARG, "batch_max must be in [1, 2^24]");
+  const int64_t es = static_cast<int64_t>(elem_size(desc->dtype));
+  if ((desc->in_width + desc->hidden) * desc->hidden * es > (int64_t(1) << 34) ||
+      desc->steps * desc->batch_max * std::max(desc->in_width, desc->hidden) * 4 > (int64_t(1) << 40))
+    return fail(DLVM_ERR_INVALID_ARG, "the network is too large");
+  dlvm_model* m = new (std::nothrow) dlvm_model();
+  if (m == nullptr) return fail(DLVM_ERR_INVALID_ARG, "out of host memory");
+  m->kind = 1;
+  m->L = 1;
+  m->rnn_T = desc->steps;
+  m->rnn_Kx = desc->in_width;
+  m->rnn_H = desc->hidden;
+  m->widths = {static_cast<int32_t>(desc->in_width + desc->hidden), static_cast<int32_t>(desc->hidden)};
+  m->acts = {desc->act};
+  m->dtype = desc->dtype;
+  m->loss = -1;
+  m->wrt_x = desc->wrt_x ? 1 : 0;
+  m->wrt_h0 = desc->wrt_h0 ? 1 : 0;
+  m->batch_max = desc->batch_max;
+  m->ldw = {desc->hidden};
+  build_layout(m);
   std::vector<LaunchInfo> plan;
   Launcher dry(m, nullptr, &plan, 0);
-  plan_gradient(m, nullptr, nullptr, nullptr, 1, nullptr, nullptr, nullptr, nullptr, dry);
+  plan_rnn_forward(m, nullptr, nullptr, 1, nullptr, dry);
+  m->n_fwd_launches = static_cast<int32_t>(plan.size());
+  plan.clear();
+  plan_step(m, 1, &plan);
   m->n_grad_launches = static_cast<int32_t>(plan.size());
   *out = m;
   return DLVM_OK;
@@ -738,13 +944,14 @@ dlvm_status dlvm_param_layout(const dlvm_model* m, int64_t* offsets, int64_t* ld
 
 size_t dlvm_workspace_bytes(const dlvm_model* m, int64_t batch) {
   if (m == nullptr || batch < 1 || batch > m->batch_max) return 0;
-  return ws_layout(m, batch).total;
+  return ws_total(m, batch);
 }
 
 dlvm_status dlvm_forward(const dlvm_model* m, const void* params, const void* x, int64_t batch,
                          float* out, void* ws, size_t ws_bytes, void* stream) {
   if (m == nullptr || params == nullptr || x == nullptr || out == nullptr)
     return fail(DLVM_ERR_INVALID_ARG, "null argument");
+  if (m->kind != 0) return fail(DLVM_ERR_UNSUPPORTED, "a recurrent model runs dlvm_rnn_forward");
   if (!aligned16(params) || !aligned16(x) || !aligned16(out))
     return fail(DLVM_ERR_MISALIGNED, "device pointers must be 16-byte aligned");
   dlvm_status st = check_batch(m, batch);
@@ -762,6 +969,7 @@ dlvm_status check_gradient_args(const dlvm_model* m, const void* params, const v
                                 float* dparams, float* dx, void* ws, size_t ws_bytes) {
   if (m == nullptr || params == nullptr || x == nullptr || loss == nullptr || dparams == nullptr)
     return fail(DLVM_ERR_INVALID_ARG, "null argument");
+  if (m->kind != 0) return fail(DLVM_ERR_UNSUPPORTED, "a recurrent model runs dlvm_rnn_backward");
   if (m->loss == DLVM_LOSS_SOFTMAX_CE && labels == nullptr)
     return fail(DLVM_ERR_INVALID_ARG, "labels are required for the softmax cross-entropy loss");
   if (m->wrt_x && dx == nullptr) return fail(DLVM_ERR_INVALID_ARG, "dx is required when wrt_x");
@@ -813,7 +1021,7 @@ dlvm_status dlvm_vjp(const dlvm_model* m, const void* params, const void* x, con
                      void* stream) {
   if (m == nullptr || params == nullptr || x == nullptr || seed == nullptr || dparams == nullptr)
     return fail(DLVM_ERR_INVALID_ARG, "null argument");
-  if (m->loss != DLVM_LOSS_SOFTMAX_CE)
+  if (m->kind != 0 || m->loss != DLVM_LOSS_SOFTMAX_CE)
     return fail(DLVM_ERR_UNSUPPORTED, "the seedable gradient is defined for softmax networks' logits");
   if (m->wrt_x && dx == nullptr) return fail(DLVM_ERR_INVALID_ARG, "dx is required when wrt_x");
   if (!aligned16(params) || !aligned16(x) || !aligned16(dparams) || !aligned16(seed) ||
@@ -899,8 +1107,7 @@ void dlvm_graph_destroy(dlvm_graph* g) {
 int32_t dlvm_plan_size(const dlvm_model* m, int64_t batch) {
   if (m == nullptr || batch < 1 || batch > m->batch_max) return 0;
   std::vector<LaunchInfo> plan;
-  Launcher dry(m, nullptr, &plan, 0);
-  plan_gradient(m, nullptr, nullptr, nullptr, batch, nullptr, nullptr, nullptr, nullptr, dry);
+  plan_step(m, batch, &plan);
   return static_cast<int32_t>(plan.size()) + 1;
 }
 
@@ -910,8 +1117,7 @@ dlvm_status dlvm_plan_entry(const dlvm_model* m, int64_t batch, int32_t index,
   dlvm_status st = check_batch(m, batch);
   if (st != DLVM_OK) return st;
   std::vector<LaunchInfo> plan;
-  Launcher dry(m, nullptr, &plan, 0);
-  plan_gradient(m, nullptr, nullptr, nullptr, batch, nullptr, nullptr, nullptr, nullptr, dry);
+  plan_step(m, batch, &plan);
   plan.push_back(sgd_info(m));
   if (index < 0 || index >= static_cast<int32_t>(plan.size()))
     return fail(DLVM_ERR_INVALID_ARG, "launch index out of range");
@@ -983,6 +1189,40 @@ dlvm_status dlvm_check(const dlvm_model* m, void* ws, void* stream) {
   return DLVM_OK;
 }
 
+dlvm_status dlvm_rnn_forward(const dlvm_model* m, const void* params, const void* xs,
+                             int64_t batch, void* hs, void* stream) {
+  if (m == nullptr || params == nullptr || xs == nullptr || hs == nullptr)
+    return fail(DLVM_ERR_INVALID_ARG, "null argument");
+  if (m->kind != 1) return fail(DLVM_ERR_UNSUPPORTED, "not a recurrent model");
+  if (!aligned16(params) || !aligned16(xs) || !aligned16(hs))
+    return fail(DLVM_ERR_MISALIGNED, "device pointers must be 16-byte aligned");
+  const dlvm_status st = check_batch(m, batch);
+  if (st != DLVM_OK) return st;
+  Launcher run(m, static_cast<hipStream_t>(stream), nullptr, 0);
+  return plan_rnn_forward(m, params, xs, batch, hs, run);
+}
+
+dlvm_status dlvm_rnn_backward(const dlvm_model* m, const void* params, const void* xs,
+                              const void* hs, const void* dhs, int64_t batch, float* dparams,
+                              float* dxs, float* dh0, void* ws, size_t ws_bytes, void* stream) {
+  if (m == nullptr || params == nullptr || xs == nullptr || hs == nullptr || dhs == nullptr ||
+      dparams == nullptr)
+    return fail(DLVM_ERR_INVALID_ARG, "null argument");
+  if (m->kind != 1) return fail(DLVM_ERR_UNSUPPORTED, "not a recurrent model");
+  if (m->wrt_x && dxs == nullptr) return fail(DLVM_ERR_INVALID_ARG, "dxs is required when wrt_x");
+  if (m->wrt_h0 && dh0 == nullptr) return fail(DLVM_ERR_INVALID_ARG, "dh0 is required when wrt_h0");
+  if (!aligned16(params) || !aligned16(xs) || !aligned16(hs) || !aligned16(dhs) ||
+      !aligned16(dparams) || (dxs && !aligned16(dxs)) || (dh0 && !aligned16(dh0)))
+    return fail(DLVM_ERR_MISALIGNED, "device pointers must be 16-byte aligned");
+  dlvm_status st = check_batch(m, batch);
+  if (st != DLVM_OK) return st;
+  if ((st = check_ws(m, batch, ws, ws_bytes)) != DLVM_OK) return st;
+  Launcher run(m, static_cast<hipStream_t>(stream), nullptr, m->n_fwd_launches);
+  st = plan_rnn_backward(m, params, xs, hs, dhs, batch, dparams, dxs, dh0, ws, run);
+  m->n_grad_launches = run.launches();
+  return st;
+}
+
 // ---------------------------------------------------------------------------
 // Step-level entry points
 // ---------------------------------------------------------------------------
@@ -999,6 +1239,24 @@ dlvm_status dlvm_dense_forward(int32_t dtype, int32_t out_dtype, int32_t act, in
     return fail(DLVM_ERR_MISALIGNED, "device pointers must be 16-byte aligned");
   return run_gemm(gemm_nn(dtype, out_dtype, act, M, N, K, alpha, X, W, N, bias, H, N),
                   static_cast<hipStream_t>(stream));
+}
+
+dlvm_status dlvm_rnn_cell_forward(int32_t dtype, int32_t act, int64_t M, int64_t Kx, int64_t Kh,
+                                  int64_t N, const void* X, const void* H, const void* WU,
+                                  const void* bias, void* Hout, void* stream) {
+  if (!valid_dtype(dtype) || !valid_act(act)) return fail(DLVM_ERR_INVALID_ARG, "bad dtype or activation");
+  if (M < 1 || Kx < 1 || Kh < 1 || N < 1) return fail(DLVM_ERR_INVALID_ARG, "sizes must be positive");
+  if (X == nullptr || H == nullptr || WU == nullptr || Hout == nullptr)
+    return fail(DLVM_ERR_INVALID_ARG, "null argument");
+  if (!aligned16(X) || !aligned16(H) || !aligned16(WU) || !aligned16(Hout) ||
+      (bias && !aligned16(bias)))
+    return fail(DLVM_ERR_MISALIGNED, "device pointers must be 16-byte aligned");
+  GemmDesc d = gemm_nn(dtype, dtype, act, M, N, Kx + Kh, 1.0f, X, WU, N, bias, Hout, N);
+  d.lda = Kx;
+  d.A2 = H;
+  d.lda2 = Kh;
+  d.K1 = Kx;
+  return run_gemm(d, static_cast<hipStream_t>(stream));
 }
 
 dlvm_status dlvm_dense_backward_data(int32_t dtype, int32_t out_dtype, int32_t act_prev, int64_t M,

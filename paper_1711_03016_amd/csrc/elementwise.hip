@@ -442,6 +442,23 @@ __global__ __launch_bounds__(kBlock) void dlvm_seed_kernel(int64_t rows, int64_t
 }
 
 // ---------------------------------------------------------------------------
+// Adjoint of an element-wise activation through its saved output:
+// out = g * act'(h), act' taken from h = act(z) (storage dtype throughout).
+// ---------------------------------------------------------------------------
+template <typename TD>
+__global__ __launch_bounds__(kBlock) void dlvm_act_adjoint_kernel(int64_t n, int act,
+                                                                  const TD* __restrict__ g,
+                                                                  const TD* __restrict__ h,
+                                                                  TD* __restrict__ out) {
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < n;
+       i += static_cast<int64_t>(gridDim.x) * kBlock) {
+    float v = load_as_f32<TD>(g + i);
+    if (act != ACT_NONE) v *= act_grad_from_output(act, load_as_f32<TD>(h + i));
+    out[i] = store_cast<TD>(v);
+  }
+}
+
+// ---------------------------------------------------------------------------
 // SGD over a flat buffer: w <- w - lr * g (fused multiply-add, one rounding).
 // Each thread moves kSgdUnroll 16-byte chunks of every operand per iteration,
 // all loads issued before the first store, so that enough bytes are in flight
@@ -766,6 +783,20 @@ hipError_t launch_split_softmax_xent(int dtype, int splits, int64_t rows, int64_
   return launch_split_softmax_typed<bf16_t, bf16_t>(
       splits, rows, classes, part, c_split, ld_part, static_cast<const bf16_t*>(bias), labels,
       scale, static_cast<bf16_t*>(dlogits), ld_dlogits, partials, bad, nb, s);
+}
+
+hipError_t launch_act_adjoint(int dtype, int act, int64_t n, const void* g, const void* h,
+                              void* out, hipStream_t s) {
+  const unsigned nb = grid_for(n, 4096);
+  if (dtype == F32)
+    launch_kernel(dlvm_act_adjoint_kernel<float>, dim3(nb), dim3(kBlock), s, n, act,
+                  static_cast<const float*>(g), static_cast<const float*>(h),
+                  static_cast<float*>(out));
+  else
+    launch_kernel(dlvm_act_adjoint_kernel<bf16_t>, dim3(nb), dim3(kBlock), s, n, act,
+                  static_cast<const bf16_t*>(g), static_cast<const bf16_t*>(h),
+                  static_cast<bf16_t*>(out));
+  return hipGetLastError();
 }
 
 hipError_t launch_seed(int dtype, int64_t rows, int64_t classes, int64_t ld, const float* seed,

@@ -55,10 +55,14 @@ bool aligned16(const void* q) { return (reinterpret_cast<uintptr_t>(q) & 15u) ==
 // 16-byte aligned bases, leading dimensions and contraction extent; its
 // epilogue moves 8 consecutive outputs at a time (16-byte aligned output rows,
 // saved activation and residual).
+bool phases_ok(const GemmDesc& d, int vw) {
+  return d.A2 == nullptr || (aligned16(d.A2) && d.lda2 % vw == 0 && d.K1 % vw == 0);
+}
+
 bool async_ok(const GemmDesc& d) {
   return d.dtype == BF16 && aligned16(d.A) && aligned16(d.B) && d.lda % 8 == 0 &&
          d.ldb % 8 == 0 && d.K % 8 == 0 && d.ldc % 8 == 0 && aligned16(d.C) &&
-         aligned16(d.aux) && aligned16(d.residual) && aligned16(d.bias);
+         aligned16(d.aux) && aligned16(d.residual) && aligned16(d.bias) && phases_ok(d, 8);
 }
 
 // Extent in bytes of a row-major operand of `rows` rows of `cols` elements at
@@ -78,7 +82,7 @@ void operand_dims(const GemmDesc& d, int64_t& ar, int64_t& ac, int64_t& br, int6
 // offsets: every offset it forms (up to one tile past either extent) must stay
 // below 2^31.
 bool xl_ok(const GemmDesc& d) {
-  if (!async_ok(d)) return false;
+  if (!async_ok(d) || d.A2 != nullptr) return false;
   int64_t ar, ac, br, bc;
   operand_dims(d, ar, ac, br, bc);
   const int64_t lim = int64_t(1) << 31;
@@ -139,7 +143,8 @@ namespace {
 // ignores the operands' addresses (for sizing scratch before they exist).
 GemmPlan choose(const GemmDesc& d, bool assume_aligned, int64_t capacity, int forced) {
   const bool can_async = assume_aligned ? (d.dtype == BF16 && d.lda % 8 == 0 && d.ldb % 8 == 0 &&
-                                           d.K % 8 == 0 && d.ldc % 8 == 0)
+                                           d.K % 8 == 0 && d.ldc % 8 == 0 &&
+                                           (d.A2 == nullptr || (d.lda2 % 8 == 0 && d.K1 % 8 == 0)))
                                         : async_ok(d);
   const TileShape* best = nullptr;
   int best_s = 1;
@@ -160,6 +165,7 @@ GemmPlan choose(const GemmDesc& d, bool assume_aligned, int64_t capacity, int fo
     if (t.cfg == 15 && forced != 15) continue;
     if (forced >= 0 && t.cfg != forced) continue;
     for (int sp = 1; sp <= kMaxSplits; sp *= 2) {
+      if (sp > 1 && d.A2 != nullptr) break;  // two-phase products are not split
       if (d.splits_hint > 0 && split_need(d, d.splits_hint) <= capacity) {
         // the caller's split (a multiple of 64 k per slice, whole slices)
         if (sp != d.splits_hint && !(sp == 1 && d.splits_hint == 1)) {
@@ -221,6 +227,12 @@ void vector_ok(const GemmDesc& d, bool& va, bool& vb) {
     case Layout::NT: va = va && d.K % vw == 0; vb = vb && d.K % vw == 0; break;
     case Layout::TN: break;
   }
+  // Two phases: every chunk along k inside or outside each phase's extent,
+  // and 16-byte rows of A2.
+  if (d.A2 != nullptr) {
+    va = va && phases_ok(d, vw);
+    if (d.layout != Layout::NN) vb = vb && d.K1 % vw == 0;
+  }
 }
 
 gemm::Params make_params(const GemmDesc& d, const GemmPlan& pl) {
@@ -233,6 +245,10 @@ gemm::Params make_params(const GemmDesc& d, const GemmPlan& pl) {
   p.nvec = d.nvec > 0 ? d.nvec : d.N;
   p.splits = pl.splits;
   p.k_chunk = pl.k_chunk;
+  p.A2 = d.A2;
+  p.lda2 = d.A2 != nullptr ? d.lda2 : 0;
+  p.K1 = d.A2 != nullptr ? d.K1 : d.K;
+  p.res_pre = d.res_pre ? 1 : 0;
   if (pl.splits > 1) {
     p.C = d.split_ws;                  // partial products, then partial column sums
     p.c_split = d.M * d.ldc;

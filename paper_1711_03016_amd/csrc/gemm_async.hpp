@@ -332,8 +332,9 @@ __device__ __forceinline__ void epilogue_row(const Params& p, const f32x16 (&acc
         if constexpr (EPI == EPI_STORE) {
           v[e] = apply_act(p.act, p.alpha * v[e] + g[b][e]);
         } else if constexpr (EPI == EPI_DACT) {
+          if (p.res_pre) v[e] += rv[b][e];
           if (has_act) v[e] *= act_grad_from_output(p.act, g[b][e]);
-          v[e] += rv[b][e];
+          if (!p.res_pre) v[e] += rv[b][e];
         }
       }
       const int64_t idx = row[b] * p.ldc + col[b];
@@ -387,8 +388,12 @@ __device__ __forceinline__ void async_gemm_tile(Params& p, const int tile, char*
   const int64_t n0 = static_cast<int64_t>(tn) * BN;
   const bf16_t* __restrict__ A = static_cast<const bf16_t*>(p.A);
   const bf16_t* __restrict__ B = static_cast<const bf16_t*>(p.B);
-  const int nk = static_cast<int>((p.K + BK - 1) / BK);
-  const int kv_last = static_cast<int>(p.K - static_cast<int64_t>(nk - 1) * BK);  // valid k of the last tile
+  // k-tiles of the two phases of the contraction (one phase unless A2 is set)
+  const int nk1 = static_cast<int>((p.K1 + BK - 1) / BK);
+  const int nk = nk1 + static_cast<int>((p.K - p.K1 + BK - 1) / BK);
+  // valid k of the last tile of phase 1 and of phase 2
+  const int kv1 = static_cast<int>(p.K1 - static_cast<int64_t>(nk1 - 1) * BK);
+  const int kv2 = static_cast<int>(p.K - p.K1 - static_cast<int64_t>(nk - nk1 - 1) * BK);
 
   f32x16 acc[TM][TN];
 #pragma unroll
@@ -407,9 +412,9 @@ __device__ __forceinline__ void async_gemm_tile(Params& p, const int tile, char*
 
   auto issue = [&](int kt) {
     char* st = smem + (kt % STAGES) * STAGE;
-    const int64_t k0 = static_cast<int64_t>(kt) * BK;
-    async_tile<AK, BM, BK, NW>(A, p.lda, m0, p.M, k0, p.K, st, wave, lane);
-    async_tile<BKM, BN, BK, NW>(B, p.ldb, n0, p.N, k0, p.K, st + A_BYTES, wave, lane);
+    const StageSrc<bf16_t, BKM> q = stage_src<bf16_t, BKM>(p, A, B, kt, nk1, BK);
+    async_tile<AK, BM, BK, NW>(q.a, q.lda, m0, p.M, q.k0, q.klim, st, wave, lane);
+    async_tile<BKM, BN, BK, NW>(q.b, p.ldb, n0, p.N, q.k0, q.klim, st + A_BYTES, wave, lane);
   };
 
 #pragma unroll
@@ -423,9 +428,10 @@ __device__ __forceinline__ void async_gemm_tile(Params& p, const int tile, char*
     barrier_only();
     char* As = smem + (kt % STAGES) * STAGE;
     char* Bs = As + A_BYTES;
-    if (kt == nk - 1 && kv_last < BK) {
-      zero_k_tail<AK, BM, BK, THREADS>(As, kv_last, tid);
-      zero_k_tail<BKM, BN, BK, THREADS>(Bs, kv_last, tid);
+    const int kv = kt == nk1 - 1 ? kv1 : (kt == nk - 1 ? kv2 : BK);
+    if (kv < BK) {
+      zero_k_tail<AK, BM, BK, THREADS>(As, kv, tid);
+      zero_k_tail<BKM, BN, BK, THREADS>(Bs, kv, tid);
       __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): the LDS writes are done
       barrier_only();
     }

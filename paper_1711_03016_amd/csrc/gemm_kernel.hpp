@@ -78,7 +78,38 @@ struct Params {
   // C + slice * c_split (colsum + slice * cs_split). splits == 1: no split.
   int splits;
   int64_t k_chunk, c_split, cs_split;
+  // Two-phase contraction (a sum of two products accumulated in one pass,
+  // sum_k over [A A2] . B): k < K1 reads A (row stride lda) at k, k >= K1
+  // reads A2 (row stride lda2) at k - K1; B runs through all K. K1 == K (and
+  // A2 null): one phase.
+  const void* A2;
+  int64_t lda2, K1;
+  int res_pre;  // EPI_DACT: (acc + R) * act'(Hprev) instead of acc * act'(Hprev) + R
 };
+
+// Source of pipeline stage kt (KSTAGE k per stage) of a two-phase
+// contraction: the stages of phase 1 cover [0, K1) and those of phase 2
+// [K1, K), each phase starting on a stage boundary (its last stage is padded
+// with zeros by the loader).
+template <typename T, bool BKM>
+struct StageSrc {
+  const T* a;
+  int64_t lda;
+  const T* b;
+  int64_t k0, klim;
+};
+template <typename T, bool BKM>
+__device__ __forceinline__ StageSrc<T, BKM> stage_src(const Params& p, const T* A, const T* B,
+                                                      int64_t kt, int64_t nk1, int64_t kstage) {
+  StageSrc<T, BKM> s;
+  const bool ph2 = kt >= nk1;
+  s.a = ph2 ? static_cast<const T*>(p.A2) : A;
+  s.lda = ph2 ? p.lda2 : p.lda;
+  s.b = ph2 ? B + (BKM ? p.K1 : p.K1 * p.ldb) : B;
+  s.k0 = (ph2 ? kt - nk1 : kt) * kstage;
+  s.klim = ph2 ? p.K - p.K1 : p.K1;
+  return s;
+}
 
 // Tile index of workgroup `bid` of a product; with a split reduction, also
 // narrows p to the workgroup's k-slice and partial outputs.
@@ -97,6 +128,7 @@ __device__ __forceinline__ int split_slice(Params& p, int bid) {
     p.a_bytes -= static_cast<uint32_t>(sa * static_cast<int64_t>(sizeof(T)));
     p.b_bytes -= static_cast<uint32_t>(sb * static_cast<int64_t>(sizeof(T)));
     p.K = kl;
+    p.K1 = kl;  // split products have one phase
     p.C = static_cast<float*>(p.C) + sl * p.c_split;
     if (p.colsum != nullptr) p.colsum += sl * p.cs_split;
   }
@@ -329,8 +361,9 @@ __device__ __forceinline__ void store_block(const Params& p, const f32x16& acc, 
         if constexpr (EPI == EPI_STORE) {
           v = apply_act(p.act, p.alpha * v + bias_v);
         } else if constexpr (EPI == EPI_DACT) {
+          if (p.res_pre) v += rv[r];
           if (has_act) v *= act_grad_from_output(p.act, g[r]);
-          v += rv[r];
+          if (!p.res_pre) v += rv[r];
         }
         C[ro * ld] = store_cast<TO>(v);
       }
@@ -344,8 +377,10 @@ __device__ __forceinline__ void store_block(const Params& p, const f32x16& acc, 
       if constexpr (EPI == EPI_STORE) {
         v = apply_act(p.act, p.alpha * v + bias_v);
       } else if constexpr (EPI == EPI_DACT) {
+        const float rr = res != nullptr ? load_as_f32<TO>(res + base + ro * ld) : 0.0f;
+        if (p.res_pre) v += rr;
         if (has_act) v *= act_grad_from_output(p.act, load_as_f32<T>(aux + base + ro * ld));
-        if (res != nullptr) v += load_as_f32<TO>(res + base + ro * ld);
+        if (!p.res_pre) v += rr;
       }
       C[ro * ld] = store_cast<TO>(v);
     }
@@ -406,10 +441,15 @@ __device__ __forceinline__ void gemm_tile(Params& p, const int tile, char* smem)
 
   TileLoader<T, AK, BM, THREADS, VA, KSEG> la;
   TileLoader<T, BKM, BN, THREADS, VB, KSEG> lb;
-  const int64_t nk = (p.K + KSTAGE - 1) / KSTAGE;
+  const int64_t nk1 = (p.K1 + KSTAGE - 1) / KSTAGE;
+  const int64_t nk = nk1 + (p.K - p.K1 + KSTAGE - 1) / KSTAGE;
+  auto load_stage = [&](int64_t kt) {
+    const StageSrc<T, BKM> q = stage_src<T, BKM>(p, A, B, kt, nk1, KSTAGE);
+    la.load(q.a, q.lda, m0, p.M, q.k0, q.klim, tid);
+    lb.load(q.b, p.ldb, n0, p.N, q.k0, q.klim, tid);
+  };
 
-  la.load(A, p.lda, m0, p.M, 0, p.K, tid);
-  lb.load(B, p.ldb, n0, p.N, 0, p.K, tid);
+  load_stage(0);
   la.template store<SEG>(smem, tid);
   lb.template store<SEG>(smem + BM * kRowStride, tid);
   __syncthreads();
@@ -421,10 +461,7 @@ __device__ __forceinline__ void gemm_tile(Params& p, const int tile, char* smem)
     const int buf = static_cast<int>(kt & 1);
     char* stage = smem + buf * STAGE;
     const bool more = kt + 1 < nk;
-    if (more) {
-      la.load(A, p.lda, m0, p.M, (kt + 1) * KSTAGE, p.K, tid);
-      lb.load(B, p.ldb, n0, p.N, (kt + 1) * KSTAGE, p.K, tid);
-    }
+    if (more) load_stage(kt + 1);
 #pragma unroll
     for (int g = 0; g < 4 * KSEG; ++g) {
       if constexpr (WK > 1) {

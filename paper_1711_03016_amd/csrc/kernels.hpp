@@ -44,7 +44,7 @@ struct GemmDesc {
   void* C; int64_t ldc;
   const void* bias;      // NN: [N] in operand dtype, or null
   const void* aux;       // NT: saved activation [M, ldc] in operand dtype, or null
-  const void* residual;  // NT: [M, ldc] in out dtype added after act', or null
+  const void* residual;  // NT: [M, ldc] in out dtype added after act' (before, with res_pre), or null
   float* colsum;         // TN: [nvec] float32 sum over k of B(k, n), or null
   float alpha;           // NN: scale of the product
   int64_t nvec;          // entries of bias / colsum (0 means N). Columns n >= nvec
@@ -58,6 +58,13 @@ struct GemmDesc {
   float* split_ws;
   int64_t split_ws_elems;
   int splits_hint;  // > 0: use exactly this many k-slices if the scratch holds them
+  // Second source of A (null: none). The contraction then has two phases:
+  // k < K1 from A (stride lda) and k in [K1, K) from A2 (stride lda2, column
+  // or row k - K1), accumulated into the same outputs; B spans all K. Such a
+  // product is never split over K.
+  const void* A2;
+  int64_t lda2, K1;
+  bool res_pre;  // NT: the residual is added before act' is applied
 };
 
 // How one product is launched: tile configuration and grid.
@@ -132,6 +139,11 @@ hipError_t launch_sgd(int dtype, int64_t n, void* params, float* master, const f
 // classes <= c < ld.
 hipError_t launch_seed(int dtype, int64_t rows, int64_t classes, int64_t ld, const float* seed,
                        void* dz, hipStream_t s);
+
+// out[i] = g[i] * act'(h[i]) for i < n, act' from the saved output h = act(z)
+// (storage dtype `dtype` for all three).
+hipError_t launch_act_adjoint(int dtype, int act, int64_t n, const void* g, const void* h,
+                              void* out, hipStream_t s);
 
 // Sum of the k-slices of a split product in slice order: out[r, c] (row
 // stride ld) = sum_s part[s * c_split + r * ld + c] for c < cols, and

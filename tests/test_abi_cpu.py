@@ -208,3 +208,58 @@ def test_probe_arguments_are_validated():
     info = dl.LaunchInfo()
     assert L.dlvm_plan_entry(m._h, 4, 99, ctypes.byref(info)) == dl.ERR_INVALID_ARG
     assert L.dlvm_plan_size(m._h, 5) == 0
+
+
+def test_rnn_handle_plan_and_errors():
+    """A recurrent model: T fused cell products (contraction Kx + H), the
+    adjoint sweep, one weight-gradient contraction over all T * B rows, and the
+    update; the dense-network entry points refuse it; errors are host-side."""
+    L = dl.lib()
+    wl = workloads.RNN_WORKLOADS["r1"]
+    m = dl.Rnn(wl.steps, wl.in_width, wl.hidden, wl.act, wl.dtype, wl.wrt_x, wl.wrt_h0, wl.batch)
+    offs, lds = m.param_layout_lds()
+    assert offs[0] == 0 and lds == [wl.hidden]
+    assert offs[1] >= (wl.in_width + wl.hidden) * wl.hidden and offs[1] % 128 == 0
+    plan = m.plan(wl.batch)
+    nn = [p for p in plan if p["name"].startswith("gemm_nn")]
+    assert len(nn) == wl.steps
+    assert all(p["K"] == wl.in_width + wl.hidden and p["M"] == wl.batch for p in nn)
+    assert plan[-1]["name"].startswith("sgd")
+    assert sum(p["flops"] for p in plan) == wl.flops()
+    ws = m.workspace_bytes(wl.batch)
+    assert ws >= wl.steps * wl.batch * wl.hidden * 2
+    A = 0x100000
+    B = wl.batch
+    # dense entry points refuse a recurrent handle
+    assert L.dlvm_forward(m._h, A, A, B, A, A, ws, None) == dl.ERR_UNSUPPORTED
+    assert L.dlvm_gradient(m._h, A, A, A, B, A, A, A, A, ws, None) == dl.ERR_UNSUPPORTED
+    assert L.dlvm_vjp(m._h, A, A, A, B, A, A, A, ws, None) == dl.ERR_UNSUPPORTED
+    # recurrent entry points: nulls, declared outputs, alignment, batch, workspace
+    assert L.dlvm_rnn_forward(m._h, None, A, B, A, None) == dl.ERR_INVALID_ARG
+    assert L.dlvm_rnn_forward(m._h, A, A + 2, B, A, None) == dl.ERR_MISALIGNED
+    assert L.dlvm_rnn_forward(m._h, A, A, B + 1, A, None) == dl.ERR_INVALID_ARG
+    assert L.dlvm_rnn_backward(m._h, A, A, A, A, B, A, None, A, A, ws, None) == dl.ERR_INVALID_ARG
+    assert L.dlvm_rnn_backward(m._h, A, A, A, A, B, A, A, None, A, ws, None) == dl.ERR_INVALID_ARG
+    assert L.dlvm_rnn_backward(m._h, A, A, A, A, B, A, A, A, A, ws - 1, None) == dl.ERR_WORKSPACE
+    mlp = dl.Model((8, 8), ("none",), batch_max=4)
+    assert L.dlvm_rnn_forward(mlp._h, A, A, 4, A, None) == dl.ERR_UNSUPPORTED
+    # create validation
+    for bad in (dict(steps=0), dict(in_width=0), dict(hidden=0), dict(batch_max=0)):
+        args = dict(steps=4, in_width=8, hidden=8, batch_max=4)
+        args.update(bad)
+        d = dl._RnnDesc(0, 2, args["steps"], args["in_width"], args["hidden"], args["batch_max"], 0, 0)
+        h = ctypes.c_void_p()
+        assert L.dlvm_rnn_create(ctypes.byref(d), ctypes.byref(h)) == dl.ERR_INVALID_ARG
+    assert L.dlvm_rnn_cell_forward(0, 2, 4, 0, 4, 4, A, A, A, None, A, None) == dl.ERR_INVALID_ARG
+    assert L.dlvm_rnn_cell_forward(0, 2, 4, 4, 4, 4, A, A + 4, A, None, A, None) == dl.ERR_MISALIGNED
+
+
+def test_rnn_dead_outputs_are_not_computed():
+    """Without wrt_x / wrt_h0 the products that only feed dxs / dh0 are absent."""
+    full = dl.Rnn(4, 64, 32, "tanh", "f32", True, True, 16).plan(16)
+    lean = dl.Rnn(4, 64, 32, "tanh", "f32", False, False, 16).plan(16)
+    nt = lambda p: sum(1 for e in p if "nt" in e["name"].split("_")[1])  # noqa: E731
+    pairs = lambda p: sum(1 for e in p if e["name"].startswith("gemm_pair"))  # noqa: E731
+    assert nt(full) + pairs(full) == nt(lean) + 2
+    assert sum(e["flops"] for e in full) - sum(e["flops"] for e in lean) == \
+        2 * 16 * 32 * 32 + 2 * 4 * 16 * 32 * 64
