@@ -1,9 +1,12 @@
-"""Benchmark of one training step of an MLP workload on one MI355X.
+"""Benchmark of one training step of a workload on one MI355X.
 
-A step is one ``dlvm_gradient`` call (the forward recomputed from the original
-inputs, then the whole adjoint) followed, for workloads with an SGD update, by
-one ``dlvm_sgd_step`` call, over one batch of seeded synthetic inputs that are
-resident in device memory before the timed region starts.
+A step of a dense workload (c1-c5) is one ``dlvm_gradient`` call (the forward
+recomputed from the original inputs, then the whole adjoint) followed, for
+workloads with an SGD update, by one ``dlvm_sgd_step`` call. A step of a
+recurrent workload (r1) is ``dlvm_rnn_forward`` over its T steps,
+``dlvm_rnn_backward`` seeded with fixed output adjoints, and the update. Inputs
+are seeded, synthetic and resident in device memory before the timed region
+starts.
 
 Prints one JSON line. ``value`` is steps per second of the whole job on one
 GPU. ``roofline`` describes the kernel that takes the most time in a step: its
@@ -41,7 +44,8 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=None)
     ap.add_argument("--warmup", type=int, default=None)
-    ap.add_argument("--workload", default="c2", choices=sorted(workloads.WORKLOADS))
+    ap.add_argument("--workload", default="c2",
+                    choices=sorted(workloads.WORKLOADS) + sorted(workloads.RNN_WORKLOADS))
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="budget of the oracle CPU baseline (0 disables it)")
     ap.add_argument("--entry", default="gradient", choices=["gradient", "vjp"],
@@ -191,6 +195,193 @@ def vjp_bench(args, wl, m, P, xd, dP, dx, ws, stream, steps, warmup):
                       "mfma_frac": round(flops * sps / 1e12 / PEAK_TFLOPS[wl.dtype], 4)}), flush=True)
 
 
+def measure(m, wl, step, eager_step, steps, warmup, with_sgd, flags_ws=None):
+    """Warm up, find the launch position that takes the most time, time `steps`
+    whole steps, then time the dominant launch on its stream over as many steps.
+
+    Returns (steps/s, seconds, roofline dict, per-group microseconds per step).
+    """
+    import torch
+
+    import paper_1711_03016_amd as dl
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    if flags_ws is not None and m.check(flags_ws) != dl.OK:
+        raise RuntimeError("device flags raised during warm-up")
+
+    # find the launch that takes the most time (outside the timed region)
+    B = wl.batch
+    plan = m.plan(B)
+    if not with_sgd:
+        plan = plan[:-1]
+    probe_steps = 3
+    m.probe_arm(-1, probe_steps * len(plan) + 8)
+    for _ in range(probe_steps):
+        eager_step()
+    torch.cuda.synchronize()
+    times = []
+    for e in plan:
+        n, ms = m.probe_read(e["index"])
+        times.append(ms / max(n, 1))
+    dom = plan[int(np.argmax(times))]
+    m.probe_disarm()
+    groups: dict = {}
+    for e, ms in zip(plan, times):
+        key = e["name"].split(" ")[0]
+        groups[key] = round(groups.get(key, 0.0) + ms * 1e3, 2)
+
+    # timed region: whole steps, nothing else on the stream
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    sps = steps / elapsed
+
+    # the same number of steps again, the dominant launch timed by events that
+    # its own dispatch packet records on its stream (begin and end on the GPU)
+    m.probe_arm(dom["index"], steps)
+    torch.cuda.synchronize()
+    t2 = time.perf_counter()
+    for _ in range(steps):
+        eager_step()
+    torch.cuda.synchronize()
+    t3 = time.perf_counter()
+    n_dom, ms_dom = m.probe_read(dom["index"])
+    m.probe_disarm()
+    avg_s = ms_dom / max(n_dom, 1) / 1e3
+
+    if dom["flops"] > 0:
+        achieved = dom["flops"] / avg_s / 1e12
+        peak = PEAK_TFLOPS[wl.dtype]
+        roof = {"bound": "mfma", "achieved": round(achieved, 3), "peak": peak,
+                "unit": "TFLOP/s", "frac": round(achieved / peak, 4)}
+    else:
+        achieved = dom["bytes"] / avg_s / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
+                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4)}
+    roof["traffic"] = traffic_record(wl.name, dom)
+    roof["kernel"] = (f"{dom['name']} M={dom['M']} N={dom['N']} K={dom['K']} "
+                      f"(launch {dom['index']} of {len(plan)}, {n_dom} timed launches, "
+                      f"avg {avg_s * 1e6:.2f} us)")
+    roof["probe_ms_per_step"] = round((t3 - t2) / steps * 1e3, 4)
+    return sps, elapsed, roof, groups
+
+
+def result_line(wl, sps, elapsed, steps, warmup, roof, config, **extra) -> dict:
+    tflops = wl.flops() * sps / 1e12
+    out = {
+        "metric": METRIC,
+        "value": round(sps, 3),
+        "unit": "steps/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": warmup,
+        "ms_per_step": round(elapsed / steps * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": wl.dtype,
+        "data": "synthetic",
+        "config": config,
+    }
+    out.update(extra)
+    out["tflops"] = round(tflops, 3)
+    out["mfma_frac"] = round(tflops / PEAK_TFLOPS[wl.dtype], 4)
+    out["roofline"] = roof
+    return out
+
+
+def rnn_main(args, wl) -> None:
+    """A step of a recurrent workload: dlvm_rnn_forward over the T steps,
+    dlvm_rnn_backward seeded with fixed output adjoints, and the fused SGD."""
+    import torch
+
+    import paper_1711_03016_amd as dl
+
+    steps, warmup = default_steps(wl)
+    steps = args.steps if args.steps is not None else steps
+    warmup = args.warmup if args.warmup is not None else warmup
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    tdt = torch.float32 if wl.dtype == "f32" else torch.bfloat16
+    B, T, Kx, H = wl.batch, wl.steps, wl.in_width, wl.hidden
+    xs, h0, W, U, b, dhs = workloads.make_rnn_inputs(wl)
+    m = dl.Rnn(T, Kx, H, wl.act, wl.dtype, wl.wrt_x, wl.wrt_h0, B)
+    P = m.pack_cell(W, U, b, dev, tdt)
+    master = m.pack_cell(W, U, b, dev, torch.float32) if wl.dtype == "bf16" else None
+    xd = torch.from_numpy(xs).to(dev).to(tdt)
+    hs = torch.empty((T + 1, B, H), dtype=tdt, device=dev)
+    hs[0] = torch.from_numpy(h0).to(dev).to(tdt)
+    dhd = torch.from_numpy(dhs).to(dev).to(tdt)
+    del xs, dhs
+    dP = torch.empty(m.param_count(), device=dev)
+    dxs = torch.empty((T, B, Kx), device=dev) if wl.wrt_x else None
+    dh0 = torch.empty((B, H), device=dev) if wl.wrt_h0 else None
+    ws = torch.empty(m.workspace_bytes(B), dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        m.forward(P, xd, B, hs, stream)
+        m.backward(P, xd, hs, dhd, B, dP, dxs, dh0, ws, stream)
+        if wl.sgd:
+            m.sgd_step(P, master, dP, wl.lr, stream)
+
+    sps, elapsed, roof, groups = measure(m, wl, step, step, steps, warmup, wl.sgd)
+    config = {"workload": f"{wl.name}: {wl.title}", "global_batch": B, "steps_T": T,
+              "in_width": Kx, "hidden": H, "act": wl.act, "parallelism": "none"}
+    out = result_line(wl, sps, elapsed, steps, warmup, roof, config, launch="eager",
+                      workspace_bytes=int(ws.numel()), launch_groups_us=groups)
+    del P, master, xd, hs, dhd, ws, dP, dxs, dh0
+    out["cpu_baseline"] = rnn_cpu_baseline(wl, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+def rnn_cpu_baseline(wl, budget_s: float) -> dict | None:
+    """The oracle's forward + seedable gradient (+ SGD) on a slice of the rows."""
+    if budget_s <= 0:
+        return None
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([d.get("num_threads", 1) for d in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover - threadpoolctl is optional
+        threads = os.cpu_count() or 1
+    rows = wl.batch
+    while rows > 4 and wl.flops(rows) > 4e10:
+        rows //= 2
+    xs, h0, W, U, b, dhs = workloads.make_rnn_inputs(wl, batch=rows)
+    spec = oracle.RnnSpec(wl.steps, wl.in_width, wl.hidden, wl.act, wl.dtype)
+    n = 0
+    t_grad = t_sgd = 0.0
+    while True:
+        t0 = time.perf_counter()
+        oracle.rnn_forward(spec, xs, h0, W, U, b)
+        dW, dU, db, _, _ = oracle.rnn_vjp(spec, xs, h0, W, U, b, dhs, wl.wrt_x, wl.wrt_h0)
+        t1 = time.perf_counter()
+        if wl.sgd:
+            for p_, g_ in ((W, dW), (U, dU), (b, db)):
+                oracle.sgd_f32(p_, g_, wl.lr)
+        t2 = time.perf_counter()
+        t_grad += t1 - t0
+        t_sgd += t2 - t1
+        n += 1
+        el = t_grad + t_sgd
+        if el >= budget_s or el * (n + 1) / n > 2 * budget_s:
+            break
+    per_step = (t_grad / n) * (wl.batch / rows) + t_sgd / n
+    sample = (f"{n} oracle steps (float64 forward + seedable gradient"
+              f"{' + SGD' if wl.sgd else ''}) on {rows} of {wl.batch} rows in {el:.1f} s")
+    if rows != wl.batch:
+        sample += (f"; forward and gradient time scaled by {wl.batch}/{rows} rows (linear in "
+                   "the rows), update time taken as measured")
+    return {"value": 1.0 / per_step, "unit": "steps/s", "cores": int(threads),
+            "kind": "oracle", "sample": sample}
+
+
 def main():
     args = parse()
     if args.copy_calibration:
@@ -200,6 +391,8 @@ def main():
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the workloads "
               "here are single-GPU and no multi-GPU path is built", file=sys.stderr)
         sys.exit(2)
+    if args.workload in workloads.RNN_WORKLOADS:
+        return rnn_main(args, workloads.RNN_WORKLOADS[args.workload])
     import torch
 
     import paper_1711_03016_amd as dl
@@ -242,91 +435,14 @@ def main():
     graph = None if not args.graph else m.step_graph(P, master, xd, yd, B, loss, dP, dx, ws,
                                                  update=wl.sgd, lr=wl.lr)
     step = eager_step if graph is None else (lambda: graph.launch(stream))
-
-    for _ in range(warmup):
-        step()
-    torch.cuda.synchronize()
-    if m.check(ws) != dl.OK:
-        raise RuntimeError("device flags raised during warm-up")
-
-    # find the launch that takes the most time (outside the timed region)
-    plan = m.plan(B)
-    if not wl.sgd:
-        plan = plan[:-1]
-    probe_steps = 3
-    m.probe_arm(-1, probe_steps * len(plan) + 8)
-    for _ in range(probe_steps):
-        eager_step()
-    torch.cuda.synchronize()
-    times = []
-    for e in plan:
-        n, ms = m.probe_read(e["index"])
-        times.append(ms / max(n, 1))
-    dom = plan[int(np.argmax(times))]
-    m.probe_disarm()
-
-    # timed region: whole steps, nothing else on the stream
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(steps):
-        step()
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    elapsed = t1 - t0
-    sps = steps / elapsed
-
-    # the same number of steps again, the dominant launch timed by events that
-    # its own dispatch packet records on its stream (begin and end on the GPU)
-    m.probe_arm(dom["index"], steps)
-    torch.cuda.synchronize()
-    t2 = time.perf_counter()
-    for _ in range(steps):
-        eager_step()
-    torch.cuda.synchronize()
-    t3 = time.perf_counter()
-    n_dom, ms_dom = m.probe_read(dom["index"])
-    m.probe_disarm()
-    avg_s = ms_dom / max(n_dom, 1) / 1e3
-
-    if dom["flops"] > 0:
-        achieved = dom["flops"] / avg_s / 1e12
-        peak = PEAK_TFLOPS[wl.dtype]
-        roof = {"bound": "mfma", "achieved": round(achieved, 3), "peak": peak,
-                "unit": "TFLOP/s", "frac": round(achieved / peak, 4)}
-    else:
-        achieved = dom["bytes"] / avg_s / 1e9
-        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
-                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4)}
-    roof["traffic"] = traffic_record(wl.name, dom)
-    roof["kernel"] = (f"{dom['name']} M={dom['M']} N={dom['N']} K={dom['K']} "
-                      f"(launch {dom['index']} of {len(plan)}, {n_dom} timed launches, "
-                      f"avg {avg_s * 1e6:.2f} us)")
-    roof["probe_ms_per_step"] = round((t3 - t2) / steps * 1e3, 4)
-
-    step_flops = wl.flops()
-    tflops = step_flops * sps / 1e12
-    out = {
-        "metric": METRIC,
-        "value": round(sps, 3),
-        "unit": "steps/s",
-        "n_gpus": 1,
-        "steps": steps,
-        "warmup": warmup,
-        "ms_per_step": round(elapsed / steps * 1e3, 4),
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": wl.dtype,
-        "data": "synthetic",
-        "config": {"workload": f"{wl.name}: {wl.title}", "global_batch": B,
-                   "widths": list(wl.widths), "loss": wl.loss, "parallelism": "none",
-                   **({"checkpoint_every": args.checkpoint} if args.checkpoint > 1 else {})},
-        "launch": "eager" if graph is None else "hip_graph",
-        "workspace_bytes": int(ws.numel()),
-        "tflops": round(tflops, 3),
-        "mfma_frac": round(tflops / PEAK_TFLOPS[wl.dtype], 4),
-        "roofline": roof,
-    }
+    sps, elapsed, roof, groups = measure(m, wl, step, eager_step, steps, warmup, wl.sgd,
+                                         flags_ws=ws)
+    config = {"workload": f"{wl.name}: {wl.title}", "global_batch": B,
+              "widths": list(wl.widths), "loss": wl.loss, "parallelism": "none",
+              **({"checkpoint_every": args.checkpoint} if args.checkpoint > 1 else {})}
+    out = result_line(wl, sps, elapsed, steps, warmup, roof, config,
+                      launch="eager" if graph is None else "hip_graph",
+                      workspace_bytes=int(ws.numel()))
     del graph, P, master, xd, ws, dP, dx
     out["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
     print(json.dumps(out), flush=True)
