@@ -325,7 +325,7 @@ def rnn_main(args, wl) -> None:
     stream = torch.cuda.current_stream()
 
     def step():
-        m.forward(P, xd, B, hs, stream)
+        m.forward(P, xd, B, hs, ws, stream)
         m.backward(P, xd, hs, dhd, B, dP, dxs, dh0, ws, stream)
         if wl.sgd:
             m.sgd_step(P, master, dP, wl.lr, stream)

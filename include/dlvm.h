@@ -188,10 +188,14 @@ dlvm_status dlvm_rnn_create(const dlvm_rnn_desc* desc, dlvm_model** out);
 
 /* Forward over the T steps: xs [T, batch, Kx] and hs [T + 1, batch, H] in the
  * storage dtype, caller's device memory; the caller writes the initial state
- * into hs[0], the call writes hs[1..T] (T launches, one fused product each).
- * hs is what dlvm_rnn_backward needs (the adjoint uses the saved outputs). */
+ * into hs[0], the call writes hs[1..T] (one fused product per step). hs is
+ * what dlvm_rnn_backward needs (the adjoint uses the saved outputs). `ws`
+ * (dlvm_workspace_bytes, or NULL) holds the float32 k-slices of products the
+ * planner splits over their contraction (summed in slice order, then bias
+ * and activation applied); with NULL no product is split. The launch plan
+ * (dlvm_plan_entry) describes calls given a workspace. */
 dlvm_status dlvm_rnn_forward(const dlvm_model* m, const void* params, const void* xs,
-                             int64_t batch, void* hs, void* stream);
+                             int64_t batch, void* hs, void* ws, size_t ws_bytes, void* stream);
 
 /* Seedable gradient of the T outputs (backpropagation through time, the
  * adjoint of the unrolled cell, section 3.1.3): dhs [T, batch, H] (storage

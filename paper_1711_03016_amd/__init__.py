@@ -99,7 +99,7 @@ _SIGS = {
     "dlvm_step_graph_create": (_I32, [_P, _P, _P, _P, _P, _I64, _P, _P, _P, _P, ctypes.c_size_t,
                                       _I32, _F, ctypes.POINTER(_P)]),
     "dlvm_rnn_create": (_I32, [ctypes.POINTER(_RnnDesc), ctypes.POINTER(_P)]),
-    "dlvm_rnn_forward": (_I32, [_P, _P, _P, _I64, _P, _P]),
+    "dlvm_rnn_forward": (_I32, [_P, _P, _P, _I64, _P, _P, ctypes.c_size_t, _P]),
     "dlvm_rnn_backward": (_I32, [_P, _P, _P, _P, _P, _I64, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "dlvm_rnn_cell_forward": (_I32, [_I32, _I32, _I64, _I64, _I64, _I64, _P, _P, _P, _P, _P, _P]),
     "dlvm_graph_launch": (_I32, [_P, _P]),
@@ -318,10 +318,12 @@ class Rnn(Model):
         (WU, b), = self.unpack(flat)
         return WU[:self.in_width], WU[self.in_width:], b
 
-    def forward(self, params, xs, batch, hs, stream=None) -> None:
-        """hs[1..T] from xs [T, batch, Kx] and hs[0] ([T + 1, batch, H] buffer)."""
+    def forward(self, params, xs, batch, hs, ws=None, stream=None) -> None:
+        """hs[1..T] from xs [T, batch, Kx] and hs[0] ([T + 1, batch, H] buffer);
+        `ws` (optional) lets the planner split the cell products."""
+        nb = 0 if ws is None else ws.numel() * ws.element_size()
         _check(lib().dlvm_rnn_forward(self._h, _ptr(params), _ptr(xs), int(batch), _ptr(hs),
-                                      _stream(stream)))
+                                      _ptr(ws), nb, _stream(stream)))
 
     def backward(self, params, xs, hs, dhs, batch, dparams, dxs, dh0, ws, stream=None) -> None:
         """d[W; U], db (and dxs, dh0 when declared) for the output adjoints dhs."""

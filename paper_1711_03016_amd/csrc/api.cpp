@@ -331,6 +331,22 @@ class Launcher {
     if (pl.splits <= 1) return DLVM_OK;
     const int64_t nv = d.nvec > 0 ? d.nvec : d.N;
     const int64_t c_split = d.M * d.ldc;
+    if (d.layout != Layout::TN) {
+      // a forward (NN) or input-adjoint (NT) product: its epilogue follows the sum
+      const double mn = double(d.M) * double(d.N);
+      const double eo = elem_size(d.out_dtype), ei = elem_size(d.dtype);
+      const double bytes = double(pl.splits) * mn * 4.0 + mn * eo +
+                           (d.aux && d.act != DLVM_ACT_NONE ? mn * ei : 0.0) +
+                           (d.residual ? mn * eo : 0.0) + (d.bias ? double(nv) * ei : 0.0);
+      return run(elementwise_info("split_epilogue", d.M, d.N, bytes),
+                 [&](hipStream_t s) {
+                   return dlvm::launch_split_epilogue(
+                       d.dtype, d.out_dtype, d.layout == Layout::NN ? 0 : 1, pl.splits, d.M, d.N,
+                       d.ldc, d.split_ws, c_split, d.act, d.alpha, d.bias, nv, d.aux, d.residual,
+                       d.res_pre, d.C, s);
+                 },
+                 "split epilogue launch");
+    }
     const float* cs = d.split_ws + pl.splits * c_split;
     const double bytes = (double(pl.splits) + 1.0) * double(d.M) * double(d.N) * 4.0 +
                          (d.colsum ? (double(pl.splits) + 1.0) * double(nv) * 4.0 : 0.0);
@@ -663,14 +679,62 @@ GemmDesc rnn_du(const dlvm_model* m, int64_t B, const void* hs, const void* dz, 
                  nullptr, m->rnn_H);
 }
 
+// k-slices for one of the recurrent step's products (a cell product or a
+// recurrent adjoint). One step's product has few output tiles (B x H over
+// 128 x 128 tiles: 64 for r1's 1024 x 1024) and the steps run one after the
+// other, so the contraction is split until there are as many tile-slices as
+// compute units, at most 4 ways, each slice at least 256 deep and, for a
+// two-phase product, within one phase. (Measured on 1024 x 1024 products,
+// K = 2048 / 1024: 4 slices fastest of 1, 2, 4, 8 for the cell products; 2 and
+// 4 alike for the recurrent adjoints.)
+int rnn_split_hint(int64_t M, int64_t N, int64_t K, int64_t K1) {
+  const int64_t tiles = (M + 127) / 128 * ((N + 127) / 128);
+  int s = 1;
+  while (s < 4 && tiles * s < 256) {
+    const int64_t kc = ((K + 2 * s - 1) / (2 * s) + 63) / 64 * 64;  // k per slice at 2s slices
+    if (kc < 256 || (K + kc - 1) / kc < 2 * s || (K1 > 0 && K1 % kc != 0)) break;
+    s *= 2;
+  }
+  return s;
+}
+
+// Cell t's fused product: hs[t+1] = act([xs[t] hs[t]] . [W; U] + b), its
+// contraction in two phases (Kx columns of xs[t], then H of hs[t]).
+GemmDesc rnn_cell(const dlvm_model* m, int64_t B, const void* x, const void* h, const void* WU,
+                  const void* bias, void* out) {
+  const int64_t Kx = m->rnn_Kx, H = m->rnn_H;
+  GemmDesc d = gemm_nn(m->dtype, m->dtype, m->acts[0], B, H, Kx + H, 1.0f, x, WU, H, bias, out, H);
+  d.lda = Kx;
+  d.A2 = h;
+  d.lda2 = H;
+  d.K1 = Kx;
+  d.split_epilogue = true;
+  d.splits_hint = rnn_split_hint(B, H, Kx + H, Kx);
+  return d;
+}
+
+// The recurrent adjoint dz[t-1] = (dz[t] . U^T + dhs[t-1]) * act'(hs[t]).
+GemmDesc rnn_recur(const dlvm_model* m, int64_t B, const void* dz, const void* U, const void* h,
+                   const void* seed, void* out) {
+  const int64_t H = m->rnn_H;
+  GemmDesc d = gemm_nt(m->dtype, m->dtype, m->acts[0], B, H, H, dz, H, U, H, h, seed, out);
+  d.res_pre = true;
+  d.split_epilogue = true;
+  d.splits_hint = rnn_split_hint(B, H, H, 0);
+  return d;
+}
+
 RnnWs rnn_ws_layout(const dlvm_model* m, int64_t B) {
   RnnWs w;
   size_t off = 0;
   w.dz = off;
   off = align_up(off + static_cast<size_t>(m->rnn_T * B * m->rnn_H) * elem_size(m->dtype));
   w.splitk = off;
-  w.splitk_elems = std::max(dlvm::split_ws_elems(rnn_dw(m, B, nullptr, nullptr, nullptr, nullptr)),
-                            dlvm::split_ws_elems(rnn_du(m, B, nullptr, nullptr, nullptr)));
+  w.splitk_elems = std::max(
+      std::max(dlvm::split_ws_elems(rnn_dw(m, B, nullptr, nullptr, nullptr, nullptr)),
+               dlvm::split_ws_elems(rnn_du(m, B, nullptr, nullptr, nullptr))),
+      std::max(dlvm::split_ws_elems(rnn_cell(m, B, nullptr, nullptr, nullptr, nullptr, nullptr)),
+               dlvm::split_ws_elems(rnn_recur(m, B, nullptr, nullptr, nullptr, nullptr, nullptr))));
   off = align_up(off + static_cast<size_t>(w.splitk_elems) * 4);
   w.total = off;
   return w;
@@ -687,20 +751,20 @@ T* seq_at(T* base, int64_t t, int64_t B, int64_t width, size_t es) {
 }
 
 // The T fused cell products of a forward call.
+// The T fused cell products of a forward call (each split over its
+// contraction, with its epilogue after the sum, when the planner prefers;
+// the k-slices go to `split` when given).
 dlvm_status plan_rnn_forward(const dlvm_model* m, const void* params, const void* xs, int64_t B,
-                             void* hs, Launcher& run) {
-  const int dt = m->dtype;
-  const size_t es = elem_size(dt);
+                             void* hs, float* split, int64_t split_elems, Launcher& run) {
+  const size_t es = elem_size(m->dtype);
   const int64_t Kx = m->rnn_Kx, H = m->rnn_H;
   const void* WU = param_ptr(m, params, m->offsets[0]);
   const void* bias = param_ptr(m, params, m->offsets[1]);
   for (int64_t t = 0; t < m->rnn_T; ++t) {
-    GemmDesc d = gemm_nn(dt, dt, m->acts[0], B, H, Kx + H, 1.0f, seq_at(xs, t, B, Kx, es), WU, H,
-                         bias, seq_at(hs, t + 1, B, H, es), H);
-    d.lda = Kx;
-    d.A2 = seq_at(hs, t, B, H, es);
-    d.lda2 = H;
-    d.K1 = Kx;
+    GemmDesc d = rnn_cell(m, B, seq_at(xs, t, B, Kx, es), seq_at(hs, t, B, H, es), WU, bias,
+                          seq_at(hs, t + 1, B, H, es));
+    d.split_ws = split;
+    d.split_ws_elems = split != nullptr ? split_elems : 0;
     const dlvm_status st = run.gemm(d);
     if (st != DLVM_OK) return st;
   }
@@ -724,7 +788,6 @@ dlvm_status plan_rnn_backward(const dlvm_model* m, const void* params, const voi
   const int dt = m->dtype;
   const size_t es = elem_size(dt);
   const int64_t T = m->rnn_T, Kx = m->rnn_Kx, H = m->rnn_H;
-  const int act = m->acts[0];
   const void* WU = param_ptr(m, params, m->offsets[0]);
   const void* U = at<const void>(WU, static_cast<size_t>(Kx * H) * es);
   float* dWU = at<float>(dparams, static_cast<size_t>(m->offsets[0]) * 4);
@@ -732,16 +795,16 @@ dlvm_status plan_rnn_backward(const dlvm_model* m, const void* params, const voi
   void* dz = at<void>(ws, w.dz);
   dlvm_status st = run.run(
       elementwise_info("act_adjoint", B, H, 3.0 * double(B) * H * es), [&](hipStream_t s) {
-        return dlvm::launch_act_adjoint(dt, act, B * H, seq_at(dhs, T - 1, B, H, es),
+        return dlvm::launch_act_adjoint(dt, m->acts[0], B * H, seq_at(dhs, T - 1, B, H, es),
                                         seq_at(hs, T, B, H, es), seq_at(dz, T - 1, B, H, es), s);
       },
       "activation adjoint launch");
   if (st != DLVM_OK) return st;
   for (int64_t t = T - 1; t >= 1; --t) {
-    GemmDesc d = gemm_nt(dt, dt, act, B, H, H, seq_at(dz, t, B, H, es), H, U, H,
-                         seq_at(hs, t, B, H, es), seq_at(dhs, t - 1, B, H, es),
-                         seq_at(dz, t - 1, B, H, es));
-    d.res_pre = true;
+    GemmDesc d = rnn_recur(m, B, seq_at(dz, t, B, H, es), U, seq_at(hs, t, B, H, es),
+                           seq_at(dhs, t - 1, B, H, es), seq_at(dz, t - 1, B, H, es));
+    d.split_ws = at<float>(ws, w.splitk);
+    d.split_ws_elems = w.splitk_elems;
     if ((st = run.gemm(d)) != DLVM_OK) return st;
   }
   if (m->wrt_h0 &&
@@ -776,7 +839,9 @@ dlvm_status plan_rnn_backward(const dlvm_model* m, const void* params, const voi
 void plan_step(const dlvm_model* m, int64_t batch, std::vector<LaunchInfo>* plan) {
   Launcher dry(m, nullptr, plan, 0);
   if (m->kind == 1) {
-    plan_rnn_forward(m, nullptr, nullptr, batch, nullptr, dry);
+    const RnnWs w = rnn_ws_layout(m, batch);
+    plan_rnn_forward(m, nullptr, nullptr, batch, nullptr, at<float>(nullptr, w.splitk),
+                     w.splitk_elems, dry);
     plan_rnn_backward(m, nullptr, nullptr, nullptr, nullptr, batch, nullptr, nullptr, nullptr,
                       nullptr, dry);
   } else {
@@ -918,7 +983,9 @@ dlvm_status dlvm_rnn_create(const dlvm_rnn_desc* desc, dlvm_model** out) {
   build_layout(m);
   std::vector<LaunchInfo> plan;
   Launcher dry(m, nullptr, &plan, 0);
-  plan_rnn_forward(m, nullptr, nullptr, 1, nullptr, dry);
+  const RnnWs w1 = rnn_ws_layout(m, 1);
+  plan_rnn_forward(m, nullptr, nullptr, 1, nullptr, at<float>(nullptr, w1.splitk), w1.splitk_elems,
+                   dry);
   m->n_fwd_launches = static_cast<int32_t>(plan.size());
   plan.clear();
   plan_step(m, 1, &plan);
@@ -1190,16 +1257,19 @@ dlvm_status dlvm_check(const dlvm_model* m, void* ws, void* stream) {
 }
 
 dlvm_status dlvm_rnn_forward(const dlvm_model* m, const void* params, const void* xs,
-                             int64_t batch, void* hs, void* stream) {
+                             int64_t batch, void* hs, void* ws, size_t ws_bytes, void* stream) {
   if (m == nullptr || params == nullptr || xs == nullptr || hs == nullptr)
     return fail(DLVM_ERR_INVALID_ARG, "null argument");
   if (m->kind != 1) return fail(DLVM_ERR_UNSUPPORTED, "not a recurrent model");
   if (!aligned16(params) || !aligned16(xs) || !aligned16(hs))
     return fail(DLVM_ERR_MISALIGNED, "device pointers must be 16-byte aligned");
-  const dlvm_status st = check_batch(m, batch);
+  dlvm_status st = check_batch(m, batch);
   if (st != DLVM_OK) return st;
+  if (ws != nullptr && (st = check_ws(m, batch, ws, ws_bytes)) != DLVM_OK) return st;
+  const RnnWs w = rnn_ws_layout(m, batch);
   Launcher run(m, static_cast<hipStream_t>(stream), nullptr, 0);
-  return plan_rnn_forward(m, params, xs, batch, hs, run);
+  return plan_rnn_forward(m, params, xs, batch, hs,
+                          ws != nullptr ? at<float>(ws, w.splitk) : nullptr, w.splitk_elems, run);
 }
 
 dlvm_status dlvm_rnn_backward(const dlvm_model* m, const void* params, const void* xs,

@@ -442,6 +442,98 @@ __global__ __launch_bounds__(kBlock) void dlvm_seed_kernel(int64_t rows, int64_t
 }
 
 // ---------------------------------------------------------------------------
+// The k-slices of a split forward or input-adjoint product summed in slice
+// order (fixed order: the same result on every run), then the epilogue the
+// unsplit product applies in its last k-tile:
+//   mode 0 (forward):        out = act(alpha * sum + bias[c])      (bias for c < nvec)
+//   mode 1 (input adjoint):  out = sum * act'(aux) + R, or (sum + R) * act'(aux) with res_pre
+// aux and bias in the operand dtype TA, R and out in the output dtype TO.
+// ---------------------------------------------------------------------------
+template <typename T>
+__device__ __forceinline__ void load4f(const T* p, float (&v)[4]);
+template <>
+__device__ __forceinline__ void load4f<float>(const float* p, float (&v)[4]) {
+  const float4 x = *reinterpret_cast<const float4*>(p);
+  v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
+}
+template <>
+__device__ __forceinline__ void load4f<bf16_t>(const bf16_t* p, float (&v)[4]) {
+  const uint2 x = *reinterpret_cast<const uint2*>(p);
+  v[0] = __uint_as_float(x.x << 16); v[1] = __uint_as_float(x.x & 0xffff0000u);
+  v[2] = __uint_as_float(x.y << 16); v[3] = __uint_as_float(x.y & 0xffff0000u);
+}
+
+__device__ __forceinline__ float split_epi(int mode, int act, float alpha, float v, float b,
+                                           float g, float r, int res_pre) {
+  if (mode == 0) return apply_act(act, alpha * v + b);
+  if (res_pre) v += r;
+  if (act != ACT_NONE) v *= act_grad_from_output(act, g);
+  if (!res_pre) v += r;
+  return v;
+}
+
+template <typename TA, typename TO, bool VEC>
+__global__ __launch_bounds__(kBlock) void dlvm_split_epilogue_kernel(
+    int S, int64_t rows, int64_t cols, int64_t ld, const float* __restrict__ part,
+    int64_t c_split, int mode, int act, float alpha, const TA* __restrict__ bias, int64_t nvec,
+    const TA* __restrict__ aux, const TO* __restrict__ res, int res_pre, TO* __restrict__ out) {
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
+  const int64_t t0 = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+  const bool use_aux = mode == 1 && act != ACT_NONE && aux != nullptr;
+  const bool use_res = mode == 1 && res != nullptr;
+  if constexpr (VEC) {
+    const int64_t c4 = cols / 4;
+    for (int64_t i = t0; i < rows * c4; i += stride) {
+      const int64_t r = i / c4, c = (i - r * c4) * 4;
+      const int64_t o = r * ld + c;
+      float4 acc = load_nt(reinterpret_cast<const float4*>(part + o));
+      int q = 1;
+      for (; q + 3 < S; q += 4) {  // four slices in flight, added in slice order
+        float4 v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          v[u] = load_nt(reinterpret_cast<const float4*>(part + (q + u) * c_split + o));
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          acc.x += v[u].x; acc.y += v[u].y; acc.z += v[u].z; acc.w += v[u].w;
+        }
+      }
+      for (; q < S; ++q) {
+        const float4 v = load_nt(reinterpret_cast<const float4*>(part + q * c_split + o));
+        acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+      }
+      float b[4] = {0.0f, 0.0f, 0.0f, 0.0f}, g[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+      float rv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+      if (mode == 0 && bias != nullptr) {
+        if (c + 4 <= nvec) {
+          load4f<TA>(bias + c, b);
+        } else {
+          for (int e = 0; e < 4; ++e) b[e] = c + e < nvec ? load_as_f32<TA>(bias + c + e) : 0.0f;
+        }
+      }
+      if (use_aux) load4f<TA>(aux + o, g);
+      if (use_res) load4f<TO>(res + o, rv);
+      const float a[4] = {acc.x, acc.y, acc.z, acc.w};
+      float y[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) y[e] = split_epi(mode, act, alpha, a[e], b[e], g[e], rv[e], res_pre);
+      store4<TO>(out + o, y[0], y[1], y[2], y[3]);
+    }
+  } else {
+    for (int64_t i = t0; i < rows * cols; i += stride) {
+      const int64_t r = i / cols, c = i - r * cols;
+      const int64_t o = r * ld + c;
+      float acc = part[o];
+      for (int q = 1; q < S; ++q) acc += part[q * c_split + o];
+      const float b = (mode == 0 && bias != nullptr && c < nvec) ? load_as_f32<TA>(bias + c) : 0.0f;
+      const float g = use_aux ? load_as_f32<TA>(aux + o) : 0.0f;
+      const float rv = use_res ? load_as_f32<TO>(res + o) : 0.0f;
+      out[o] = store_cast<TO>(split_epi(mode, act, alpha, acc, b, g, rv, res_pre));
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Adjoint of an element-wise activation through its saved output:
 // out = g * act'(h), act' taken from h = act(z) (storage dtype throughout).
 // ---------------------------------------------------------------------------
@@ -783,6 +875,50 @@ hipError_t launch_split_softmax_xent(int dtype, int splits, int64_t rows, int64_
   return launch_split_softmax_typed<bf16_t, bf16_t>(
       splits, rows, classes, part, c_split, ld_part, static_cast<const bf16_t*>(bias), labels,
       scale, static_cast<bf16_t*>(dlogits), ld_dlogits, partials, bad, nb, s);
+}
+
+namespace {
+template <typename TA, typename TO>
+hipError_t launch_split_epilogue_typed(int splits, int64_t rows, int64_t cols, int64_t ld,
+                                       const float* part, int64_t c_split, int mode, int act,
+                                       float alpha, const void* bias, int64_t nvec,
+                                       const void* aux, const void* res, bool res_pre, void* out,
+                                       hipStream_t s) {
+  const bool vec = cols % 4 == 0 && ld % 4 == 0 && c_split % 4 == 0 &&
+                   ((reinterpret_cast<uintptr_t>(part) | reinterpret_cast<uintptr_t>(out) |
+                     reinterpret_cast<uintptr_t>(aux) | reinterpret_cast<uintptr_t>(res) |
+                     reinterpret_cast<uintptr_t>(bias)) & 15u) == 0;
+  const unsigned nb = grid_for(vec ? rows * cols / 4 : rows * cols, 8192);
+  const TA* b = static_cast<const TA*>(bias);
+  const TA* a = static_cast<const TA*>(aux);
+  const TO* r = static_cast<const TO*>(res);
+  TO* o = static_cast<TO*>(out);
+  if (vec)
+    launch_kernel(dlvm_split_epilogue_kernel<TA, TO, true>, dim3(nb), dim3(kBlock), s, splits, rows,
+                  cols, ld, part, c_split, mode, act, alpha, b, nvec, a, r, res_pre ? 1 : 0, o);
+  else
+    launch_kernel(dlvm_split_epilogue_kernel<TA, TO, false>, dim3(nb), dim3(kBlock), s, splits,
+                  rows, cols, ld, part, c_split, mode, act, alpha, b, nvec, a, r, res_pre ? 1 : 0, o);
+  return hipGetLastError();
+}
+}  // namespace
+
+hipError_t launch_split_epilogue(int dtype, int out_dtype, int mode, int splits, int64_t rows,
+                                 int64_t cols, int64_t ld, const float* part, int64_t c_split,
+                                 int act, float alpha, const void* bias, int64_t nvec,
+                                 const void* aux, const void* res, bool res_pre, void* out,
+                                 hipStream_t s) {
+  if (dtype == F32)
+    return launch_split_epilogue_typed<float, float>(splits, rows, cols, ld, part, c_split, mode,
+                                                     act, alpha, bias, nvec, aux, res, res_pre,
+                                                     out, s);
+  if (out_dtype == F32)
+    return launch_split_epilogue_typed<bf16_t, float>(splits, rows, cols, ld, part, c_split, mode,
+                                                      act, alpha, bias, nvec, aux, res, res_pre,
+                                                      out, s);
+  return launch_split_epilogue_typed<bf16_t, bf16_t>(splits, rows, cols, ld, part, c_split, mode,
+                                                     act, alpha, bias, nvec, aux, res, res_pre,
+                                                     out, s);
 }
 
 hipError_t launch_act_adjoint(int dtype, int act, int64_t n, const void* g, const void* h,

@@ -128,20 +128,26 @@ int64_t split_need(const GemmDesc& d, int splits) {
 // Tile configuration forced through the environment variable
 // DLVM_GEMM_CONFIG (for tests and tuning), or -1. A forced configuration that
 // cannot run the product is ignored.
-int forced_config() {
-  const char* v = std::getenv("DLVM_GEMM_CONFIG");
+int env_int(const char* name) {
+  const char* v = std::getenv(name);
   if (v == nullptr || *v == 0) return -1;
   char* end = nullptr;
   const long c = std::strtol(v, &end, 10);
   return (end != nullptr && *end == 0) ? static_cast<int>(c) : -1;
 }
+int forced_config() { return env_int("DLVM_GEMM_CONFIG"); }
+
+// Number of k-slices forced through DLVM_GEMM_SPLITS (for tests and tuning)
+// on products the caller lets split with their epilogue, or -1.
+int forced_splits() { return env_int("DLVM_GEMM_SPLITS"); }
 
 namespace {
 
 // The configuration and split (only products wrt the weights, TN, with
 // scratch for the partials) that the estimate prefers. `assume_aligned`
 // ignores the operands' addresses (for sizing scratch before they exist).
-GemmPlan choose(const GemmDesc& d, bool assume_aligned, int64_t capacity, int forced) {
+GemmPlan choose(const GemmDesc& d, bool assume_aligned, int64_t capacity, int forced,
+                int fsplits) {
   const bool can_async = assume_aligned ? (d.dtype == BF16 && d.lda % 8 == 0 && d.ldb % 8 == 0 &&
                                            d.K % 8 == 0 && d.ldc % 8 == 0 &&
                                            (d.A2 == nullptr || (d.lda2 % 8 == 0 && d.K1 % 8 == 0)))
@@ -165,18 +171,21 @@ GemmPlan choose(const GemmDesc& d, bool assume_aligned, int64_t capacity, int fo
     if (t.cfg == 15 && forced != 15) continue;
     if (forced >= 0 && t.cfg != forced) continue;
     for (int sp = 1; sp <= kMaxSplits; sp *= 2) {
-      if (sp > 1 && d.A2 != nullptr) break;  // two-phase products are not split
-      if (d.splits_hint > 0 && split_need(d, d.splits_hint) <= capacity) {
+      // a two-phase product's slices must not straddle its phase boundary
+      if (sp > 1 && d.A2 != nullptr && d.K1 % slice_k(d.K, sp) != 0) continue;
+      const bool forcing = fsplits > 0 && d.split_epilogue;  // (overrides the caller's split)
+      if (!forcing && d.splits_hint > 0 && split_need(d, d.splits_hint) <= capacity) {
         // the caller's split (a multiple of 64 k per slice, whole slices)
         if (sp != d.splits_hint && !(sp == 1 && d.splits_hint == 1)) {
           if (sp > d.splits_hint) break;
           continue;
         }
       } else if (sp > 1) {
-        if (d.layout != Layout::TN || capacity <= 0) break;
+        if ((d.layout != Layout::TN && !d.split_epilogue) || capacity <= 0) break;
         if (slice_k(d.K, sp) < kMinChunk || ceil_div(d.K, slice_k(d.K, sp)) < sp) break;
         if (split_need(d, sp) > capacity) break;
       }
+      if (forcing && sp != fsplits) continue;
       const double e = estimate(d, t, sp);
       if (best == nullptr || e < best_t * 0.97) {  // prefer earlier (larger) tiles, fewer splits
         best = &t;
@@ -185,8 +194,11 @@ GemmPlan choose(const GemmDesc& d, bool assume_aligned, int64_t capacity, int fo
       }
     }
   }
-  if (best == nullptr)  // a forced configuration that cannot run this product is ignored
-    return choose(d, assume_aligned, capacity, -1);
+  if (best == nullptr) {  // a forced configuration or split that cannot run is ignored
+    if (forced >= 0 || fsplits > 0) return choose(d, assume_aligned, capacity, -1, -1);
+    best = &kTiles[3];      // (not reached: the 32 x 32 tile runs every product unsplit)
+    best_s = 1;
+  }
   GemmPlan pl{};
   pl.cfg = best->cfg;
   pl.bm = best->bm;
@@ -201,12 +213,13 @@ GemmPlan choose(const GemmDesc& d, bool assume_aligned, int64_t capacity, int fo
 }  // namespace
 
 GemmPlan plan_gemm(const GemmDesc& d) {
-  return choose(d, false, d.split_ws != nullptr ? d.split_ws_elems : 0, forced_config());
+  return choose(d, false, d.split_ws != nullptr ? d.split_ws_elems : 0, forced_config(),
+                forced_splits());
 }
 
 int64_t split_ws_elems(const GemmDesc& d) {
-  if (d.layout != Layout::TN) return 0;
-  const GemmPlan pl = choose(d, true, int64_t(1) << 40, forced_config());
+  if (d.layout != Layout::TN && !d.split_epilogue) return 0;
+  const GemmPlan pl = choose(d, true, int64_t(1) << 40, forced_config(), forced_splits());
   return pl.splits > 1 ? split_need(d, pl.splits) : 0;
 }
 
@@ -254,7 +267,12 @@ gemm::Params make_params(const GemmDesc& d, const GemmPlan& pl) {
     p.c_split = d.M * d.ldc;
     p.colsum = d.colsum != nullptr ? d.split_ws + pl.splits * p.c_split : nullptr;
     p.cs_split = p.nvec;
-    if (d.layout == Layout::NN) p.bias = nullptr;  // slices are raw products
+    if (d.layout != Layout::TN) {  // slices are raw products (the epilogue follows the sum)
+      p.bias = p.aux = p.residual = nullptr;
+      p.act = ACT_NONE;
+      p.alpha = 1.0f;
+      p.res_pre = 0;
+    }
   } else {
     p.c_split = p.cs_split = 0;
   }
@@ -280,9 +298,10 @@ hipError_t launch_gemm(const GemmDesc& d, const GemmPlan& pl, hipStream_t s) {
   vector_ok(d, va, vb);
   const gemm::Params p = make_params(d, pl);
   const unsigned grid = grid_of(pl);
+  const int out = pl.splits > 1 ? F32 : d.out_dtype;  // split slices: float32 partials
   switch (d.layout) {
-    case Layout::NN: return gemm::launch_nn(p, d.dtype, d.out_dtype, pl.cfg, grid, va, vb, s);
-    case Layout::NT: return gemm::launch_nt(p, d.dtype, d.out_dtype, pl.cfg, grid, va, vb, s);
+    case Layout::NN: return gemm::launch_nn(p, d.dtype, out, pl.cfg, grid, va, vb, s);
+    case Layout::NT: return gemm::launch_nt(p, d.dtype, out, pl.cfg, grid, va, vb, s);
     case Layout::TN: return gemm::launch_tn(p, d.dtype, pl.cfg, grid, va, vb, s);
   }
   return hipErrorInvalidValue;

@@ -121,8 +121,14 @@ __device__ __forceinline__ int split_slice(Params& p, int bid) {
     bid -= sl * tiles;
     const int64_t k0 = static_cast<int64_t>(sl) * p.k_chunk;
     const int64_t kl = p.K - k0 < p.k_chunk ? p.K - k0 : p.k_chunk;
-    const int64_t sa = AK ? k0 : k0 * p.lda;
+    int64_t sa = AK ? k0 : k0 * p.lda;
     const int64_t sb = BKM ? k0 : k0 * p.ldb;
+    if (p.A2 != nullptr && k0 >= p.K1) {
+      // a slice of the second phase (slices never straddle K1)
+      p.A = p.A2;
+      p.lda = p.lda2;
+      sa = AK ? k0 - p.K1 : (k0 - p.K1) * p.lda2;
+    }
     p.A = static_cast<const T*>(p.A) + sa;
     p.B = static_cast<const T*>(p.B) + sb;
     p.a_bytes -= static_cast<uint32_t>(sa * static_cast<int64_t>(sizeof(T)));

@@ -65,6 +65,11 @@ struct GemmDesc {
   const void* A2;
   int64_t lda2, K1;
   bool res_pre;  // NT: the residual is added before act' is applied
+  // NN / NT: the planner may split K (scratch permitting): the k-slices write
+  // raw float32 partials to split_ws and launch_split_epilogue sums them and
+  // applies the product's epilogue. A two-phase product is split only at
+  // slice boundaries that fall on K1.
+  bool split_epilogue;
 };
 
 // How one product is launched: tile configuration and grid.
@@ -139,6 +144,17 @@ hipError_t launch_sgd(int dtype, int64_t n, void* params, float* master, const f
 // classes <= c < ld.
 hipError_t launch_seed(int dtype, int64_t rows, int64_t classes, int64_t ld, const float* seed,
                        void* dz, hipStream_t s);
+
+// Sum of the k-slices of a split NN (mode 0) or NT (mode 1) product in slice
+// order, then its epilogue: mode 0 out = act(alpha * sum + bias[c]) (bias for
+// c < nvec, operand dtype); mode 1 out = sum * act'(aux) + res, or
+// (sum + res) * act'(aux) with res_pre (aux operand dtype; res, out output
+// dtype). part[s * c_split + r * ld + c], out[r * ld + c], c < cols.
+hipError_t launch_split_epilogue(int dtype, int out_dtype, int mode, int splits, int64_t rows,
+                                 int64_t cols, int64_t ld, const float* part, int64_t c_split,
+                                 int act, float alpha, const void* bias, int64_t nvec,
+                                 const void* aux, const void* res, bool res_pre, void* out,
+                                 hipStream_t s);
 
 // out[i] = g[i] * act'(h[i]) for i < n, act' from the saved output h = act(z)
 // (storage dtype `dtype` for all three).

@@ -235,14 +235,15 @@ def test_rnn_handle_plan_and_errors():
     assert L.dlvm_gradient(m._h, A, A, A, B, A, A, A, A, ws, None) == dl.ERR_UNSUPPORTED
     assert L.dlvm_vjp(m._h, A, A, A, B, A, A, A, ws, None) == dl.ERR_UNSUPPORTED
     # recurrent entry points: nulls, declared outputs, alignment, batch, workspace
-    assert L.dlvm_rnn_forward(m._h, None, A, B, A, None) == dl.ERR_INVALID_ARG
-    assert L.dlvm_rnn_forward(m._h, A, A + 2, B, A, None) == dl.ERR_MISALIGNED
-    assert L.dlvm_rnn_forward(m._h, A, A, B + 1, A, None) == dl.ERR_INVALID_ARG
+    assert L.dlvm_rnn_forward(m._h, None, A, B, A, None, 0, None) == dl.ERR_INVALID_ARG
+    assert L.dlvm_rnn_forward(m._h, A, A + 2, B, A, None, 0, None) == dl.ERR_MISALIGNED
+    assert L.dlvm_rnn_forward(m._h, A, A, B + 1, A, None, 0, None) == dl.ERR_INVALID_ARG
+    assert L.dlvm_rnn_forward(m._h, A, A, B, A, A, ws - 1, None) == dl.ERR_WORKSPACE
     assert L.dlvm_rnn_backward(m._h, A, A, A, A, B, A, None, A, A, ws, None) == dl.ERR_INVALID_ARG
     assert L.dlvm_rnn_backward(m._h, A, A, A, A, B, A, A, None, A, ws, None) == dl.ERR_INVALID_ARG
     assert L.dlvm_rnn_backward(m._h, A, A, A, A, B, A, A, A, A, ws - 1, None) == dl.ERR_WORKSPACE
     mlp = dl.Model((8, 8), ("none",), batch_max=4)
-    assert L.dlvm_rnn_forward(mlp._h, A, A, 4, A, None) == dl.ERR_UNSUPPORTED
+    assert L.dlvm_rnn_forward(mlp._h, A, A, 4, A, None, 0, None) == dl.ERR_UNSUPPORTED
     # create validation
     for bad in (dict(steps=0), dict(in_width=0), dict(hidden=0), dict(batch_max=0)):
         args = dict(steps=4, in_width=8, hidden=8, batch_max=4)

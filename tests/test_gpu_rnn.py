@@ -78,7 +78,7 @@ def sync():
     torch.cuda.synchronize()
 
 
-def _run(wl, inputs, wrt_x, wrt_h0, B=None):
+def _run(wl, inputs, wrt_x, wrt_h0, B=None, use_ws=True):
     """Forward and backward on the GPU; host copies of every result."""
     import torch
     xs, h0, W, U, b, dhs = inputs
@@ -90,11 +90,11 @@ def _run(wl, inputs, wrt_x, wrt_h0, B=None):
     xd = to_dev(xs, wl.dtype)
     hs = torch.full((T + 1, B, H), float("nan"), dtype=torch_dtype(wl.dtype), device=dev)
     hs[0] = to_dev(h0, wl.dtype)
-    m.forward(P, xd, B, hs)
+    ws = torch.full((m.workspace_bytes(B),), 0xFF, dtype=torch.uint8, device=dev)
+    m.forward(P, xd, B, hs, ws if use_ws else None)
     dP = torch.full((m.param_count(),), float("nan"), device=dev)
     dxs = torch.full((T, B, Kx), float("nan"), device=dev) if wrt_x else None
     dh0 = torch.full((B, H), float("nan"), device=dev) if wrt_h0 else None
-    ws = torch.full((m.workspace_bytes(B),), 0xFF, dtype=torch.uint8, device=dev)
     m.backward(P, xd, hs, to_dev(dhs, wl.dtype), B, dP, dxs, dh0, ws)
     sync()
     dW, dU, db = m.split_cell(dP)
@@ -193,3 +193,34 @@ def test_rnn_backward_is_deterministic():
     b = _run(wl, inputs, True, True)
     for k in ("hs", "dW", "dU", "db", "dxs", "dh0"):
         np.testing.assert_array_equal(a[k], b[k])
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("splits", [2, 4])
+def test_split_cell_and_recurrent_products(dtype, splits, monkeypatch):
+    """The cell products and recurrent adjoints computed in k-slices (forced),
+    summed in slice order with the epilogue (bias + activation, residual +
+    act') applied after the sum; the cell's slices fall on its phase boundary.
+    Two runs are bitwise equal."""
+    monkeypatch.setenv("DLVM_GEMM_SPLITS", str(splits))
+    wl, inputs = _case(4, 512, 512, 100, dtype, "tanh", seed=21)
+    m = dl.Rnn(4, 512, 512, "tanh", dtype, True, True, 100)
+    names = [p["name"] for p in m.plan(100)]
+    assert any(n.startswith("gemm_nn") and n.endswith(f"s{splits}") for n in names)
+    assert names.count("split_epilogue") >= 4
+    got = _run(wl, inputs, True, True)
+    _compare(wl, got, inputs, True, True)
+    again = _run(wl, inputs, True, True)
+    for k in ("hs", "dW", "dU", "db", "dxs", "dh0"):
+        np.testing.assert_array_equal(got[k], again[k])
+
+
+def test_forward_without_workspace_matches_split_forward():
+    """dlvm_rnn_forward without a workspace runs every cell product unsplit; the
+    states agree with the split forward to the storage precision."""
+    wl = workloads.RNN_WORKLOADS["r1"]
+    inputs = workloads.make_rnn_inputs(wl, batch=128)
+    a = _run(wl, inputs, False, False, use_ws=True)
+    b = _run(wl, inputs, False, False, use_ws=False)
+    assert rel_l2(a["hs"], b["hs"]) <= 1e-2
+    _compare(wl, b, inputs, False, False)
