@@ -18,3 +18,4 @@ from .mlp import (MlpSpec, apply_act, chain8, dense_forward, dense_vjp_input,  #
                   dense_vjp_params, gemm, mlp_forward, mlp_gradient, mlp_vjp, sgd_bf16,
                   sgd_f32, softmax_xent)
 from .rnn import RnnSpec, rnn_forward, rnn_vjp  # noqa: F401
+from .chain import chain_order, chain_product, chain_product_in_order, parenthesisation  # noqa: F401

@@ -821,3 +821,59 @@ def test_rnn_bf16_states_are_stored_as_bf16():
                                xs, h0, W, U, b)
     assert not np.array_equal(exact, hs)
     assert np.max(np.abs(exact - hs)) < 0.05
+
+
+# --------------------------------------------------------------------------
+# Matrix multiplication reordering (§3.1.2): oracle.chain_order / chain_product
+# --------------------------------------------------------------------------
+def _brute_force_chain(d, i, j):
+    """Minimal multiply-add count of A_i..A_j over every parenthesisation."""
+    if i == j:
+        return 0
+    return min(_brute_force_chain(d, i, k) + _brute_force_chain(d, k + 1, j) + d[i] * d[k + 1] * d[j + 1]
+               for k in range(i, j))
+
+
+def test_chain_order_textbook_example():
+    """The textbook's six-matrix example (tests/golden/matrix_chain_textbook.json)."""
+    g = json.load(open(os.path.join(GOLDEN, "matrix_chain_textbook.json")))
+    cost, split = oracle.chain_order(g["dims"])
+    assert cost == g["min_cost"]
+    assert oracle.parenthesisation(split) == g["order"]
+    sub, _ = oracle.chain_order(g["dims"][1:6])    # A1..A4 of the example's 0-based names
+    assert sub == g["cost_2_5"]
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_chain_order_against_brute_force(seed):
+    """The dynamic programme's cost is the minimum over all parenthesisations
+    (enumerated), and the order it returns achieves that cost."""
+    rng = np.random.default_rng(seed)
+    n = int(rng.integers(1, 8))
+    d = [int(v) for v in rng.integers(1, 60, size=n + 1)]
+    cost, split = oracle.chain_order(d)
+    assert cost == _brute_force_chain(d, 0, n - 1)
+
+    def order_cost(i, j):
+        if i == j:
+            return 0
+        k = split[i][j]
+        return order_cost(i, k) + order_cost(k + 1, j) + d[i] * d[k + 1] * d[j + 1]
+
+    assert order_cost(0, n - 1) == cost
+
+
+def test_chain_products_agree_with_library_and_every_order():
+    """The left-to-right product equals numpy's multi_dot (a library routine
+    that picks its own order), and the product in the optimal order equals it
+    too (associativity), in float64."""
+    rng = np.random.default_rng(3)
+    d = [7, 33, 4, 19, 2, 25]
+    mats = [rng.standard_normal((d[i], d[i + 1])).astype(np.float32) for i in range(len(d) - 1)]
+    ref = np.linalg.multi_dot([m.astype(np.float64) for m in mats])
+    got = oracle.chain_product(mats)
+    np.testing.assert_allclose(got, ref, rtol=1e-12, atol=1e-12)
+    _, split = oracle.chain_order(d)
+    np.testing.assert_allclose(oracle.chain_product_in_order(mats, split), ref, rtol=1e-12, atol=1e-12)
+    single = oracle.chain_product(mats[:1])
+    np.testing.assert_array_equal(single, mats[0].astype(np.float64))
