@@ -45,7 +45,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=None)
     ap.add_argument("--warmup", type=int, default=None)
     ap.add_argument("--workload", default="c2",
-                    choices=sorted(workloads.WORKLOADS) + sorted(workloads.RNN_WORKLOADS))
+                    choices=sorted(workloads.WORKLOADS) + sorted(workloads.RNN_WORKLOADS) +
+                    sorted(workloads.CHAIN_WORKLOADS))
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="budget of the oracle CPU baseline (0 disables it)")
     ap.add_argument("--entry", default="gradient", choices=["gradient", "vjp"],
@@ -195,7 +196,8 @@ def vjp_bench(args, wl, m, P, xd, dP, dx, ws, stream, steps, warmup):
                       "mfma_frac": round(flops * sps / 1e12 / PEAK_TFLOPS[wl.dtype], 4)}), flush=True)
 
 
-def measure(m, wl, step, eager_step, steps, warmup, with_sgd, flags_ws=None):
+def measure(m, wl, step, eager_step, steps, warmup, with_sgd, flags_ws=None,
+            bound_by_intensity=False):
     """Warm up, find the launch position that takes the most time, time `steps`
     whole steps, then time the dominant launch on its stream over as many steps.
 
@@ -212,7 +214,7 @@ def measure(m, wl, step, eager_step, steps, warmup, with_sgd, flags_ws=None):
         raise RuntimeError("device flags raised during warm-up")
 
     # find the launch that takes the most time (outside the timed region)
-    B = wl.batch
+    B = getattr(wl, "batch", 1)
     plan = m.plan(B)
     if not with_sgd:
         plan = plan[:-1]
@@ -254,7 +256,9 @@ def measure(m, wl, step, eager_step, steps, warmup, with_sgd, flags_ws=None):
     m.probe_disarm()
     avg_s = ms_dom / max(n_dom, 1) / 1e3
 
-    if dom["flops"] > 0:
+    ridge = PEAK_TFLOPS[wl.dtype] * 1e12 / (PEAK_HBM_GBS * 1e9)  # flop per byte
+    mfma = dom["flops"] > 0 and (not bound_by_intensity or dom["flops"] >= ridge * dom["bytes"])
+    if mfma:
         achieved = dom["flops"] / avg_s / 1e12
         peak = PEAK_TFLOPS[wl.dtype]
         roof = {"bound": "mfma", "achieved": round(achieved, 3), "peak": peak,
@@ -271,8 +275,8 @@ def measure(m, wl, step, eager_step, steps, warmup, with_sgd, flags_ws=None):
     return sps, elapsed, roof, groups
 
 
-def result_line(wl, sps, elapsed, steps, warmup, roof, config, **extra) -> dict:
-    tflops = wl.flops() * sps / 1e12
+def result_line(wl, sps, elapsed, steps, warmup, roof, config, step_flops=None, **extra) -> dict:
+    tflops = (wl.flops() if step_flops is None else step_flops) * sps / 1e12
     out = {
         "metric": METRIC,
         "value": round(sps, 3),
@@ -382,6 +386,101 @@ def rnn_cpu_baseline(wl, budget_s: float) -> dict | None:
             "kind": "oracle", "sample": sample}
 
 
+def chain_main(args, wl) -> None:
+    """A step of a chain workload: one dlvm_chain_run of the chain in its
+    optimal order. Also timed: the same chain left to right (what it costs
+    without reordering)."""
+    import torch
+
+    import paper_1711_03016_amd as dl
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    tdt = torch.float32 if wl.dtype == "f32" else torch.bfloat16
+    dims, n = list(wl.dims), wl.n
+    mats = [torch.from_numpy(a).to(dev).to(tdt).contiguous() for a in workloads.make_chain_inputs(dims)]
+    out = torch.empty((dims[0], dims[-1]), device=dev)
+    cost, split = dl.chain_order(dims)
+    l2r = [[(j - 1 if j > i else -1) for j in range(n)] for i in range(n)]
+    l2r_cost = sum(dims[0] * dims[k + 1] * dims[k + 2] for k in range(n - 1))
+    m = dl.Chain(wl.dtype, dims)
+    m_l2r = dl.Chain(wl.dtype, dims, l2r)
+    ws = torch.empty(max(m.workspace_bytes(1), m_l2r.workspace_bytes(1)), dtype=torch.uint8,
+                     device=dev)
+    steps = args.steps if args.steps is not None else 200
+    warmup = args.warmup if args.warmup is not None else 20
+    stream = torch.cuda.current_stream()
+
+    def step():
+        m.run(mats, out, ws, stream)
+
+    def step_l2r():
+        m_l2r.run(mats, out, ws, stream)
+
+    for _ in range(warmup):
+        step_l2r()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step_l2r()
+    torch.cuda.synchronize()
+    elapsed_l2r = time.perf_counter() - t0
+
+    sps, elapsed, roof, groups = measure(m, wl, step, step, steps, warmup, False,
+                                         bound_by_intensity=True)
+    config = {"workload": f"{wl.name}: {wl.title}", "dims": dims,
+              "order": oracle_free_order(split), "parallelism": "none"}
+    out_line = result_line(wl, sps, elapsed, steps, warmup, roof, config, step_flops=2 * cost,
+                           launch="eager",
+                           workspace_bytes=int(ws.numel()), launch_groups_us=groups,
+                           multiply_adds=cost, left_to_right_multiply_adds=l2r_cost,
+                           left_to_right_steps_per_s=round(steps / elapsed_l2r, 3))
+    del mats, out, ws
+    out_line["cpu_baseline"] = chain_cpu_baseline(wl, args.cpu_seconds)
+    print(json.dumps(out_line), flush=True)
+
+
+def oracle_free_order(split, i=0, j=None) -> str:
+    """The order of a split table as text (written here so that the timed
+    path does not need the oracle)."""
+    if j is None:
+        j = len(split) - 1
+    if i == j:
+        return f"A{i}"
+    k = split[i][j]
+    return "(" + oracle_free_order(split, i, k) + oracle_free_order(split, k + 1, j) + ")"
+
+
+def chain_cpu_baseline(wl, budget_s: float) -> dict | None:
+    """The oracle's chain product (float64, left to right as it stands) on the
+    first rows of A_0; the work is linear in those rows."""
+    if budget_s <= 0:
+        return None
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([d.get("num_threads", 1) for d in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover - threadpoolctl is optional
+        threads = os.cpu_count() or 1
+    mats = workloads.make_chain_inputs(wl.dims)
+    rows = wl.dims[0]
+    while rows > 16 and rows * sum(wl.dims[k + 1] * wl.dims[k + 2] for k in range(wl.n - 1)) > 2e9:
+        rows //= 2
+    sample = [mats[0][:rows]] + mats[1:]
+    n, el = 0, 0.0
+    while True:
+        t0 = time.perf_counter()
+        oracle.chain_product(sample, wl.dtype)
+        el += time.perf_counter() - t0
+        n += 1
+        if el >= budget_s or el * (n + 1) / n > 2 * budget_s:
+            break
+    per = el / n * wl.dims[0] / rows
+    return {"value": 1.0 / per, "unit": "steps/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{n} oracle chain products (float64, left to right) on {rows} of "
+                      f"{wl.dims[0]} rows of A_0 in {el:.1f} s, scaled by {wl.dims[0]}/{rows}"}
+
+
 def main():
     args = parse()
     if args.copy_calibration:
@@ -393,6 +492,8 @@ def main():
         sys.exit(2)
     if args.workload in workloads.RNN_WORKLOADS:
         return rnn_main(args, workloads.RNN_WORKLOADS[args.workload])
+    if args.workload in workloads.CHAIN_WORKLOADS:
+        return chain_main(args, workloads.CHAIN_WORKLOADS[args.workload])
     import torch
 
     import paper_1711_03016_amd as dl

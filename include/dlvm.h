@@ -211,6 +211,51 @@ dlvm_status dlvm_rnn_backward(const dlvm_model* m, const void* params, const voi
                               float* dxs, float* dh0, void* ws, size_t ws_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------
+ * Matrix multiplication reordering (section 3.1.2)
+ * ------------------------------------------------------------------------- */
+
+/* The chain A_0 A_1 ... A_{n-1}, A_i of shape dims[i] x dims[i+1], can be
+ * evaluated in any order (associativity); a p x q by q x r product costs
+ * p q r multiply-adds. Computes the order of least total cost (over every
+ * sub-chain, the best outermost cut given the best orders of both sides; the
+ * smallest cut among equal costs) and returns that cost (saturated at
+ * INT64_MAX), or -1 for invalid arguments (n outside [1, 32], a dimension
+ * outside [1, 2^20]). If `split` is not NULL it receives the n x n row-major
+ * table of cuts: split[i * n + j] = k means A_i..A_j is computed as
+ * (A_i..A_k)(A_{k+1}..A_j); entries with i >= j are -1. Host only. */
+int64_t dlvm_chain_order(int32_t n, const int64_t* dims, int32_t* split);
+
+/* Workspace bytes dlvm_matrix_chain needs for this chain and order (split
+ * NULL: the optimal order), 0 for invalid arguments. */
+size_t dlvm_matrix_chain_ws_bytes(int32_t dtype, int32_t n, const int64_t* dims,
+                                  const int32_t* split);
+
+/* out (float32 [dims[0], dims[n]]) = A_0 ... A_{n-1}, evaluated in the order
+ * of `split` (an n x n table as above, caller's host memory), or in the
+ * optimal order when split is NULL. n in [2, 32]. `mats` is a host array of n
+ * device pointers to row-major matrices of `dtype` (F32, or BF16 with float32
+ * accumulate); intermediate products are kept in `ws` in `dtype` (bf16
+ * intermediates are rounded to nearest even). One matrix-core product per
+ * cut, in evaluation order on `stream`; a product with too few output tiles
+ * for the device may be computed in k-slices (float32, in `ws`) summed in
+ * slice order by one more launch. DLVM_ERR_INVALID_ARG for a split table
+ * that is not an order of the chain. */
+dlvm_status dlvm_matrix_chain(int32_t dtype, int32_t n, const int64_t* dims,
+                              const void* const* mats, const int32_t* split, float* out,
+                              void* ws, size_t ws_bytes, void* stream);
+
+/* A chain of fixed shapes and order as a handle (order: split, or the
+ * optimal one when NULL): dlvm_chain_run computes the same product as
+ * dlvm_matrix_chain; dlvm_workspace_bytes (batch 1), dlvm_plan_size /
+ * dlvm_plan_entry (batch 1: the chain's products and slice sums, then an
+ * empty update entry), the timing probe and dlvm_destroy take the handle;
+ * the network calls refuse it. */
+dlvm_status dlvm_chain_create(int32_t dtype, int32_t n, const int64_t* dims, const int32_t* split,
+                              dlvm_model** out);
+dlvm_status dlvm_chain_run(const dlvm_model* m, const void* const* mats, float* out, void* ws,
+                           size_t ws_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
  * Captured training step (HIP graph)
  * ------------------------------------------------------------------------- */
 

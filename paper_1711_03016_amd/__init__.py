@@ -102,6 +102,14 @@ _SIGS = {
     "dlvm_rnn_forward": (_I32, [_P, _P, _P, _I64, _P, _P, ctypes.c_size_t, _P]),
     "dlvm_rnn_backward": (_I32, [_P, _P, _P, _P, _P, _I64, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "dlvm_rnn_cell_forward": (_I32, [_I32, _I32, _I64, _I64, _I64, _I64, _P, _P, _P, _P, _P, _P]),
+    "dlvm_chain_order": (_I64, [_I32, ctypes.POINTER(_I64), ctypes.POINTER(_I32)]),
+    "dlvm_matrix_chain_ws_bytes": (ctypes.c_size_t, [_I32, _I32, ctypes.POINTER(_I64),
+                                                     ctypes.POINTER(_I32)]),
+    "dlvm_matrix_chain": (_I32, [_I32, _I32, ctypes.POINTER(_I64), ctypes.POINTER(_P),
+                                 ctypes.POINTER(_I32), _P, _P, ctypes.c_size_t, _P]),
+    "dlvm_chain_create": (_I32, [_I32, _I32, ctypes.POINTER(_I64), ctypes.POINTER(_I32),
+                                 ctypes.POINTER(_P)]),
+    "dlvm_chain_run": (_I32, [_P, ctypes.POINTER(_P), _P, _P, ctypes.c_size_t, _P]),
     "dlvm_graph_launch": (_I32, [_P, _P]),
     "dlvm_graph_destroy": (None, [_P]),
 }
@@ -398,3 +406,65 @@ def chain8(rows, cols, z, bias, x_skip, zbar, xbar, loss, ws, stream=None):
 def sgd(dtype, n, params, master, grads, lr, stream=None):
     _check(lib().dlvm_sgd(DTYPES[dtype], int(n), _ptr(params), _ptr(master), _ptr(grads),
                           float(lr), _stream(stream)))
+
+
+# ---------------------------------------------------------------------------
+# matrix multiplication reordering
+# ---------------------------------------------------------------------------
+def _split_arg(split, n):
+    if split is None:
+        return None
+    flat = [int(v) for row in split for v in row]
+    assert len(flat) == n * n
+    return (_I32 * (n * n))(*flat)
+
+
+def chain_order(dims) -> tuple[int, list[list[int]]]:
+    """(multiply-add count of the best order, n x n split table) for a chain
+    with shapes dims[i] x dims[i+1] (``dlvm_chain_order``)."""
+    n = len(dims) - 1
+    d = (_I64 * (n + 1))(*[int(v) for v in dims])
+    sp = (_I32 * (n * n))()
+    cost = int(lib().dlvm_chain_order(n, d, sp))
+    if cost < 0:
+        raise DlvmError(ERR_INVALID_ARG, "invalid chain")
+    return cost, [list(sp[i * n:(i + 1) * n]) for i in range(n)]
+
+
+def matrix_chain_ws_bytes(dtype, dims, split=None) -> int:
+    n = len(dims) - 1
+    d = (_I64 * (n + 1))(*[int(v) for v in dims])
+    return int(lib().dlvm_matrix_chain_ws_bytes(DTYPES[dtype], n, d, _split_arg(split, n)))
+
+
+def matrix_chain(dtype, dims, mats, out, ws, split=None, stream=None) -> None:
+    """out = mats[0] @ ... @ mats[-1] in the given (or the optimal) order."""
+    n = len(dims) - 1
+    d = (_I64 * (n + 1))(*[int(v) for v in dims])
+    ptrs = (_P * n)(*[_ptr(m) for m in mats])
+    nb = 0 if ws is None else ws.numel() * ws.element_size()
+    _check(lib().dlvm_matrix_chain(DTYPES[dtype], n, d, ptrs, _split_arg(split, n), _ptr(out),
+                                   _ptr(ws), nb, _stream(stream)))
+
+
+class Chain(Model):
+    """A matrix chain of fixed shapes and order (``dlvm_chain_create``)."""
+
+    def __init__(self, dtype, dims, split=None):
+        self.dims = tuple(int(v) for v in dims)
+        n = len(self.dims) - 1
+        self.dtype, self.n = dtype, n
+        self.widths, self.acts, self.loss, self.batch_max = (), (), None, 1
+        d = (_I64 * (n + 1))(*self.dims)
+        h = _P()
+        _check(lib().dlvm_chain_create(DTYPES[dtype], n, d, _split_arg(split, n), ctypes.byref(h)))
+        self._h = h
+
+    @property
+    def n_layers(self) -> int:
+        return 0
+
+    def run(self, mats, out, ws, stream=None) -> None:
+        ptrs = (_P * self.n)(*[_ptr(m) for m in mats])
+        _check(lib().dlvm_chain_run(self._h, ptrs, _ptr(out), _ptr(ws),
+                                    ws.numel() * ws.element_size(), _stream(stream)))

@@ -10,6 +10,8 @@
 // code elimination, section 3.1.4).
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
+#include <climits>
 #include <cstdio>
 #include <cstring>
 #include <new>
@@ -52,8 +54,10 @@ struct dlvm_model {
   // Recurrent networks (kind 1): T steps of the cell
   // hs[t+1] = act(xs[t] . W + hs[t] . U + b); L = 1 and widths = {Kx + H, H},
   // the one "layer" being the stacked [W; U] and b.
-  int32_t kind = 0;              // 0: dense network, 1: recurrent network
+  int32_t kind = 0;              // 0: dense network, 1: recurrent network, 2: matrix chain
   int64_t rnn_T = 0, rnn_Kx = 0, rnn_H = 0;
+  std::vector<int64_t> chain_dims;   // matrix chains (kind 2): shapes and order
+  std::vector<int32_t> chain_cuts;
   int32_t wrt_h0 = 0;
   mutable int32_t n_fwd_launches = 0;  // launches of a recurrent forward call
   std::vector<int64_t> offsets;  // element offsets: W_l, b_l interleaved
@@ -300,6 +304,10 @@ class Launcher {
     if (plan_ != nullptr) {
       plan_->push_back(std::move(info));
       return DLVM_OK;
+    }
+    if (m_ == nullptr) {  // a call without a model handle: nothing to record
+      const hipError_t e = launch(main_);
+      return e != hipSuccess ? hip_fail(e, what) : DLVM_OK;
     }
     ProbeState& p = m_->probe;
     const bool rec = p.armed && (p.index < 0 || p.index == idx) && p.used < p.capacity;
@@ -740,7 +748,12 @@ RnnWs rnn_ws_layout(const dlvm_model* m, int64_t B) {
   return w;
 }
 
+size_t chain_model_ws(const dlvm_model* m);
+dlvm_status chain_model_run(const dlvm_model* m, const void* const* mats, float* out, void* ws,
+                            Launcher& run);
+
 size_t ws_total(const dlvm_model* m, int64_t batch) {
+  if (m->kind == 2) return chain_model_ws(m);
   return m->kind == 1 ? rnn_ws_layout(m, batch).total : ws_layout(m, batch).total;
 }
 
@@ -838,7 +851,10 @@ dlvm_status plan_rnn_backward(const dlvm_model* m, const void* params, const voi
 // (recurrent networks).
 void plan_step(const dlvm_model* m, int64_t batch, std::vector<LaunchInfo>* plan) {
   Launcher dry(m, nullptr, plan, 0);
-  if (m->kind == 1) {
+  if (m->kind == 2) {
+    std::vector<const void*> mats(m->chain_dims.size() - 1, nullptr);
+    chain_model_run(m, mats.data(), nullptr, nullptr, dry);
+  } else if (m->kind == 1) {
     const RnnWs w = rnn_ws_layout(m, batch);
     plan_rnn_forward(m, nullptr, nullptr, batch, nullptr, at<float>(nullptr, w.splitk),
                      w.splitk_elems, dry);
@@ -1291,6 +1307,255 @@ dlvm_status dlvm_rnn_backward(const dlvm_model* m, const void* params, const voi
   st = plan_rnn_backward(m, params, xs, hs, dhs, batch, dparams, dxs, dh0, ws, run);
   m->n_grad_launches = run.launches();
   return st;
+}
+
+// ---------------------------------------------------------------------------
+// Matrix multiplication reordering (section 3.1.2)
+// ---------------------------------------------------------------------------
+}  // extern "C"
+
+namespace {
+
+constexpr int kChainMax = 32;
+
+// Multiply-adds of the best order of every sub-chain A_i..A_j (A_i is
+// d[i] x d[i+1]; a p x q by q x r product costs p q r), sub-chains taken by
+// increasing length, the outermost cut of each recorded in split[i * n + j]
+// (the smallest cut among equal costs). Returns the whole chain's cost.
+unsigned __int128 chain_optimal(int n, const int64_t* d, int32_t* split) {
+  std::vector<unsigned __int128> cost(static_cast<size_t>(n) * n, 0);
+  for (int len = 2; len <= n; ++len) {
+    for (int i = 0; i + len - 1 < n; ++i) {
+      const int j = i + len - 1;
+      bool have = false;
+      for (int k = i; k < j; ++k) {
+        const unsigned __int128 c = cost[i * n + k] + cost[(k + 1) * n + j] +
+                                    static_cast<unsigned __int128>(d[i]) * d[k + 1] * d[j + 1];
+        if (!have || c < cost[i * n + j]) {
+          cost[i * n + j] = c;
+          split[i * n + j] = k;
+          have = true;
+        }
+      }
+    }
+  }
+  return cost[n - 1];
+}
+
+// Every cut reachable from the whole chain lies inside its sub-chain.
+bool chain_split_valid(int n, const int32_t* split, int i, int j) {
+  if (i == j) return true;
+  const int k = split[i * n + j];
+  return k >= i && k < j && chain_split_valid(n, split, i, k) &&
+         chain_split_valid(n, split, k + 1, j);
+}
+
+// The product that computes A_i..A_j from its two sides (a and b), into dst:
+// the planner may split its contraction (the k-slices' sum then applies the
+// epilogue) when the scratch holds the slices.
+GemmDesc chain_product(int dtype, int n, const int64_t* d, const int32_t* split, int i, int j,
+                       const void* a, const void* b, void* dst) {
+  const int k = split[i * n + j];
+  const bool root = i == 0 && j == n - 1;
+  GemmDesc g = gemm_nn(dtype, root ? DLVM_F32 : dtype, DLVM_ACT_NONE, d[i], d[j + 1], d[k + 1],
+                       1.0f, a, b, d[j + 1], nullptr, dst, d[j + 1]);
+  g.split_epilogue = true;
+  return g;
+}
+
+// Workspace offsets of the intermediate products (every inner node of the
+// order but the whole chain), in evaluation order; returns the end offset.
+// `split_elems` receives the largest float32 k-slice scratch any product of
+// the order may use.
+size_t chain_layout(int dtype, int n, const int64_t* d, const int32_t* split, int i, int j,
+                    std::vector<size_t>& off, size_t base, int64_t& split_elems) {
+  if (i == j) return base;
+  const int k = split[i * n + j];
+  base = chain_layout(dtype, n, d, split, i, k, off, base, split_elems);
+  base = chain_layout(dtype, n, d, split, k + 1, j, off, base, split_elems);
+  split_elems = std::max(split_elems, dlvm::split_ws_elems(chain_product(
+                                          dtype, n, d, split, i, j, nullptr, nullptr, nullptr)));
+  if (!(i == 0 && j == n - 1)) {
+    off[i * n + j] = base;
+    base = align_up(base + static_cast<size_t>(d[i] * d[j + 1]) * elem_size(dtype));
+  }
+  return base;
+}
+
+// Total workspace of an order: the intermediates, then the k-slice scratch.
+size_t chain_ws(int dtype, int n, const int64_t* d, const int32_t* split,
+                std::vector<size_t>& off, size_t& split_off, int64_t& split_elems) {
+  split_elems = 0;
+  split_off = chain_layout(dtype, n, d, split, 0, n - 1, off, 0, split_elems);
+  return align_up(split_off + static_cast<size_t>(split_elems) * 4);
+}
+
+dlvm_status chain_args(int32_t dtype, int32_t n, const int64_t* dims, const int32_t* split) {
+  if (!valid_dtype(dtype)) return fail(DLVM_ERR_INVALID_ARG, "unknown dtype");
+  if (n < 2 || n > kChainMax || dims == nullptr)
+    return fail(DLVM_ERR_INVALID_ARG, "a chain has 2 to 32 matrices and their dims");
+  for (int i = 0; i <= n; ++i)
+    if (dims[i] < 1 || dims[i] > (int64_t(1) << 20))
+      return fail(DLVM_ERR_INVALID_ARG, "every dimension must be in [1, 2^20]");
+  if (split != nullptr && !chain_split_valid(n, split, 0, n - 1))
+    return fail(DLVM_ERR_INVALID_ARG, "the split table is not an order of the chain");
+  return DLVM_OK;
+}
+
+// The order to run: the caller's, or the optimal one.
+std::vector<int32_t> chain_split(int n, const int64_t* dims, const int32_t* split) {
+  std::vector<int32_t> s(static_cast<size_t>(n) * n, -1);
+  if (split != nullptr)
+    std::memcpy(s.data(), split, s.size() * sizeof(int32_t));
+  else
+    chain_optimal(n, dims, s.data());
+  return s;
+}
+
+// Evaluate A_i..A_j into dst (the whole chain: float32 `out`; an inner node:
+// its workspace buffer in the storage dtype); returns the operand pointer.
+struct ChainRun {
+  int dtype, n;
+  const int64_t* d;
+  const void* const* mats;
+  const int32_t* split;
+  const std::vector<size_t>* off;
+  float* out;
+  void* ws;
+  float* split_ws;
+  int64_t split_elems;
+};
+
+dlvm_status chain_eval(const ChainRun& c, int i, int j, const void** result, Launcher& run) {
+  if (i == j) {
+    *result = c.mats[i];
+    return DLVM_OK;
+  }
+  const int k = c.split[i * c.n + j];
+  const void* a = nullptr;
+  const void* b = nullptr;
+  dlvm_status st = chain_eval(c, i, k, &a, run);
+  if (st == DLVM_OK) st = chain_eval(c, k + 1, j, &b, run);
+  if (st != DLVM_OK) return st;
+  const bool root = i == 0 && j == c.n - 1;
+  void* dst = root ? static_cast<void*>(c.out) : at<void>(c.ws, (*c.off)[i * c.n + j]);
+  GemmDesc g = chain_product(c.dtype, c.n, c.d, c.split, i, j, a, b, dst);
+  g.split_ws = c.split_ws;
+  g.split_ws_elems = c.split_elems;
+  *result = dst;
+  return run.gemm(g);
+}
+
+size_t chain_model_ws(const dlvm_model* m) {
+  const int n = static_cast<int>(m->chain_dims.size()) - 1;
+  std::vector<size_t> off(static_cast<size_t>(n) * n, 0);
+  size_t split_off = 0;
+  int64_t split_elems = 0;
+  return std::max<size_t>(
+      chain_ws(m->dtype, n, m->chain_dims.data(), m->chain_cuts.data(), off, split_off, split_elems),
+      16);
+}
+
+dlvm_status chain_model_run(const dlvm_model* m, const void* const* mats, float* out, void* ws,
+                            Launcher& run) {
+  const int n = static_cast<int>(m->chain_dims.size()) - 1;
+  std::vector<size_t> off(static_cast<size_t>(n) * n, 0);
+  size_t split_off = 0;
+  int64_t split_elems = 0;
+  chain_ws(m->dtype, n, m->chain_dims.data(), m->chain_cuts.data(), off, split_off, split_elems);
+  const ChainRun c{m->dtype, n, m->chain_dims.data(), mats, m->chain_cuts.data(), &off, out, ws,
+                   split_elems > 0 ? at<float>(ws, split_off) : nullptr, split_elems};
+  const void* res = nullptr;
+  return chain_eval(c, 0, n - 1, &res, run);
+}
+
+}  // namespace
+
+extern "C" {
+
+dlvm_status dlvm_chain_create(int32_t dtype, int32_t n, const int64_t* dims, const int32_t* split,
+                              dlvm_model** out) {
+  if (out == nullptr) return fail(DLVM_ERR_INVALID_ARG, "null argument");
+  *out = nullptr;
+  const dlvm_status st = chain_args(dtype, n, dims, split);
+  if (st != DLVM_OK) return st;
+  dlvm_model* m = new (std::nothrow) dlvm_model();
+  if (m == nullptr) return fail(DLVM_ERR_INVALID_ARG, "out of host memory");
+  m->kind = 2;
+  m->dtype = dtype;
+  m->loss = -1;
+  m->batch_max = 1;
+  m->chain_dims.assign(dims, dims + n + 1);
+  m->chain_cuts = chain_split(n, dims, split);
+  std::vector<LaunchInfo> plan;
+  plan_step(m, 1, &plan);
+  m->n_grad_launches = static_cast<int32_t>(plan.size());
+  *out = m;
+  return DLVM_OK;
+}
+
+dlvm_status dlvm_chain_run(const dlvm_model* m, const void* const* mats, float* out, void* ws,
+                           size_t ws_bytes, void* stream) {
+  if (m == nullptr || mats == nullptr || out == nullptr)
+    return fail(DLVM_ERR_INVALID_ARG, "null argument");
+  if (m->kind != 2) return fail(DLVM_ERR_UNSUPPORTED, "not a matrix-chain handle");
+  const int n = static_cast<int>(m->chain_dims.size()) - 1;
+  for (int i = 0; i < n; ++i) {
+    if (mats[i] == nullptr) return fail(DLVM_ERR_INVALID_ARG, "null matrix");
+    if (!aligned16(mats[i])) return fail(DLVM_ERR_MISALIGNED, "device pointers must be 16-byte aligned");
+  }
+  if (!aligned16(out)) return fail(DLVM_ERR_MISALIGNED, "device pointers must be 16-byte aligned");
+  const dlvm_status st = check_ws(m, 1, ws, ws_bytes);
+  if (st != DLVM_OK) return st;
+  Launcher run(m, static_cast<hipStream_t>(stream), nullptr, 0);
+  return chain_model_run(m, mats, out, ws, run);
+}
+
+int64_t dlvm_chain_order(int32_t n, const int64_t* dims, int32_t* split) {
+  if (n < 1 || n > kChainMax || dims == nullptr) return -1;
+  for (int i = 0; i <= n; ++i)
+    if (dims[i] < 1 || dims[i] > (int64_t(1) << 20)) return -1;
+  std::vector<int32_t> s(static_cast<size_t>(n) * n, -1);
+  const unsigned __int128 c = chain_optimal(n, dims, s.data());
+  if (split != nullptr) std::memcpy(split, s.data(), s.size() * sizeof(int32_t));
+  const unsigned __int128 lim = static_cast<unsigned __int128>(INT64_MAX);
+  return static_cast<int64_t>(c > lim ? lim : c);
+}
+
+size_t dlvm_matrix_chain_ws_bytes(int32_t dtype, int32_t n, const int64_t* dims,
+                                  const int32_t* split) {
+  if (chain_args(dtype, n, dims, split) != DLVM_OK) return 0;
+  const std::vector<int32_t> sp = chain_split(n, dims, split);
+  std::vector<size_t> off(static_cast<size_t>(n) * n, 0);
+  size_t split_off = 0;
+  int64_t split_elems = 0;
+  return std::max<size_t>(chain_ws(dtype, n, dims, sp.data(), off, split_off, split_elems), 16);
+}
+
+dlvm_status dlvm_matrix_chain(int32_t dtype, int32_t n, const int64_t* dims,
+                              const void* const* mats, const int32_t* split, float* out, void* ws,
+                              size_t ws_bytes, void* stream) {
+  dlvm_status st = chain_args(dtype, n, dims, split);
+  if (st != DLVM_OK) return st;
+  if (mats == nullptr || out == nullptr) return fail(DLVM_ERR_INVALID_ARG, "null argument");
+  for (int i = 0; i < n; ++i) {
+    if (mats[i] == nullptr) return fail(DLVM_ERR_INVALID_ARG, "null matrix");
+    if (!aligned16(mats[i])) return fail(DLVM_ERR_MISALIGNED, "device pointers must be 16-byte aligned");
+  }
+  if (!aligned16(out)) return fail(DLVM_ERR_MISALIGNED, "device pointers must be 16-byte aligned");
+  const std::vector<int32_t> sp = chain_split(n, dims, split);
+  std::vector<size_t> off(static_cast<size_t>(n) * n, 0);
+  size_t split_off = 0;
+  int64_t split_elems = 0;
+  const size_t need = chain_ws(dtype, n, dims, sp.data(), off, split_off, split_elems);
+  if (need > 0 && (ws == nullptr || ws_bytes < need))
+    return fail(DLVM_ERR_WORKSPACE, "workspace is smaller than dlvm_matrix_chain_ws_bytes");
+  if (ws != nullptr && !aligned16(ws)) return fail(DLVM_ERR_MISALIGNED, "workspace is not 16-byte aligned");
+  const ChainRun c{dtype, n, dims, mats, sp.data(), &off, out, ws,
+                   split_elems > 0 ? at<float>(ws, split_off) : nullptr, split_elems};
+  Launcher run(nullptr, static_cast<hipStream_t>(stream), nullptr, 0);
+  const void* res = nullptr;
+  return chain_eval(c, 0, n - 1, &res, run);
 }
 
 // ---------------------------------------------------------------------------

@@ -264,3 +264,38 @@ def test_rnn_dead_outputs_are_not_computed():
     assert nt(full) + pairs(full) == nt(lean) + 2
     assert sum(e["flops"] for e in full) - sum(e["flops"] for e in lean) == \
         2 * 16 * 32 * 32 + 2 * 4 * 16 * 32 * 64
+
+
+def test_chain_order_matches_oracle():
+    """The library's host-side order (its own recurrence) against the oracle's:
+    the same least cost and the same cuts (smallest cut among equal costs)."""
+    import numpy as np
+    import oracle
+    rng = np.random.default_rng(17)
+    for _ in range(300):
+        n = int(rng.integers(1, 10))
+        d = [int(v) for v in rng.integers(1, 200, size=n + 1)]
+        assert dl.chain_order(d) == oracle.chain_order(d)
+    assert dl.chain_order([30, 35, 15, 5, 10, 20, 25])[0] == 15125
+    # large dimensions: the cost stays exact in 64 bits here
+    d = [1 << 20, 1 << 20, 1 << 10, 1 << 20]
+    assert dl.chain_order(d) == oracle.chain_order(d)
+
+
+def test_matrix_chain_errors_are_host_side():
+    L = dl.lib()
+    A = 0x100000
+    n = 3
+    dims = (ctypes.c_int64 * 4)(8, 16, 4, 8)
+    mats = (ctypes.c_void_p * 3)(A, A, A)
+    assert L.dlvm_chain_order(0, dims, None) == -1
+    assert L.dlvm_chain_order(n, (ctypes.c_int64 * 4)(8, 0, 4, 8), None) == -1
+    assert L.dlvm_matrix_chain(0, 1, dims, mats, None, A, A, 1 << 20, None) == dl.ERR_INVALID_ARG
+    bad = (ctypes.c_int32 * 9)(-1, 0, 2, -1, -1, 1, -1, -1, -1)   # cut of (0,2) outside [0, 2)
+    assert L.dlvm_matrix_chain(0, n, dims, mats, bad, A, A, 1 << 20, None) == dl.ERR_INVALID_ARG
+    assert L.dlvm_matrix_chain_ws_bytes(0, n, dims, bad) == 0
+    mis = (ctypes.c_void_p * 3)(A, A + 4, A)
+    assert L.dlvm_matrix_chain(0, n, dims, mis, None, A, A, 1 << 20, None) == dl.ERR_MISALIGNED
+    need = L.dlvm_matrix_chain_ws_bytes(0, n, dims, None)
+    assert need >= 8 * 4 * 4 or need >= 16 * 8 * 4
+    assert L.dlvm_matrix_chain(0, n, dims, mats, None, A, A, need - 1, None) == dl.ERR_WORKSPACE

@@ -248,3 +248,35 @@ def make_rnn_inputs(wl: RnnWorkload, batch: int | None = None, seed: int | None 
     b = _draw(_rng(seed, 205), (H,), ("uniform", -0.1, 0.1))
     dhs = _draw(_rng(seed, 206), (T, B, H), ("normal_var", 1.0)) / np.float32(B)
     return xs, h0, W, U, b, dhs
+
+
+# ---------------------------------------------------------------------------
+# Matrix chains (the reordering row): seeded inputs.
+# ---------------------------------------------------------------------------
+@dataclass(frozen=True)
+class ChainWorkload:
+    """The product A_0 ... A_{n-1}, A_i of shape dims[i] x dims[i+1], entries
+    N(0, 1 / dims[i]) (each product keeps unit-variance entries)."""
+
+    name: str
+    title: str
+    dims: tuple
+    dtype: str
+
+    @property
+    def n(self) -> int:
+        return len(self.dims) - 1
+
+
+CHAIN_WORKLOADS = {
+    "m1": ChainWorkload(
+        "m1", "bf16 chain 16384x4096 . 4096x64 . 64x4096 . 4096x64 . 64x1024 (low-rank factors)",
+        (16384, 4096, 64, 4096, 64, 1024), "bf16"),
+}
+
+
+def make_chain_inputs(dims, seed: int | None = None):
+    """The chain's matrices, float32."""
+    seed = SEED_BASE if seed is None else seed
+    return [_draw(_rng(seed, 300 + i), (dims[i], dims[i + 1]), ("normal_var", 1.0 / dims[i]))
+            for i in range(len(dims) - 1)]
