@@ -364,7 +364,7 @@ __device__ __forceinline__ void epilogue_lds(const Params& p, const f32x16 (&acc
 // One output tile (`tile` from split_slice) of the direct-to-LDS kernel, LDS
 // ring at `smem` (STAGES * (BM + BN) * 2 * BK bytes, 1024-byte aligned).
 template <typename TO, bool AK, bool BKM, int BM, int BN, int BK, int WM, int WN, int STAGES,
-          int EPI>
+          int EPI, bool PH2 = false>
 __device__ __forceinline__ void async_gemm_tile(Params& p, const int tile, char* smem) {
   constexpr int NW = WM * WN;
   constexpr int THREADS = 64 * NW;
@@ -388,12 +388,13 @@ __device__ __forceinline__ void async_gemm_tile(Params& p, const int tile, char*
   const int64_t n0 = static_cast<int64_t>(tn) * BN;
   const bf16_t* __restrict__ A = static_cast<const bf16_t*>(p.A);
   const bf16_t* __restrict__ B = static_cast<const bf16_t*>(p.B);
-  // k-tiles of the two phases of the contraction (one phase unless A2 is set)
-  const int nk1 = static_cast<int>((p.K1 + BK - 1) / BK);
-  const int nk = nk1 + static_cast<int>((p.K - p.K1 + BK - 1) / BK);
+  // k-tiles of the two phases of the contraction (PH2), else of its one phase
+  const int64_t K1 = PH2 ? p.K1 : p.K;
+  const int nk1 = static_cast<int>((K1 + BK - 1) / BK);
+  const int nk = PH2 ? nk1 + static_cast<int>((p.K - K1 + BK - 1) / BK) : nk1;
   // valid k of the last tile of phase 1 and of phase 2
-  const int kv1 = static_cast<int>(p.K1 - static_cast<int64_t>(nk1 - 1) * BK);
-  const int kv2 = static_cast<int>(p.K - p.K1 - static_cast<int64_t>(nk - nk1 - 1) * BK);
+  const int kv1 = static_cast<int>(K1 - static_cast<int64_t>(nk1 - 1) * BK);
+  const int kv2 = PH2 ? static_cast<int>(p.K - K1 - static_cast<int64_t>(nk - nk1 - 1) * BK) : BK;
 
   f32x16 acc[TM][TN];
 #pragma unroll
@@ -412,7 +413,7 @@ __device__ __forceinline__ void async_gemm_tile(Params& p, const int tile, char*
 
   auto issue = [&](int kt) {
     char* st = smem + (kt % STAGES) * STAGE;
-    const StageSrc<bf16_t, BKM> q = stage_src<bf16_t, BKM>(p, A, B, kt, nk1, BK);
+    const StageSrc<bf16_t, BKM> q = stage_src<bf16_t, BKM, PH2>(p, A, B, kt, nk1, BK);
     async_tile<AK, BM, BK, NW>(q.a, q.lda, m0, p.M, q.k0, q.klim, st, wave, lane);
     async_tile<BKM, BN, BK, NW>(q.b, p.ldb, n0, p.N, q.k0, q.klim, st + A_BYTES, wave, lane);
   };
@@ -428,7 +429,7 @@ __device__ __forceinline__ void async_gemm_tile(Params& p, const int tile, char*
     barrier_only();
     char* As = smem + (kt % STAGES) * STAGE;
     char* Bs = As + A_BYTES;
-    const int kv = kt == nk1 - 1 ? kv1 : (kt == nk - 1 ? kv2 : BK);
+    const int kv = kt == nk1 - 1 ? kv1 : ((PH2 && kt == nk - 1) ? kv2 : BK);
     if (kv < BK) {
       zero_k_tail<AK, BM, BK, THREADS>(As, kv, tid);
       zero_k_tail<BKM, BN, BK, THREADS>(Bs, kv, tid);
@@ -471,11 +472,15 @@ __device__ __forceinline__ void async_gemm_tile(Params& p, const int tile, char*
 }
 
 template <typename TO, bool AK, bool BKM, int BM, int BN, int BK, int WM, int WN, int STAGES,
-          int EPI>
+          int EPI, bool PH2>
 __global__ __launch_bounds__(64 * WM * WN) void dlvm_gemm_async_kernel(Params p) {
   __shared__ __attribute__((aligned(1024))) char smem[STAGES * (BM + BN) * 2 * BK];
   const int tile = split_slice<bf16_t, AK, BKM>(p, static_cast<int>(blockIdx.x));
-  async_gemm_tile<TO, AK, BKM, BM, BN, BK, WM, WN, STAGES, EPI>(p, tile, smem);
+  // a k-slice of a split two-phase product lies in one phase
+  if (PH2 && p.splits <= 1)
+    async_gemm_tile<TO, AK, BKM, BM, BN, BK, WM, WN, STAGES, EPI, PH2>(p, tile, smem);
+  else
+    async_gemm_tile<TO, AK, BKM, BM, BN, BK, WM, WN, STAGES, EPI, false>(p, tile, smem);
 }
 
 // The two adjoint products of one dense layer in one launch (blocks [0, n1):
@@ -501,20 +506,20 @@ __global__ __launch_bounds__(64 * WM * WN) void dlvm_gemm_async_pair_kernel(Para
 //   13: 256 x 256, BK 32, 2 x 4 waves (128 x 64 per wave),  4 stages (128 KiB LDS)
 constexpr int kAsyncFirst = 10;
 
-template <typename TO, bool AK, bool BKM, int EPI>
+template <typename TO, bool AK, bool BKM, int EPI, bool PH2 = false>
 hipError_t launch_async(const Params& p, int cfg, unsigned grid, hipStream_t s) {
   switch (cfg) {
     case 10:
-      launch_kernel((dlvm_gemm_async_kernel<TO, AK, BKM, 256, 256, 64, 2, 4, 2, EPI>), dim3(grid), dim3(512), s, p);
+      launch_kernel((dlvm_gemm_async_kernel<TO, AK, BKM, 256, 256, 64, 2, 4, 2, EPI, PH2>), dim3(grid), dim3(512), s, p);
       break;
     case 11:
-      launch_kernel((dlvm_gemm_async_kernel<TO, AK, BKM, 256, 128, 64, 2, 2, 3, EPI>), dim3(grid), dim3(256), s, p);
+      launch_kernel((dlvm_gemm_async_kernel<TO, AK, BKM, 256, 128, 64, 2, 2, 3, EPI, PH2>), dim3(grid), dim3(256), s, p);
       break;
     case 12:
-      launch_kernel((dlvm_gemm_async_kernel<TO, AK, BKM, 128, 128, 64, 2, 2, 4, EPI>), dim3(grid), dim3(256), s, p);
+      launch_kernel((dlvm_gemm_async_kernel<TO, AK, BKM, 128, 128, 64, 2, 2, 4, EPI, PH2>), dim3(grid), dim3(256), s, p);
       break;
     default:
-      launch_kernel((dlvm_gemm_async_kernel<TO, AK, BKM, 256, 256, 32, 2, 4, 4, EPI>), dim3(grid), dim3(512), s, p);
+      launch_kernel((dlvm_gemm_async_kernel<TO, AK, BKM, 256, 256, 32, 2, 4, 4, EPI, PH2>), dim3(grid), dim3(512), s, p);
       break;
   }
   return hipGetLastError();

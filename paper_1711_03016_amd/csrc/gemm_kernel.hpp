@@ -98,10 +98,15 @@ struct StageSrc {
   const T* b;
   int64_t k0, klim;
 };
-template <typename T, bool BKM>
+// PH2 false: the product has one phase (A2 unused) and no per-stage choice is made.
+template <typename T, bool BKM, bool PH2>
 __device__ __forceinline__ StageSrc<T, BKM> stage_src(const Params& p, const T* A, const T* B,
                                                       int64_t kt, int64_t nk1, int64_t kstage) {
   StageSrc<T, BKM> s;
+  if constexpr (!PH2) {
+    s.a = A; s.lda = p.lda; s.b = B; s.k0 = kt * kstage; s.klim = p.K;
+    return s;
+  }
   const bool ph2 = kt >= nk1;
   s.a = ph2 ? static_cast<const T*>(p.A2) : A;
   s.lda = ph2 ? p.lda2 : p.lda;
@@ -403,7 +408,7 @@ constexpr int gemm_smem_bytes() {
 
 // One output tile of a product (`tile` from split_slice), LDS at `smem`.
 template <typename T, typename TO, bool AK, bool BKM, int BM, int BN, int WM, int WN, int WK,
-          int KSEG, bool VA, bool VB, int EPI>
+          int KSEG, bool VA, bool VB, int EPI, bool PH2 = false>
 __device__ __forceinline__ void gemm_tile(Params& p, const int tile, char* smem) {
   constexpr int THREADS = 64 * WM * WN * WK;
   constexpr int BK = Elem<T>::BK;
@@ -447,10 +452,10 @@ __device__ __forceinline__ void gemm_tile(Params& p, const int tile, char* smem)
 
   TileLoader<T, AK, BM, THREADS, VA, KSEG> la;
   TileLoader<T, BKM, BN, THREADS, VB, KSEG> lb;
-  const int64_t nk1 = (p.K1 + KSTAGE - 1) / KSTAGE;
-  const int64_t nk = nk1 + (p.K - p.K1 + KSTAGE - 1) / KSTAGE;
+  const int64_t nk1 = PH2 ? (p.K1 + KSTAGE - 1) / KSTAGE : (p.K + KSTAGE - 1) / KSTAGE;
+  const int64_t nk = PH2 ? nk1 + (p.K - p.K1 + KSTAGE - 1) / KSTAGE : nk1;
   auto load_stage = [&](int64_t kt) {
-    const StageSrc<T, BKM> q = stage_src<T, BKM>(p, A, B, kt, nk1, KSTAGE);
+    const StageSrc<T, BKM> q = stage_src<T, BKM, PH2>(p, A, B, kt, nk1, KSTAGE);
     la.load(q.a, q.lda, m0, p.M, q.k0, q.klim, tid);
     lb.load(q.b, p.ldb, n0, p.N, q.k0, q.klim, tid);
   };
@@ -579,11 +584,15 @@ __device__ __forceinline__ void gemm_tile(Params& p, const int tile, char* smem)
 }
 
 template <typename T, typename TO, bool AK, bool BKM, int BM, int BN, int WM, int WN, int WK,
-          int KSEG, bool VA, bool VB, int EPI>
+          int KSEG, bool VA, bool VB, int EPI, bool PH2>
 __global__ __launch_bounds__(64 * WM * WN * WK) void dlvm_gemm_kernel(Params p) {
   __shared__ __attribute__((aligned(16))) char smem[gemm_smem_bytes<T, BM, BN, WK, KSEG>()];
   const int tile = split_slice<T, AK, BKM>(p, static_cast<int>(blockIdx.x));
-  gemm_tile<T, TO, AK, BKM, BM, BN, WM, WN, WK, KSEG, VA, VB, EPI>(p, tile, smem);
+  // a k-slice of a split two-phase product lies in one phase
+  if (PH2 && p.splits <= 1)
+    gemm_tile<T, TO, AK, BKM, BM, BN, WM, WN, WK, KSEG, VA, VB, EPI, PH2>(p, tile, smem);
+  else
+    gemm_tile<T, TO, AK, BKM, BM, BN, WM, WN, WK, KSEG, VA, VB, EPI, false>(p, tile, smem);
 }
 
 // The two adjoint products of one dense layer in one launch: blocks
@@ -612,39 +621,39 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void dlvm_gemm_pair_kernel(Param
 //   2: 128 x  32, 4 x 1 waves,             2 segments   narrow outputs (N <= 32)
 //   3:  32 x  32, 1 wave x 4 k-groups,     4 segments   small products (latency-bound)
 //   4:  64 x  64, 2 x 2 waves x 2 k-groups, 2 segments  (512 threads) medium-small products
-template <typename T, typename TO, bool AK, bool BKM, bool VA, bool VB, int EPI>
+template <typename T, typename TO, bool AK, bool BKM, bool VA, bool VB, int EPI, bool PH2 = false>
 hipError_t launch_cfg(const Params& p, int cfg, unsigned grid, hipStream_t s) {
   switch (cfg) {
     case 0:
-      launch_kernel((dlvm_gemm_kernel<T, TO, AK, BKM, 128, 128, 2, 2, 1, 1, VA, VB, EPI>), dim3(grid), dim3(256), s, p);
+      launch_kernel((dlvm_gemm_kernel<T, TO, AK, BKM, 128, 128, 2, 2, 1, 1, VA, VB, EPI, PH2>), dim3(grid), dim3(256), s, p);
       break;
     case 1:
-      launch_kernel((dlvm_gemm_kernel<T, TO, AK, BKM, 64, 64, 2, 2, 1, 2, VA, VB, EPI>), dim3(grid), dim3(256), s, p);
+      launch_kernel((dlvm_gemm_kernel<T, TO, AK, BKM, 64, 64, 2, 2, 1, 2, VA, VB, EPI, PH2>), dim3(grid), dim3(256), s, p);
       break;
     case 2:
-      launch_kernel((dlvm_gemm_kernel<T, TO, AK, BKM, 128, 32, 4, 1, 1, 2, VA, VB, EPI>), dim3(grid), dim3(256), s, p);
+      launch_kernel((dlvm_gemm_kernel<T, TO, AK, BKM, 128, 32, 4, 1, 1, 2, VA, VB, EPI, PH2>), dim3(grid), dim3(256), s, p);
       break;
     case 3:
-      launch_kernel((dlvm_gemm_kernel<T, TO, AK, BKM, 32, 32, 1, 1, 4, 4, VA, VB, EPI>), dim3(grid), dim3(256), s, p);
+      launch_kernel((dlvm_gemm_kernel<T, TO, AK, BKM, 32, 32, 1, 1, 4, 4, VA, VB, EPI, PH2>), dim3(grid), dim3(256), s, p);
       break;
     case 5:
-      launch_kernel((dlvm_gemm_kernel<T, TO, AK, BKM, 32, 32, 1, 1, 4, 8, VA, VB, EPI>), dim3(grid), dim3(256), s, p);
+      launch_kernel((dlvm_gemm_kernel<T, TO, AK, BKM, 32, 32, 1, 1, 4, 8, VA, VB, EPI, PH2>), dim3(grid), dim3(256), s, p);
       break;
     default:
-      launch_kernel((dlvm_gemm_kernel<T, TO, AK, BKM, 64, 64, 2, 2, 2, 2, VA, VB, EPI>), dim3(grid), dim3(512), s, p);
+      launch_kernel((dlvm_gemm_kernel<T, TO, AK, BKM, 64, 64, 2, 2, 2, 2, VA, VB, EPI, PH2>), dim3(grid), dim3(512), s, p);
       break;
   }
   return hipGetLastError();
 }
 
-template <typename T, typename TO, bool AK, bool BKM, int EPI>
+template <typename T, typename TO, bool AK, bool BKM, int EPI, bool PH2 = false>
 hipError_t launch_vec(const Params& p, int cfg, unsigned grid, bool va, bool vb, hipStream_t s) {
   if (va) {
-    return vb ? launch_cfg<T, TO, AK, BKM, true, true, EPI>(p, cfg, grid, s)
-              : launch_cfg<T, TO, AK, BKM, true, false, EPI>(p, cfg, grid, s);
+    return vb ? launch_cfg<T, TO, AK, BKM, true, true, EPI, PH2>(p, cfg, grid, s)
+              : launch_cfg<T, TO, AK, BKM, true, false, EPI, PH2>(p, cfg, grid, s);
   }
-  return vb ? launch_cfg<T, TO, AK, BKM, false, true, EPI>(p, cfg, grid, s)
-            : launch_cfg<T, TO, AK, BKM, false, false, EPI>(p, cfg, grid, s);
+  return vb ? launch_cfg<T, TO, AK, BKM, false, true, EPI, PH2>(p, cfg, grid, s)
+            : launch_cfg<T, TO, AK, BKM, false, false, EPI, PH2>(p, cfg, grid, s);
 }
 
 // The two adjoint products of a layer (TN wrt the weights, NT wrt the input)
