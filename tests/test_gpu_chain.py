@@ -85,3 +85,27 @@ def test_chain_handle_matches_stateless_call():
     torch.cuda.synchronize()
     assert torch.equal(a, b)
     assert sum(p["flops"] for p in h.plan(1)) == 2 * dl.chain_order(dims)[0]
+
+
+@pytest.mark.parametrize("dims", [
+    [1, 1, 1],                         # two 1 x 1 matrices
+    [1, 300, 1],                       # a dot product
+    [300, 1, 300],                     # an outer product
+    [17, 1, 9, 1, 33],
+])
+def test_degenerate_chains(dims):
+    mats = workloads.make_chain_inputs(dims, seed=12)
+    ref = oracle.chain_product(mats)
+    assert rel_l2(_run("f32", dims, mats), ref) <= 1e-5
+    assert rel_l2(_run("bf16", dims, mats), oracle.chain_product(mats, "bf16")) <= TOL["bf16"]
+
+
+def test_longest_chain():
+    """32 matrices (the maximum), shapes 1..24."""
+    rng = np.random.default_rng(77)
+    dims = [int(v) for v in rng.integers(1, 25, size=33)]
+    mats = workloads.make_chain_inputs(dims, seed=13)
+    ref = oracle.chain_product(mats)
+    cost, split = dl.chain_order(dims)
+    assert (cost, split) == oracle.chain_order(dims)
+    assert rel_l2(_run("f32", dims, mats), ref) <= 1e-5

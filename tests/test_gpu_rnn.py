@@ -224,3 +224,15 @@ def test_forward_without_workspace_matches_split_forward():
     b = _run(wl, inputs, False, False, use_ws=False)
     assert rel_l2(a["hs"], b["hs"]) <= 1e-2
     _compare(wl, b, inputs, False, False)
+
+
+@pytest.mark.parametrize("dtype,act,T,Kx,H,B", [
+    ("f32", "tanh", 3, 1, 1, 1),      # one input, one unit, one row
+    ("f32", "relu", 2, 3, 5, 2),
+    ("bf16", "sigmoid", 4, 2, 3, 5),
+    ("bf16", "tanh", 2, 8, 8, 1),
+])
+def test_rnn_degenerate_sizes(dtype, act, T, Kx, H, B):
+    wl, inputs = _case(T, Kx, H, B, dtype, act, seed=33)
+    got = _run(wl, inputs, True, True)
+    _compare(wl, got, inputs, True, True)
