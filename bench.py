@@ -67,11 +67,15 @@ def parse():
 
 
 def kernel_source_hash() -> str:
-    """Hash of the library's kernel sources (a traffic record is valid only for them)."""
+    """Hash of the library's device sources, the .hip and .hpp files (a traffic
+    record is valid only for them; the host planner's choices are part of the
+    launch name a record is matched on)."""
     import hashlib
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_1711_03016_amd", "csrc")
     for name in sorted(os.listdir(csrc)):
+        if not name.endswith((".hip", ".hpp")):
+            continue
         with open(os.path.join(csrc, name), "rb") as f:
             h.update(name.encode() + b"\0" + f.read())
     return h.hexdigest()[:16]

@@ -150,7 +150,8 @@ dlvm_status dlvm_vjp(const dlvm_model* m, const void* params, const void* x, con
 
 /* Plain SGD over the whole flat buffer in one launch: params -= lr * dparams.
  * F32 models update params in place and take master == NULL. BF16 models
- * update the float32 `master` copy and write params = bf16(master). */
+ * update the float32 `master` copy and write params = bf16(master). Dense and
+ * recurrent handles; DLVM_ERR_UNSUPPORTED for a matrix chain. */
 dlvm_status dlvm_sgd_step(const dlvm_model* m, void* params, float* master,
                           const float* dparams, float lr, void* stream);
 
@@ -282,7 +283,8 @@ void dlvm_graph_destroy(dlvm_graph* g);
  * DLVM_ERR_LABEL_RANGE if a label was outside [0, classes) (that row's loss
  * term is NaN), else DLVM_ERR_NONFINITE if the loss was NaN or infinite, else
  * DLVM_OK. The step-level loss calls write the same flags at the start of
- * their `ws`, so dlvm_check also reads those. */
+ * their `ws`, so dlvm_check also reads those. DLVM_ERR_UNSUPPORTED for a
+ * recurrent or matrix-chain handle (their calls write no flags). */
 dlvm_status dlvm_check(const dlvm_model* m, void* ws, void* stream);
 
 /* Message describing the last failure on this thread ("" if none). */

@@ -1067,6 +1067,7 @@ dlvm_status check_gradient_args(const dlvm_model* m, const void* params, const v
 dlvm_status check_sgd_args(const dlvm_model* m, void* params, float* master, const float* dparams) {
   if (m == nullptr || params == nullptr || dparams == nullptr)
     return fail(DLVM_ERR_INVALID_ARG, "null argument");
+  if (m->kind == 2) return fail(DLVM_ERR_UNSUPPORTED, "a matrix chain has no parameters to update");
   if (m->dtype == DLVM_BF16 && master == nullptr)
     return fail(DLVM_ERR_INVALID_ARG, "bf16 models need float32 master weights");
   if (!aligned16(params) || !aligned16(dparams) || (master && !aligned16(master)))
@@ -1262,6 +1263,7 @@ dlvm_status dlvm_probe_disarm(dlvm_model* m) {
 
 dlvm_status dlvm_check(const dlvm_model* m, void* ws, void* stream) {
   if (m == nullptr || ws == nullptr) return fail(DLVM_ERR_INVALID_ARG, "null argument");
+  if (m->kind != 0) return fail(DLVM_ERR_UNSUPPORTED, "only dense-network calls write device flags");
   hipStream_t s = static_cast<hipStream_t>(stream);
   int32_t flags[4] = {0, 0, 0, 0};
   hipError_t e = hipMemcpyAsync(flags, ws, 2 * sizeof(int32_t), hipMemcpyDeviceToHost, s);

@@ -299,3 +299,18 @@ def test_matrix_chain_errors_are_host_side():
     need = L.dlvm_matrix_chain_ws_bytes(0, n, dims, None)
     assert need >= 8 * 4 * 4 or need >= 16 * 8 * 4
     assert L.dlvm_matrix_chain(0, n, dims, mats, None, A, A, need - 1, None) == dl.ERR_WORKSPACE
+
+
+def test_handle_kinds_refuse_calls_that_do_not_apply():
+    L = dl.lib()
+    A = 0x100000
+    r = dl.Rnn(2, 8, 8, "tanh", "f32", False, False, 4)
+    c = dl.Chain("f32", [8, 4, 8])
+    assert L.dlvm_check(r._h, A, None) == dl.ERR_UNSUPPORTED
+    assert L.dlvm_check(c._h, A, None) == dl.ERR_UNSUPPORTED
+    assert L.dlvm_sgd_step(c._h, A, None, A, 0.1, None) == dl.ERR_UNSUPPORTED
+    assert L.dlvm_chain_run(r._h, (ctypes.c_void_p * 2)(A, A), A, A, 1 << 20, None) == dl.ERR_UNSUPPORTED
+    assert L.dlvm_rnn_backward(c._h, A, A, A, A, 1, A, None, None, A, 1 << 20, None) == dl.ERR_UNSUPPORTED
+    assert c.workspace_bytes(1) >= 16 and c.workspace_bytes(2) == 0
+    plan = c.plan(1)
+    assert [p["name"].split("_")[0] for p in plan[:-1]] == ["gemm"]
