@@ -547,7 +547,7 @@ def main():
               **({"checkpoint_every": args.checkpoint} if args.checkpoint > 1 else {})}
     out = result_line(wl, sps, elapsed, steps, warmup, roof, config,
                       launch="eager" if graph is None else "hip_graph",
-                      workspace_bytes=int(ws.numel()))
+                      workspace_bytes=int(ws.numel()), launch_groups_us=groups)
     del graph, P, master, xd, ws, dP, dx
     out["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
     print(json.dumps(out), flush=True)
