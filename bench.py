@@ -60,6 +60,9 @@ def parse():
                     help="keep only every K-th hidden layer output and recompute the rest in "
                          "the adjoint sweep (1: keep all); the rate still counts the "
                          "algorithmic flops only")
+    ap.add_argument("--chain-in-epilogue", action="store_true",
+                    help="c4: run the eight-operator chain in the dense product's epilogue "
+                         "instead of the standalone chain kernel")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (5 times) and exit: the "
                          "reference kernel for scaling the FETCH_SIZE / WRITE_SIZE counters")
@@ -514,7 +517,7 @@ def main():
     x, params, y = workloads.make_inputs(wl)
     B = wl.batch
     m = dl.Model(wl.widths, wl.acts, wl.dtype, wl.loss, wl.wrt_x, B,
-                 checkpoint_every=args.checkpoint)
+                 checkpoint_every=args.checkpoint, chain_in_epilogue=args.chain_in_epilogue)
     P = m.pack(params, dev, tdt)
     master = m.pack(params, dev, torch.float32) if wl.dtype == "bf16" and wl.sgd else None
     del params
@@ -544,7 +547,8 @@ def main():
                                          flags_ws=ws)
     config = {"workload": f"{wl.name}: {wl.title}", "global_batch": B,
               "widths": list(wl.widths), "loss": wl.loss, "parallelism": "none",
-              **({"checkpoint_every": args.checkpoint} if args.checkpoint > 1 else {})}
+              **({"checkpoint_every": args.checkpoint} if args.checkpoint > 1 else {}),
+              **({"chain": "in_epilogue"} if args.chain_in_epilogue and wl.loss == "chain8" else {})}
     out = result_line(wl, sps, elapsed, steps, warmup, roof, config,
                       launch="eager" if graph is None else "hip_graph",
                       workspace_bytes=int(ws.numel()), launch_groups_us=groups)

@@ -72,6 +72,10 @@ typedef struct dlvm_mlp_desc {
                              * recompute the others, one segment at a time, during the
                              * sweep (checkpointing, section 3.1.3). Results are bitwise
                              * the same for every k; the workspace shrinks. */
+  int32_t chain_in_epilogue; /* CHAIN8 only: 1 runs the eight-operator chain and its
+                              * adjoint in the epilogue of the dense layer's product (z is
+                              * never stored; zbar, xbar are bitwise those of the
+                              * standalone chain kernel); 0 runs the standalone kernel. */
 } dlvm_mlp_desc;
 
 typedef struct dlvm_model dlvm_model;

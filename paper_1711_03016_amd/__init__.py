@@ -41,6 +41,7 @@ class _Desc(ctypes.Structure):
         ("wrt_x", ctypes.c_int32),
         ("batch_max", ctypes.c_int64),
         ("checkpoint_every", ctypes.c_int32),
+        ("chain_in_epilogue", ctypes.c_int32),
     ]
 
 
@@ -166,7 +167,8 @@ class Model:
     """A handle on one shape-specialised network (see ``dlvm_create``)."""
 
     def __init__(self, widths, acts, dtype: str = "f32", loss: str = "softmax_ce",
-                 wrt_x: bool = False, batch_max: int = 1, checkpoint_every: int = 1):
+                 wrt_x: bool = False, batch_max: int = 1, checkpoint_every: int = 1,
+                 chain_in_epilogue: bool = False):
         self.widths = tuple(int(w) for w in widths)
         self.acts = tuple(acts)
         self.dtype = dtype
@@ -174,11 +176,12 @@ class Model:
         self.wrt_x = bool(wrt_x)
         self.batch_max = int(batch_max)
         self.checkpoint_every = int(checkpoint_every)
+        self.chain_in_epilogue = bool(chain_in_epilogue)
         L = len(self.widths) - 1
         self._w = (ctypes.c_int32 * (L + 1))(*self.widths)
         self._a = (ctypes.c_int32 * max(L, 1))(*[ACTS[a] for a in self.acts])
         desc = _Desc(L, self._w, self._a, DTYPES[dtype], LOSSES[loss], int(self.wrt_x),
-                     self.batch_max, self.checkpoint_every)
+                     self.batch_max, self.checkpoint_every, int(self.chain_in_epilogue))
         h = _P()
         _check(lib().dlvm_create(ctypes.byref(desc), ctypes.byref(h)))
         self._h = h

@@ -51,6 +51,7 @@ struct dlvm_model {
   int32_t wrt_x = 0;
   int64_t batch_max = 0;
   int32_t ckpt = 1;              // keep every ckpt-th hidden activation (1: all)
+  int32_t chain_epi = 0;         // CHAIN8: run the chain in the product's epilogue
   // Recurrent networks (kind 1): T steps of the cell
   // hs[t+1] = act(xs[t] . W + hs[t] . U + b); L = 1 and widths = {Kx + H, H},
   // the one "layer" being the stacked [W; U] and b.
@@ -133,8 +134,11 @@ WsLayout ws_layout(const dlvm_model* m, int64_t B) {
   size_t off = 0;
   w.flags = off;
   off = align_up(off + 16);
-  const int64_t np = std::max<int64_t>(dlvm::softmax_xent_partials(B),
-                                       dlvm::chain8_partials(B, m->widths[m->L]));
+  int64_t np = std::max<int64_t>(dlvm::softmax_xent_partials(B),
+                                 dlvm::chain8_partials(B, m->widths[m->L]));
+  // the chain epilogue writes one partial per wavefront; every register-staged
+  // configuration gives each wavefront at least a 32 x 32 block
+  if (m->chain_epi) np = std::max<int64_t>(np, (B + 31) / 32 * ((m->widths[m->L] + 31) / 32));
   w.partials = off;
   off = align_up(off + static_cast<size_t>(np) * 4);
   w.bad = off;
@@ -525,19 +529,38 @@ dlvm_status plan_gradient(const dlvm_model* m, const void* params, const void* x
     const int64_t N = m->widths[1], K = m->widths[0];
     float* z = at<float>(ws, w.logits);
     float* zbar = at<float>(ws, w.dz[0]);
-    if ((st = run.gemm(gemm_nn(dt, DLVM_F32, DLVM_ACT_NONE, batch, N, K, 1.0f, x, P(0), N, nullptr,
-                               z, N))) != DLVM_OK)
-      return st;
-    np = dlvm::chain8_partials(batch, N);
     scale = static_cast<float>(1.0 / (static_cast<double>(batch) * static_cast<double>(N)));
-    st = run.run(elementwise_info("chain8", batch, N, 16.0 * double(batch) * N + 4.0 * N),
-                 [&](hipStream_t s) {
-                   int n = 0;
-                   return dlvm::launch_chain8(batch, N, z, static_cast<const float*>(P(1)),
-                                              static_cast<const float*>(x), zbar, dx, partials,
-                                              false, &n, s);
-                 },
-                 "chain launch");
+    if (m->chain_epi) {
+      // The chain in the product's epilogue (z is never stored): zbar to the
+      // workspace, xbar into dx, one loss partial per wavefront.
+      GemmDesc d = gemm_nn(dt, DLVM_F32, DLVM_ACT_NONE, batch, N, K, 1.0f, x, P(0), N, P(1), zbar, N);
+      d.aux = x;
+      d.chain_epilogue = true;
+      d.C2 = dx;
+      d.partials = partials;
+      d.inv_n = scale;
+      const dlvm::GemmPlan pl = dlvm::plan_gemm(d);
+      np = static_cast<int>(dlvm::chain_partials(pl));
+      LaunchInfo info = gemm_info(d);
+      info.name = "gemm_nn_chain8_f32_" + std::to_string(pl.bm) + "x" + std::to_string(pl.bn) + "c" +
+                  std::to_string(pl.cfg);
+      info.bytes += 12.0 * double(batch) * double(N);  // x_skip read, zbar and xbar written
+      st = run.run(std::move(info), [&](hipStream_t s) { return dlvm::launch_gemm(d, pl, s); },
+                   "chain product launch");
+    } else {
+      if ((st = run.gemm(gemm_nn(dt, DLVM_F32, DLVM_ACT_NONE, batch, N, K, 1.0f, x, P(0), N,
+                                 nullptr, z, N))) != DLVM_OK)
+        return st;
+      np = dlvm::chain8_partials(batch, N);
+      st = run.run(elementwise_info("chain8", batch, N, 16.0 * double(batch) * N + 4.0 * N),
+                   [&](hipStream_t s) {
+                     int n = 0;
+                     return dlvm::launch_chain8(batch, N, z, static_cast<const float*>(P(1)),
+                                                static_cast<const float*>(x), zbar, dx, partials,
+                                                false, &n, s);
+                   },
+                   "chain launch");
+    }
     if (st != DLVM_OK) return st;
     GemmDesc dw = gemm_tn(dt, batch, N, K, x, zbar, N, G(0), N, G(1), N);
     dw.split_ws = at<float>(ws, w.splitk);
@@ -953,6 +976,7 @@ dlvm_status dlvm_create(const dlvm_mlp_desc* desc, dlvm_model** out) {
   m->wrt_x = desc->wrt_x ? 1 : 0;
   m->batch_max = desc->batch_max;
   m->ckpt = desc->checkpoint_every > 1 ? desc->checkpoint_every : 1;
+  m->chain_epi = desc->loss == DLVM_LOSS_CHAIN8 && desc->chain_in_epilogue ? 1 : 0;
   // The class dimension of a softmax network's last weight matrix is padded
   // to a multiple of 8 (zero columns), so every row is 16-byte aligned.
   for (int l = 0; l < L; ++l) {

@@ -77,4 +77,23 @@ __device__ __forceinline__ float act_grad_from_output(int act, float h) {
   }
 }
 
+// One element of the eight-operator chain and its adjoint: a = tanh(z + b),
+// s = sigmoid(0.5 a + 1), e = s x; returns e^2 (the loss term before the
+// mean); with the seed 1 / n of the mean, zbar = dL/dz and xbar = dL/dx (the
+// x_skip path), unless fwd_only.
+__device__ __forceinline__ float chain_elem(float z, float b, float x, float inv_n, bool fwd_only,
+                                            float& zbar, float& xbar, float& e_out) {
+  const float a = tanhf(z + b);
+  const float d = 0.5f * a + 1.0f;
+  const float s = sigmoidf_(d);
+  const float e = s * x;
+  e_out = e;
+  if (!fwd_only) {
+    const float eb = 2.0f * e * inv_n;
+    xbar = eb * s;
+    zbar = eb * x * (s * (1.0f - s)) * 0.5f * (1.0f - a * a);
+  }
+  return e * e;
+}
+
 }  // namespace dlvm

@@ -308,21 +308,6 @@ __global__ __launch_bounds__(kBlock) void dlvm_softmax_xent_rows_kernel(
 constexpr int kChainBlocks = 2048;
 constexpr int kChainUnroll = 4;
 
-__device__ __forceinline__ float chain_elem(float z, float b, float x, float inv_n, bool fwd_only,
-                                            float& zbar, float& xbar, float& e_out) {
-  const float a = tanhf(z + b);
-  const float d = 0.5f * a + 1.0f;
-  const float s = sigmoidf_(d);
-  const float e = s * x;
-  e_out = e;
-  if (!fwd_only) {
-    const float eb = 2.0f * e * inv_n;
-    xbar = eb * s;
-    zbar = eb * x * (s * (1.0f - s)) * 0.5f * (1.0f - a * a);
-  }
-  return e * e;
-}
-
 template <bool VEC, bool FWD_ONLY>
 __global__ __launch_bounds__(kBlock) void dlvm_chain8_kernel(
     int64_t rows, int64_t cols, const float* __restrict__ z, const float* __restrict__ bias,

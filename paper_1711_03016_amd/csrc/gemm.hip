@@ -212,6 +212,12 @@ GemmPlan choose(const GemmDesc& d, bool assume_aligned, int64_t capacity, int fo
 
 }  // namespace
 
+int64_t chain_partials(const GemmPlan& pl) {
+  // wavefronts of a tile (waves along M x N) of the register-staged configurations
+  const int waves = (pl.cfg == 3 || pl.cfg == 5) ? 1 : 4;
+  return static_cast<int64_t>(pl.tiles_m) * pl.tiles_n * waves;
+}
+
 GemmPlan plan_gemm(const GemmDesc& d) {
   return choose(d, false, d.split_ws != nullptr ? d.split_ws_elems : 0, forced_config(),
                 forced_splits());
@@ -262,6 +268,9 @@ gemm::Params make_params(const GemmDesc& d, const GemmPlan& pl) {
   p.lda2 = d.A2 != nullptr ? d.lda2 : 0;
   p.K1 = d.A2 != nullptr ? d.K1 : d.K;
   p.res_pre = d.res_pre ? 1 : 0;
+  p.C2 = d.chain_epilogue ? d.C2 : nullptr;
+  p.partials = d.chain_epilogue ? d.partials : nullptr;
+  p.inv_n = d.inv_n;
   if (pl.splits > 1) {
     p.C = d.split_ws;                  // partial products, then partial column sums
     p.c_split = d.M * d.ldc;

@@ -52,7 +52,7 @@ namespace gemm {
 constexpr int kRowStride = 144;  // bytes per LDS row: 128 bytes of k plus 16 of padding
 constexpr int kChunks = 8;       // 16-byte chunks of k per LDS row
 
-enum Epi { EPI_STORE = 0, EPI_DACT = 1, EPI_DW = 2 };
+enum Epi { EPI_STORE = 0, EPI_DACT = 1, EPI_DW = 2, EPI_CHAIN = 3 };
 
 template <typename T> struct Elem;
 template <> struct Elem<float> { static constexpr int VW = 4; static constexpr int BK = 32; };
@@ -85,6 +85,12 @@ struct Params {
   const void* A2;
   int64_t lda2, K1;
   int res_pre;  // EPI_DACT: (acc + R) * act'(Hprev) instead of acc * act'(Hprev) + R
+  // EPI_CHAIN (float32 NN): the eight-operator chain on z = acc with bias[n]
+  // and x_skip = aux (same shape as C): C receives zbar, C2 xbar, and each
+  // wavefront of tile t writes its sum of e^2 to partials[t * WM * WN + wave].
+  void* C2;
+  float* partials;
+  float inv_n;
 };
 
 // Source of pipeline stage kt (KSTAGE k per stage) of a two-phase
@@ -398,6 +404,32 @@ __device__ __forceinline__ void store_block(const Params& p, const f32x16& acc, 
   }
 }
 
+// The chain epilogue of one 32 x 32 accumulator block (EPI_CHAIN): per
+// element the standalone chain kernel's arithmetic (chain_elem), outputs
+// zbar and xbar; returns this lane's sum of e^2 over the block.
+__device__ __forceinline__ float chain_block(const Params& p, const f32x16& acc, int64_t r0,
+                                             int64_t c0, int lane) {
+  const int64_t col = c0 + (lane & 31);
+  const int64_t rb = r0 + 4 * (lane >> 5);
+  if (col >= p.N) return 0.0f;
+  const float b = static_cast<const float*>(p.bias)[col];
+  const float* __restrict__ xs = static_cast<const float*>(p.aux);
+  float* __restrict__ zb = static_cast<float*>(p.C);
+  float* __restrict__ xb = static_cast<float*>(p.C2);
+  float sq = 0.0f;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int64_t row = rb + 8 * (r >> 2) + (r & 3);
+    if (row >= p.M) continue;
+    const int64_t i = row * p.ldc + col;
+    float zo, xo, eo;
+    sq += chain_elem(acc[r], b, xs[i], p.inv_n, false, zo, xo, eo);
+    zb[i] = zo;
+    xb[i] = xo;
+  }
+  return sq;
+}
+
 // LDS bytes of one workgroup of the register-staged kernel.
 template <typename T, int BM, int BN, int WK, int KSEG>
 constexpr int gemm_smem_bytes() {
@@ -567,6 +599,20 @@ __device__ __forceinline__ void gemm_tile(Params& p, const int tile, char* smem)
   }
 
   // Epilogue.
+  if constexpr (EPI == EPI_CHAIN) {
+    // Each wavefront's e^2 sum (fixed-order butterfly) is one loss partial:
+    // no synchronisation between the wavefronts of the tile.
+    float sq = 0.0f;
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+        sq += chain_block(p, acc[i][j], m0 + wm * WTM + i * 32, n0 + wn * WTN + j * 32, lane);
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) sq += __shfl_xor(sq, o, 64);
+    if (lane == 0) p.partials[static_cast<int64_t>(tile) * (WM * WN) + wmn] = sq;
+    return;
+  }
 #pragma unroll
   for (int j = 0; j < TN; ++j)
 #pragma unroll

@@ -70,6 +70,14 @@ struct GemmDesc {
   // applies the product's epilogue. A two-phase product is split only at
   // slice boundaries that fall on K1.
   bool split_epilogue;
+  // NN float32 only: the eight-operator chain in the epilogue (z = the
+  // product; bias, x_skip = aux): C receives zbar, C2 xbar, and partials one
+  // loss term (sum of e^2) per wavefront of each tile (chain_partials of them);
+  // inv_n is the seed 1 / (M N) of the mean. Never split.
+  bool chain_epilogue;
+  void* C2;
+  float* partials;
+  float inv_n;
 };
 
 // How one product is launched: tile configuration and grid.
@@ -87,6 +95,9 @@ int64_t split_ws_elems(const GemmDesc& d);
 
 // Choose the launch of a product.
 GemmPlan plan_gemm(const GemmDesc& d);
+
+// Loss partials a chain-epilogue product writes (one per wavefront of a tile).
+int64_t chain_partials(const GemmPlan& plan);
 
 // Enqueue one GEMM with its fused epilogue as planned. Returns hipSuccess or
 // the launch error. The caller has validated shapes and pointers.

@@ -33,7 +33,7 @@ def _desc(widths, acts, dtype=0, loss=0, wrt_x=0, batch_max=8, ckpt=1):
     L = len(widths) - 1
     w = (ctypes.c_int32 * len(widths))(*widths)
     a = (ctypes.c_int32 * max(L, 1))(*acts)
-    return dl._Desc(L, w, a, dtype, loss, wrt_x, batch_max, ckpt), (w, a)
+    return dl._Desc(L, w, a, dtype, loss, wrt_x, batch_max, ckpt, 0), (w, a)
 
 
 @pytest.mark.parametrize("widths,acts,dtype,loss,wrt_x,batch_max,status", [

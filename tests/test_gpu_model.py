@@ -486,3 +486,53 @@ def test_vjp_rejects_chain_models():
     with pytest.raises(dl.DlvmError) as e:
         m.vjp(A, A, A, 8, A, A, ws)
     assert e.value.status == dl.ERR_UNSUPPORTED
+
+
+def _chain_run(wl, x, params, chain_in_epilogue, B):
+    import torch
+    dev = device()
+    m = dl.Model(wl.widths, wl.acts, wl.dtype, wl.loss, True, B,
+                 chain_in_epilogue=chain_in_epilogue)
+    P = m.pack(params, dev, torch.float32)
+    ws = torch.full((m.workspace_bytes(B),), 0xFF, dtype=torch.uint8, device=dev)
+    loss = torch.empty(1, device=dev)
+    dP = torch.full((m.param_count(),), float("nan"), device=dev)
+    dx = torch.full((B, wl.widths[0]), float("nan"), device=dev)
+    m.gradient(P, to_dev(x), None, B, loss, dP, dx, ws)
+    torch.cuda.synchronize()
+    assert m.check(ws) == dl.OK
+    return loss.item(), dP.cpu(), dx.cpu(), m
+
+
+@pytest.mark.parametrize("widths,batch,cfg", [((4096, 4096), 256, None), ((200, 200), 300, None),
+                                              ((200, 200), 300, 0), ((200, 200), 300, 1),
+                                              ((200, 200), 300, 2), ((200, 200), 300, 3),
+                                              ((200, 200), 300, 4), ((200, 200), 300, 5)])
+def test_chain_in_epilogue(widths, batch, cfg, monkeypatch):
+    """The eight-operator chain run in the dense product's epilogue (z never
+    stored) against the oracle and, bit for bit in dparams and dx, against the
+    standalone chain kernel (same element arithmetic; only the loss partials
+    are grouped differently). Every register-staged configuration forced."""
+    from dataclasses import replace
+    if cfg is not None:
+        monkeypatch.setenv("DLVM_GEMM_CONFIG", str(cfg))
+    wl = replace(workloads.WORKLOADS["c4"], widths=widths, batch=batch)
+    x, params, _ = workloads.make_inputs(wl, bias_scale=0.05)
+    l1, g1, d1, m = _chain_run(wl, x, params, True, batch)
+    l0, g0, d0, _ = _chain_run(wl, x, params, False, batch)
+    assert torch_equal(g1, g0) and torch_equal(d1, d0)
+    assert abs(l1 - l0) <= 1e-6 * abs(l0)
+    rl, rg, rdx = oracle.mlp_gradient(_spec(wl), x, params, None, wrt_x=True)
+    assert abs(l1 - rl) <= TOL["f32"] * abs(rl)
+    (gW, gb), = m.unpack(g1)
+    assert rel_l2(to_np(gW), rg[0][0]) <= TOL["f32"]
+    assert rel_l2(to_np(gb), rg[0][1]) <= TOL["f32"]
+    assert rel_l2(to_np(d1), rdx) <= TOL["f32"]
+    names = [p["name"] for p in m.plan(batch)]
+    assert any(n.startswith("gemm_nn_chain8") for n in names)
+    assert "chain8" not in names
+
+
+def torch_equal(a, b):
+    import torch
+    return bool(torch.equal(a, b))
