@@ -18,7 +18,7 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libdlvm.so")
 SOURCES = ["gemm.hip", "gemm_nn.hip", "gemm_nt.hip", "gemm_tn.hip", "gemm_pair.hip",
-           "elementwise.hip", "api.cpp"]
+           "elementwise.hip", "small_step.hip", "api.cpp"]
 
 HIPCC = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
 ARCH = "gfx950"

@@ -13,6 +13,7 @@
 #include <algorithm>
 #include <climits>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <new>
 #include <string>
@@ -300,7 +301,12 @@ LaunchInfo elementwise_info(const char* name, int64_t rows, int64_t cols, double
 class Launcher {
  public:
   Launcher(const dlvm_model* m, hipStream_t s, std::vector<LaunchInfo>* plan, int32_t first)
-      : m_(m), main_(s), plan_(plan), index_(first) {}
+      : m_(m), main_(s), plan_(plan), index_(first) {
+    dlvm::tuning_scope_begin();
+  }
+  ~Launcher() { dlvm::tuning_scope_end(); }
+  Launcher(const Launcher&) = delete;
+  Launcher& operator=(const Launcher&) = delete;
 
   template <class F>
   dlvm_status run(LaunchInfo info, F&& launch, const char* what) {
@@ -499,6 +505,13 @@ dlvm_status plan_adjoint_layers(const dlvm_model* m, const void* params, const v
 
 // The launches of one gradient call (section 3.1.3): forward keeping every
 // layer output, the loss adjoint, then the adjoint of each layer, last first.
+// The one-workgroup gradient of small networks is used unless DLVM_SMALL_STEP=0
+// (for tests that compare it with the general plan).
+bool small_step_allowed() {
+  const char* v = std::getenv("DLVM_SMALL_STEP");
+  return v == nullptr || std::strcmp(v, "0") != 0;
+}
+
 dlvm_status plan_gradient(const dlvm_model* m, const void* params, const void* x,
                           const int32_t* labels, int64_t batch, float* loss, float* dparams,
                           float* dx, void* ws, Launcher& run) {
@@ -570,6 +583,32 @@ dlvm_status plan_gradient(const dlvm_model* m, const void* params, const void* x
                                  nullptr, dx, dx);
     if ((st = run.gemm_pair(dw, dxd)) != DLVM_OK) return st;
     return finalize();
+  }
+
+  // A small float32 network: the whole gradient in one workgroup (one launch).
+  dlvm::SmallNet sn{};
+  if (small_step_allowed() && m->dtype == DLVM_F32 &&
+      dlvm::small_net(L, m->widths.data(), m->acts.data(), m->offsets.data(), m->ldw.data(),
+                      batch, m->wrt_x != 0, sn)) {
+    double flops = 0.0, bytes = 0.0;
+    for (int l = 0; l < L; ++l) {
+      const double k = m->widths[l], n = m->widths[l + 1];
+      flops += 2.0 * batch * k * n * ((l > 0 || m->wrt_x) ? 3.0 : 2.0);
+      bytes += 8.0 * (k * n + n);  // parameters read, their gradient written
+    }
+    bytes += 4.0 * batch * (m->widths[0] + (m->wrt_x ? m->widths[0] : 0) + 1);
+    LaunchInfo info;
+    info.name = "small_step_f32";
+    info.M = batch; info.N = m->widths[L]; info.K = m->widths[0];
+    info.flops = flops;
+    info.bytes = bytes;
+    return run.run(std::move(info),
+                   [&](hipStream_t s) {
+                     return dlvm::launch_small_step(sn, static_cast<const float*>(params),
+                                                    static_cast<const float*>(x), labels, loss,
+                                                    dparams, dx, flags, m->gaps, s);
+                   },
+                   "small-network gradient launch");
   }
 
   // Forward, keeping the layer outputs (every one, or the checkpoints and the

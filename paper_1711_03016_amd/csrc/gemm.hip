@@ -135,11 +135,35 @@ int env_int(const char* name) {
   const long c = std::strtol(v, &end, 10);
   return (end != nullptr && *end == 0) ? static_cast<int>(c) : -1;
 }
-int forced_config() { return env_int("DLVM_GEMM_CONFIG"); }
+// Inside a tuning scope (one library call) the two variables are read once,
+// at its start, not once per product.
+thread_local int t_depth = 0;
+thread_local bool t_loaded = false;
+thread_local int t_config = -1, t_splits = -1;
+
+void load_tuning() {
+  if (t_depth > 0 && t_loaded) return;
+  t_config = env_int("DLVM_GEMM_CONFIG");
+  t_splits = env_int("DLVM_GEMM_SPLITS");
+  t_loaded = t_depth > 0;
+}
+
+int forced_config() {
+  load_tuning();
+  return t_config;
+}
 
 // Number of k-slices forced through DLVM_GEMM_SPLITS (for tests and tuning)
 // on products the caller lets split with their epilogue, or -1.
-int forced_splits() { return env_int("DLVM_GEMM_SPLITS"); }
+int forced_splits() {
+  load_tuning();
+  return t_splits;
+}
+
+void tuning_scope_begin() {
+  if (t_depth++ == 0) t_loaded = false;
+}
+void tuning_scope_end() { --t_depth; }
 
 namespace {
 

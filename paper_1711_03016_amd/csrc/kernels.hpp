@@ -96,6 +96,11 @@ int64_t split_ws_elems(const GemmDesc& d);
 // Choose the launch of a product.
 GemmPlan plan_gemm(const GemmDesc& d);
 
+// Between begin and end (nestable; one library call), the tuning variables
+// DLVM_GEMM_CONFIG / DLVM_GEMM_SPLITS are read once instead of per product.
+void tuning_scope_begin();
+void tuning_scope_end();
+
 // Loss partials a chain-epilogue product writes (one per wavefront of a tile).
 int64_t chain_partials(const GemmPlan& plan);
 
@@ -166,6 +171,42 @@ hipError_t launch_split_epilogue(int dtype, int out_dtype, int mode, int splits,
                                  int act, float alpha, const void* bias, int64_t nvec,
                                  const void* aux, const void* res, bool res_pre, void* out,
                                  hipStream_t s);
+
+// A small float32 softmax network whose whole gradient runs in one workgroup
+// (its input, weights and activations in LDS): see small_step.hip.
+constexpr int kSmallMaxLayers = 8;
+constexpr int kSmallThreads = 1024;
+constexpr int kSmallMaxLds = 64 * 1024;                   // bytes of LDS for everything
+constexpr int kSmallStageRegs = kSmallMaxLds / 4 / kSmallThreads;  // staged words per thread
+constexpr int64_t kSmallMaxMacs = int64_t(1) << 21;       // forward + both adjoints
+constexpr int kSmallMaxSegs = 2 * kSmallMaxLayers + 2;
+// One block of words copied from global memory into LDS at the start: `rows`
+// rows of `cols` words, global row stride `gstride` from source `src` (0 x,
+// 1 params, 2 labels) at word offset `goff`, LDS row stride `lstride` at LDS
+// word offset `lds`; `start` is the block's first index in the flat copy.
+struct SmallSeg {
+  int64_t goff;
+  int gstride, cols, lds, lstride, start, src;
+};
+struct SmallNet {
+  int L, B, maxw, wrt_x, nseg, nstage;
+  int w[kSmallMaxLayers + 1];
+  int act[kSmallMaxLayers];
+  int hoff[kSmallMaxLayers + 1];  // LDS word offsets of the layer outputs H_0 (= x) .. H_L
+  int woff[kSmallMaxLayers], sw[kSmallMaxLayers], boff[kSmallMaxLayers];  // W_l, its row stride, b_l
+  int g0, g1, rowloss, rowbad, labels;  // adjoint ping-pong, per-row loss and label marks, labels
+  int64_t offW[kSmallMaxLayers], offB[kSmallMaxLayers], ldw[kSmallMaxLayers];  // in dparams
+  SmallSeg seg[kSmallMaxSegs];
+  float scale;                    // 1 / B
+};
+// Fill t for a network; false if it does not fit one workgroup (layers,
+// batch, LDS) or has too much work for one compute unit.
+bool small_net(int L, const int32_t* widths, const int32_t* acts, const int64_t* offsets,
+               const int64_t* ldw, int64_t B, bool wrt_x, SmallNet& t);
+// The whole gradient (loss, dparams with zero padding, dx if t.wrt_x, flags).
+hipError_t launch_small_step(const SmallNet& t, const float* params, const float* x,
+                             const int32_t* labels, float* loss, float* dparams, float* dx,
+                             int32_t* flags, const ZeroGaps& gaps, hipStream_t s);
 
 // out[i] = g[i] * act'(h[i]) for i < n, act' from the saved output h = act(z)
 // (storage dtype `dtype` for all three).

@@ -93,6 +93,10 @@ def test_layout_and_plan(name):
     # dead-code elimination: no input-gradient product for layer 1 unless x is
     # differentiated (a paired launch holds one product wrt the weights and one
     # wrt the input)
+    if plan[0]["name"].startswith("small_step"):
+        # a small float32 network: the whole gradient is one launch
+        assert wl.dtype == "f32" and len(plan) == 2
+        return
     pair = [p for p in plan if p["name"].startswith("gemm_pair")]
     nt = [p for p in plan if p["name"].startswith("gemm_nt")]
     tn = [p for p in plan if p["name"].startswith("gemm_tn")]
@@ -314,3 +318,17 @@ def test_handle_kinds_refuse_calls_that_do_not_apply():
     assert c.workspace_bytes(1) >= 16 and c.workspace_bytes(2) == 0
     plan = c.plan(1)
     assert [p["name"].split("_")[0] for p in plan[:-1]] == ["gemm"]
+
+
+def test_small_network_plan(monkeypatch):
+    """Small float32 softmax networks take the one-workgroup gradient; larger
+    ones, bf16 ones and the chain keep the general plan; DLVM_SMALL_STEP=0
+    turns it off."""
+    small = dl.Model((64, 32, 10), ("sigmoid", "none"), batch_max=16)
+    assert [p["name"] for p in small.plan(16)] == ["small_step_f32", "sgd_f32"]
+    assert not dl.Model((784, 512, 512, 10), ("tanh", "tanh", "none"), batch_max=256) \
+        .plan(256)[0]["name"].startswith("small")
+    assert not dl.Model((64, 32, 10), ("sigmoid", "none"), "bf16", batch_max=16) \
+        .plan(16)[0]["name"].startswith("small")
+    monkeypatch.setenv("DLVM_SMALL_STEP", "0")
+    assert small.plan(16)[0]["name"].startswith("gemm_nn")

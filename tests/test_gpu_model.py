@@ -536,3 +536,62 @@ def test_chain_in_epilogue(widths, batch, cfg, monkeypatch):
 def torch_equal(a, b):
     import torch
     return bool(torch.equal(a, b))
+
+
+
+@pytest.mark.parametrize("widths,acts,batch,wrt_x", [
+    ((64, 32, 10), ("sigmoid", "none"), 16, False),             # c1
+    ((64, 32, 10), ("sigmoid", "none"), 16, True),
+    ((37, 50, 23, 10), ("relu", "tanh", "none"), 7, True),      # ragged widths and batch
+    ((96, 48, 48, 40, 30), ("tanh", "relu", "sigmoid", "none"), 9, False),
+    ((20, 300), ("none",), 5, True),                             # one layer, wide head
+])
+def test_small_network_path(widths, acts, batch, wrt_x, monkeypatch):
+    """The one-workgroup gradient of a small float32 network against the
+    oracle and against the general multi-launch plan (DLVM_SMALL_STEP=0)."""
+    from dataclasses import replace
+    wl = replace(workloads.WORKLOADS["c1"], widths=widths, acts=acts, batch=batch, wrt_x=wrt_x)
+    x, params, y = workloads.make_inputs(wl, bias_scale=0.1)
+    m = dl.Model(wl.widths, wl.acts, wl.dtype, wl.loss, wrt_x, batch)
+    assert m.plan(batch)[0]["name"] == "small_step_f32"
+    got = _run(wl, x, params, y, wrt_x=wrt_x, forward=False)
+    rl, rg, rdx = oracle.mlp_gradient(_spec(wl), x, params, y, wrt_x=wrt_x)
+    _compare(wl, got, rl, rg, rdx if wrt_x else None)
+    again = _run(wl, x, params, y, wrt_x=wrt_x, forward=False)   # fixed summation order
+    assert again["loss"] == got["loss"]
+    assert bool((again["dparams"] == got["dparams"]).all())
+    monkeypatch.setenv("DLVM_SMALL_STEP", "0")
+    gen = _run(wl, x, params, y, wrt_x=wrt_x, forward=False)
+    assert abs(got["loss"] - gen["loss"]) <= 1e-5 * abs(gen["loss"])
+    for (a, b), (c, d) in zip(got["grads"], gen["grads"]):
+        assert rel_l2(a, c) <= 1e-5 and rel_l2(b, d) <= 1e-5
+    # the padding of dparams is zero on both paths
+    import torch
+    dP = got["dparams"]
+    offs, lds = m.param_layout_lds()
+    used = torch.zeros(m.param_count(), dtype=torch.bool, device=dP.device)
+    for l in range(m.n_layers):
+        used[offs[2 * l]:offs[2 * l] + widths[l] * lds[l]] = True
+        used[offs[2 * l + 1]:offs[2 * l + 1] + widths[l + 1]] = True
+    assert torch.count_nonzero(dP[~used]).item() == 0
+
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("cfg", [0, 1, 2, 3, 4, 5])
+def test_register_staged_configurations(dtype, cfg, monkeypatch):
+    """Every register-staged tile configuration forced on a ragged network:
+    forward (NN), adjoint wrt the input (NT) and wrt the weights (TN, paired
+    with NT where the configuration allows), against the oracle. The
+    contraction lengths 520, 300, 150 and 72 give odd, even and single stage
+    counts (128 k per stage in float32, 256 in bf16 for the 4-segment tiles)."""
+    from dataclasses import replace
+    monkeypatch.setenv("DLVM_GEMM_CONFIG", str(cfg))
+    base = workloads.WORKLOADS["c2" if dtype == "f32" else "c3"]
+    wl = replace(base, widths=(520, 150, 72, 10), acts=("tanh", "relu", "none"), batch=300,
+                 wrt_x=True)
+    x, params, y = workloads.make_inputs(wl, bias_scale=0.1)
+    got = _run(wl, x, params, y, wrt_x=True)
+    rl, rg, rdx = oracle.mlp_gradient(_spec(wl), x, params, y, wrt_x=True)
+    _, ref_out = oracle.mlp_forward(_spec(wl), x, params, y)
+    _compare(wl, got, rl, rg, rdx, ref_out=ref_out)
