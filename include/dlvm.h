@@ -133,7 +133,12 @@ dlvm_status dlvm_forward(const dlvm_model* m, const void* params, const void* x,
  * (float32, flat layout, padding set to zero) and, iff wrt_x, dx (float32
  * [batch, widths[0]]). `labels` are int32 [batch] in [0, classes) for
  * SOFTMAX_CE and NULL for CHAIN8. The input gradient of the first layer is
- * not computed unless wrt_x (dead code elimination, section 3.1.3). */
+ * not computed unless wrt_x (dead code elimination, section 3.1.3).
+ * A float32 SOFTMAX_CE network of at most 8 layers and 1024 rows whose
+ * input, weights and layer outputs fit in 64 KB (and at most 2^21
+ * multiply-adds a call) runs as one launch of one workgroup, which writes
+ * only the error flags of the workspace; setting the environment variable DLVM_SMALL_STEP=0
+ * selects the multi-launch plan for it as well. */
 dlvm_status dlvm_gradient(const dlvm_model* m, const void* params, const void* x,
                           const int32_t* labels, int64_t batch, float* loss,
                           float* dparams, float* dx, void* ws, size_t ws_bytes,
