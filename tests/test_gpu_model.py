@@ -579,16 +579,19 @@ def test_small_network_path(widths, acts, batch, wrt_x, monkeypatch):
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("cfg", [0, 1, 2, 3, 4, 5])
-def test_register_staged_configurations(dtype, cfg, monkeypatch):
+@pytest.mark.parametrize("batch", [300, 7])
+def test_forced_tile_configurations(dtype, cfg, batch, monkeypatch):
     """Every register-staged tile configuration forced on a ragged network:
     forward (NN), adjoint wrt the input (NT) and wrt the weights (TN, paired
     with NT where the configuration allows), against the oracle. The
-    contraction lengths 520, 300, 150 and 72 give odd, even and single stage
-    counts (128 k per stage in float32, 256 in bf16 for the 4-segment tiles)."""
+    contraction lengths 520, 300, 150, 72 and 10 give odd, even and single
+    stage counts (128 k per stage in float32, 256 in bf16 for the 4-segment
+    tiles) and K not a multiple of the vector width (150, 10, and a batch of 7
+    for the products wrt the weights), where the loads go element by element."""
     from dataclasses import replace
     monkeypatch.setenv("DLVM_GEMM_CONFIG", str(cfg))
     base = workloads.WORKLOADS["c2" if dtype == "f32" else "c3"]
-    wl = replace(base, widths=(520, 150, 72, 10), acts=("tanh", "relu", "none"), batch=300,
+    wl = replace(base, widths=(520, 150, 72, 10), acts=("tanh", "relu", "none"), batch=batch,
                  wrt_x=True)
     x, params, y = workloads.make_inputs(wl, bias_scale=0.1)
     got = _run(wl, x, params, y, wrt_x=True)
