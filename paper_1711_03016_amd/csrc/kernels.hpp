@@ -177,27 +177,23 @@ hipError_t launch_split_epilogue(int dtype, int out_dtype, int mode, int splits,
 constexpr int kSmallMaxLayers = 8;
 constexpr int kSmallThreads = 1024;
 constexpr int kSmallMaxLds = 64 * 1024;                   // bytes of LDS for everything
-constexpr int kSmallStageRegs = kSmallMaxLds / 4 / kSmallThreads;  // staged words per thread
 constexpr int64_t kSmallMaxMacs = int64_t(1) << 21;       // forward + both adjoints
-constexpr int kSmallMaxSegs = 2 * kSmallMaxLayers + 2;
-// One block of words copied from global memory into LDS at the start: `rows`
-// rows of `cols` words, global row stride `gstride` from source `src` (0 x,
-// 1 params, 2 labels) at word offset `goff`, LDS row stride `lstride` at LDS
-// word offset `lds`; `start` is the block's first index in the flat copy.
-struct SmallSeg {
-  int64_t goff;
-  int gstride, cols, lds, lstride, start, src;
-};
 struct SmallNet {
-  int L, B, maxw, wrt_x, nseg, nstage;
+  int L, B, maxw, wrt_x;
   int w[kSmallMaxLayers + 1];
   int act[kSmallMaxLayers];
-  int hoff[kSmallMaxLayers + 1];  // LDS word offsets of the layer outputs H_0 (= x) .. H_L
-  int woff[kSmallMaxLayers], sw[kSmallMaxLayers], boff[kSmallMaxLayers];  // W_l, its row stride, b_l
-  int g0, g1, rowloss, rowbad, labels;  // adjoint ping-pong, per-row loss and label marks, labels
-  int64_t offW[kSmallMaxLayers], offB[kSmallMaxLayers], ldw[kSmallMaxLayers];  // in dparams
-  SmallSeg seg[kSmallMaxSegs];
-  float scale;                    // 1 / B
+  // LDS word offsets: the parameter block (params[pbase, pbase + pwords) as
+  // it lies in memory, so W_l at woff[l] with row stride ldw[l] and b_l at
+  // boff[l]), the layer outputs H_0 (= x) .. H_L, the adjoint ping-pong, the
+  // per-row loss and label marks, the labels
+  int woff[kSmallMaxLayers], boff[kSmallMaxLayers];
+  int hoff[kSmallMaxLayers + 1];
+  int g0, g1, rowloss, rowbad, labels;
+  int64_t pbase;
+  int pwords;
+  int64_t offW[kSmallMaxLayers], offB[kSmallMaxLayers];  // in dparams
+  int ldw[kSmallMaxLayers];
+  float scale;  // 1 / B
 };
 // Fill t for a network; false if it does not fit one workgroup (layers,
 // batch, LDS) or has too much work for one compute unit.

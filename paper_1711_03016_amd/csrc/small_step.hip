@@ -4,8 +4,10 @@
 // compute unit's LDS and the products are tiny (the 64-32-10 network at batch
 // 16 does 81K multiply-adds a step), a launch costs more than the work: the
 // usual plan's launches are host-bound. Here one workgroup of 1024 threads
-//   stages    x, the labels, every W_l and b_l into LDS, all loads issued
-//             before the first store so that HBM latency is paid once;
+//   stages    the parameter block (every W_l and b_l, as it lies in memory),
+//             x and the labels into LDS with plain contiguous copies (16-byte
+//             loads where whole), all loads issued before the first store so
+//             that HBM latency is paid once;
 //   forward   H_{l+1} = act_l(H_l . W_l + b_l), the last layer giving logits;
 //   loss      softmax cross-entropy, one wave per row, and the adjoint of the
 //             logits (p - onehot) / B;
@@ -14,15 +16,17 @@
 //             differentiated; the first layer's input adjoint is otherwise dead);
 //   finalise  the mean loss, the device flags, the padding of dparams zeroed;
 // with workgroup barriers between the phases and nothing but the results
-// written to global memory. Every sum runs in a fixed order (one thread per
-// output with k in order, or a fixed butterfly across a wave), so the result
-// is the same on every run. Products are plain float32 fused multiply-adds:
-// at these sizes the matrix cores would not be fed.
+// written to global memory. A phase with fewer outputs than threads gives each
+// output a group of T adjacent lanes (T the largest power of two, at most 16,
+// with T x outputs <= 1024): lane q of the group sums the terms q, q + T, ...
+// and a butterfly over the group adds the T partial sums. Every sum thus runs
+// in a fixed order, so the result is the same on every run. Products are
+// plain float32 fused multiply-adds: at these sizes the matrix cores would
+// not be fed.
 //
-// LDS layout (words): H_0 .. H_L as [B][w_l]; two adjoint buffers [B][maxw];
-// row losses, row label marks and labels [B] each; W_l as [w_l][sw_l] with an
-// odd row stride sw_l >= w_{l+1} (the transposed read of the input adjoint
-// walks down a column: an odd stride keeps its lanes on distinct banks); b_l.
+// LDS layout (words): the parameter block (W_l as [w_l][ldw_l], b_l, the
+// padding between them); H_0 .. H_L as [B][w_l]; two adjoint buffers
+// [B][maxw]; row losses, row label marks and labels [B] each.
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -30,6 +34,7 @@ namespace dlvm {
 namespace {
 
 constexpr int kWaves = kSmallThreads / 64;
+constexpr int kStage4 = kSmallMaxLds / 16 / kSmallThreads;  // 16-byte loads per thread and block
 
 __device__ __forceinline__ float wave_sum(float v) {
   // butterfly: every lane ends with the same bits
@@ -47,58 +52,74 @@ __device__ __forceinline__ int wave_or(int v) {
   return v;
 }
 
+// Lanes per output for a phase of `outputs` sums (uniform over the workgroup).
+__device__ __forceinline__ int group_lanes(int outputs) {
+  int t = 1;
+  while (t < 16 && 2 * t * outputs <= kSmallThreads) t *= 2;
+  return t;
+}
+
+// Sum of v over the T adjacent lanes of a group (T a power of two <= 16;
+// every lane of the group active).
+__device__ __forceinline__ float group_sum(float v, int T) {
+  for (int o = T >> 1; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
 __global__ __launch_bounds__(kSmallThreads) void dlvm_small_step_kernel(
     SmallNet t, const float* __restrict__ params, const float* __restrict__ x,
     const int32_t* __restrict__ labels, float* __restrict__ loss, float* __restrict__ dparams,
     float* __restrict__ dx, int32_t* __restrict__ flags, ZeroGaps gaps) {
-  __shared__ float sm[kSmallMaxLds / 4];
+  __shared__ __attribute__((aligned(16))) float sm[kSmallMaxLds / 4];
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int B = t.B;
 
-  // stage x, labels, weights and biases
+  // stage the parameter block, x and the labels (16-byte body, word tail)
   {
-    uint32_t v[kSmallStageRegs];
-    int dst[kSmallStageRegs];
+    const float* pb = params + t.pbase;
+    const int np4 = t.pwords / 4, nx = B * t.w[0], nx4 = nx / 4;
+    float4 pv[kStage4], xv[kStage4];
 #pragma unroll
-    for (int j = 0; j < kSmallStageRegs; ++j) {
+    for (int j = 0; j < kStage4; ++j) {
       const int e = tid + j * kSmallThreads;
-      dst[j] = -1;
-      v[j] = 0;
-      if (e < t.nstage) {
-        int s = 0;
-        while (s + 1 < t.nseg && t.seg[s + 1].start <= e) ++s;
-        const SmallSeg& g = t.seg[s];
-        const int q = e - g.start;
-        const int r = q / g.cols, c = q - r * g.cols;
-        const uint32_t* src = g.src == 0   ? reinterpret_cast<const uint32_t*>(x)
-                              : g.src == 1 ? reinterpret_cast<const uint32_t*>(params)
-                                           : reinterpret_cast<const uint32_t*>(labels);
-        v[j] = src[g.goff + static_cast<int64_t>(r) * g.gstride + c];
-        dst[j] = g.lds + r * g.lstride + c;
-      }
+      if (e < np4) pv[j] = reinterpret_cast<const float4*>(pb)[e];
+      if (e < nx4) xv[j] = reinterpret_cast<const float4*>(x)[e];
     }
-    uint32_t* smu = reinterpret_cast<uint32_t*>(sm);
+    const int pt = np4 * 4 + tid, xt = nx4 * 4 + tid;
+    const float ptail = pt < t.pwords ? pb[pt] : 0.0f;
+    const float xtail = xt < nx ? x[xt] : 0.0f;
+    const int lab = tid < B ? labels[tid] : 0;
+    float* xs = sm + t.hoff[0];
 #pragma unroll
-    for (int j = 0; j < kSmallStageRegs; ++j)
-      if (dst[j] >= 0) smu[dst[j]] = v[j];
+    for (int j = 0; j < kStage4; ++j) {
+      const int e = tid + j * kSmallThreads;
+      if (e < np4) reinterpret_cast<float4*>(sm)[e] = pv[j];
+      if (e < nx4) reinterpret_cast<float4*>(xs)[e] = xv[j];
+    }
+    if (pt < t.pwords) sm[pt] = ptail;
+    if (xt < nx) xs[xt] = xtail;
+    if (tid < B) reinterpret_cast<int*>(sm + t.labels)[tid] = lab;
   }
   __syncthreads();
 
   // forward
   for (int l = 0; l < t.L; ++l) {
-    const int K = t.w[l], N = t.w[l + 1], sw = t.sw[l], act = t.act[l];
+    const int K = t.w[l], N = t.w[l + 1], sw = t.ldw[l], act = t.act[l];
     const float* h = sm + t.hoff[l];
     const float* W = sm + t.woff[l];
     const float* bias = sm + t.boff[l];
     float* o = sm + t.hoff[l + 1];
     const bool last = l == t.L - 1;
-    for (int i = tid; i < B * N; i += kSmallThreads) {
+    const int T = group_lanes(B * N), q = tid & (T - 1);
+    for (int i = tid / T; i < B * N; i += kSmallThreads / T) {
       const int r = i / N, n = i - r * N;
       const float* hr = h + r * K;
-      float acc = bias[n];
-      for (int k = 0; k < K; ++k) acc = fmaf(hr[k], W[k * sw + n], acc);
-      o[i] = last ? acc : apply_act(act, acc);
+      float acc = 0.0f;
+#pragma unroll 4
+      for (int k = q; k < K; k += T) acc = fmaf(hr[k], W[k * sw + n], acc);
+      acc = group_sum(acc, T) + bias[n];
+      if (q == 0) o[i] = last ? acc : apply_act(act, acc);
     }
     __syncthreads();
   }
@@ -151,36 +172,50 @@ __global__ __launch_bounds__(kSmallThreads) void dlvm_small_step_kernel(
 
   // adjoint, last layer first
   for (int l = t.L - 1; l >= 0; --l) {
-    const int K = t.w[l], N = t.w[l + 1], sw = t.sw[l];
-    const int ld = static_cast<int>(t.ldw[l]);
+    const int K = t.w[l], N = t.w[l + 1], ld = t.ldw[l];
     const float* W = sm + t.woff[l];
     const float* h = sm + t.hoff[l];
     float* dW = dparams + t.offW[l];
     float* db = dparams + t.offB[l];
     // dW [K, ld] (padding columns zero) and db [N]
-    for (int i = tid; i < K * ld; i += kSmallThreads) {
-      const int k = i / ld, n = i - k * ld;
-      float acc = 0.0f;
-      if (n < N)
-        for (int r = 0; r < B; ++r) acc = fmaf(h[r * K + k], g[r * N + n], acc);
-      dW[i] = acc;
+    {
+      const int T = group_lanes(K * ld), q = tid & (T - 1);
+      for (int i = tid / T; i < K * ld; i += kSmallThreads / T) {
+        const int k = i / ld, n = i - k * ld;
+        float acc = 0.0f;
+        if (n < N) {
+#pragma unroll 4
+          for (int r = q; r < B; r += T) acc = fmaf(h[r * K + k], g[r * N + n], acc);
+        }
+        acc = group_sum(acc, T);
+        if (q == 0) dW[i] = acc;
+      }
     }
-    for (int n = tid; n < N; n += kSmallThreads) {
-      float acc = 0.0f;
-      for (int r = 0; r < B; ++r) acc += g[r * N + n];
-      db[n] = acc;
+    {
+      const int T = group_lanes(N), q = tid & (T - 1);
+      for (int n = tid / T; n < N; n += kSmallThreads / T) {
+        float acc = 0.0f;
+        for (int r = q; r < B; r += T) acc += g[r * N + n];
+        acc = group_sum(acc, T);
+        if (q == 0) db[n] = acc;
+      }
     }
     if (l > 0 || t.wrt_x) {
-      for (int i = tid; i < B * K; i += kSmallThreads) {
+      const int T = group_lanes(B * K), q = tid & (T - 1);
+      for (int i = tid / T; i < B * K; i += kSmallThreads / T) {
         const int r = i / K, k = i - r * K;
         const float* gr = g + r * N;
-        const float* wr = W + k * sw;
+        const float* wr = W + k * ld;
         float acc = 0.0f;
-        for (int n = 0; n < N; ++n) acc = fmaf(gr[n], wr[n], acc);
-        if (l > 0)
-          gn[i] = acc * act_grad_from_output(t.act[l - 1], h[i]);
-        else
-          dx[i] = acc;
+#pragma unroll 4
+        for (int n = q; n < N; n += T) acc = fmaf(gr[n], wr[n], acc);
+        acc = group_sum(acc, T);
+        if (q == 0) {
+          if (l > 0)
+            gn[i] = acc * act_grad_from_output(t.act[l - 1], h[i]);
+          else
+            dx[i] = acc;
+        }
       }
     }
     __syncthreads();
@@ -207,25 +242,29 @@ bool small_net(int L, const int32_t* widths, const int32_t* acts, const int64_t*
     t.w[l] = widths[l];
     t.maxw = widths[l] > t.maxw ? widths[l] : t.maxw;
   }
-  // LDS layout, in words, checked against the budget before any narrowing
+  // LDS layout, in words, checked against the budget before any narrowing;
+  // blocks start on 4-word (16-byte) boundaries
+  const int64_t pbase = offsets[0];
+  const int64_t pwords = offsets[2 * L - 1] + widths[L] - pbase;
   int64_t words = 0;
   auto take = [&](int64_t n) {
     const int64_t o = words;
-    words += n;
+    words += (n + 3) / 4 * 4;
     return o;
   };
-  int64_t hoff[kSmallMaxLayers + 1], woff[kSmallMaxLayers], boff[kSmallMaxLayers];
+  take(pwords);
+  int64_t hoff[kSmallMaxLayers + 1];
   for (int l = 0; l <= L; ++l) hoff[l] = take(B * widths[l]);
   const int64_t g0 = take(B * t.maxw), g1 = take(B * t.maxw);
   const int64_t rl = take(B), rb = take(B), lb = take(B);
   int64_t macs = 0;
   for (int l = 0; l < L; ++l) {
-    t.sw[l] = widths[l + 1] | 1;
-    woff[l] = take(int64_t(widths[l]) * t.sw[l]);
-    boff[l] = take(widths[l + 1]);
+    if (ldw[l] > 4096) return false;
     macs += 3 * B * int64_t(widths[l]) * widths[l + 1];
   }
   if (words > kSmallMaxLds / 4 || macs > kSmallMaxMacs) return false;
+  t.pbase = pbase;
+  t.pwords = static_cast<int>(pwords);
   for (int l = 0; l <= L; ++l) t.hoff[l] = static_cast<int>(hoff[l]);
   t.g0 = static_cast<int>(g0);
   t.g1 = static_cast<int>(g1);
@@ -234,26 +273,12 @@ bool small_net(int L, const int32_t* widths, const int32_t* acts, const int64_t*
   t.labels = static_cast<int>(lb);
   for (int l = 0; l < L; ++l) {
     t.act[l] = acts[l];
-    t.woff[l] = static_cast<int>(woff[l]);
-    t.boff[l] = static_cast<int>(boff[l]);
+    t.woff[l] = static_cast<int>(offsets[2 * l] - pbase);
+    t.boff[l] = static_cast<int>(offsets[2 * l + 1] - pbase);
     t.offW[l] = offsets[2 * l];
     t.offB[l] = offsets[2 * l + 1];
-    t.ldw[l] = ldw[l];
+    t.ldw[l] = static_cast<int>(ldw[l]);
   }
-  // what the staging copies: x [B][w_0], the labels, then W_l and b_l per layer
-  int start = 0;
-  auto seg = [&](int src, int64_t goff, int rows, int cols, int gstride, int lds, int lstride) {
-    SmallSeg& s = t.seg[t.nseg++];
-    s = SmallSeg{goff, gstride, cols, lds, lstride, start, src};
-    start += rows * cols;
-  };
-  seg(0, 0, t.B, widths[0], widths[0], t.hoff[0], widths[0]);
-  seg(2, 0, 1, t.B, t.B, t.labels, t.B);
-  for (int l = 0; l < L; ++l) {
-    seg(1, offsets[2 * l], widths[l], widths[l + 1], static_cast<int>(ldw[l]), t.woff[l], t.sw[l]);
-    seg(1, offsets[2 * l + 1], 1, widths[l + 1], widths[l + 1], t.boff[l], widths[l + 1]);
-  }
-  t.nstage = start;  // <= words <= kSmallThreads * kSmallStageRegs
   t.scale = static_cast<float>(1.0 / static_cast<double>(B));
   return true;
 }
@@ -261,7 +286,7 @@ bool small_net(int L, const int32_t* widths, const int32_t* acts, const int64_t*
 hipError_t launch_small_step(const SmallNet& t, const float* params, const float* x,
                              const int32_t* labels, float* loss, float* dparams, float* dx,
                              int32_t* flags, const ZeroGaps& gaps, hipStream_t s) {
-  if (t.nstage > kSmallThreads * kSmallStageRegs) return hipErrorInvalidValue;
+  if (t.pwords > kSmallMaxLds / 4 || t.B * t.w[0] > kSmallMaxLds / 4) return hipErrorInvalidValue;
   launch_kernel(dlvm_small_step_kernel, dim3(1), dim3(kSmallThreads), s, t, params, x, labels,
                 loss, dparams, dx, flags, gaps);
   return hipGetLastError();
