@@ -37,6 +37,7 @@ METRIC = "MLP fwd+grad steps/s, TFLOP/s (% MFMA peak); fused elementwise GB/s"
 # MI355X published peaks: dense MFMA per dtype, and HBM3E bandwidth.
 PEAK_TFLOPS = {"f32": 157.3, "bf16": 2500.0}
 PEAK_HBM_GBS = 8000.0
+PEAK_VALU_F32_TFLOPS = 157.3  # float32 vector FMA rate of the whole chip
 
 
 def parse():
@@ -265,7 +266,13 @@ def measure(m, wl, step, eager_step, steps, warmup, with_sgd, flags_ws=None,
 
     ridge = PEAK_TFLOPS[wl.dtype] * 1e12 / (PEAK_HBM_GBS * 1e9)  # flop per byte
     mfma = dom["flops"] > 0 and (not bound_by_intensity or dom["flops"] >= ridge * dom["bytes"])
-    if mfma:
+    if dom["name"].startswith("small_step"):
+        # one workgroup of plain float32 fused multiply-adds (no matrix cores):
+        # priced against the chip's float32 vector rate (256 CUs x 2.4 GHz)
+        achieved = dom["flops"] / avg_s / 1e12
+        roof = {"bound": "alu", "achieved": round(achieved, 4), "peak": PEAK_VALU_F32_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(achieved / PEAK_VALU_F32_TFLOPS, 6)}
+    elif mfma:
         achieved = dom["flops"] / avg_s / 1e12
         peak = PEAK_TFLOPS[wl.dtype]
         roof = {"bound": "mfma", "achieved": round(achieved, 3), "peak": peak,
