@@ -33,7 +33,8 @@ constexpr TileShape kTiles[] = {
     {4, 64, 64, 0.65, 0.2, false, 2},    {5, 32, 32, 0.5, 0.25, false, 8},
     {10, 256, 256, 0.0, 0.9, true, 0},   {11, 256, 128, 0.0, 0.63, true, 0},
     {12, 128, 128, 0.0, 0.54, true, 0},  {13, 256, 256, 0.0, 0.88, true, 0},
-    {14, 256, 256, 0.0, 0.89, true, 0},  {15, 256, 256, 0.0, 0.85, true, 0}};
+    {14, 256, 256, 0.0, 0.89, true, 0},  {15, 256, 256, 0.0, 0.85, true, 0},
+    {16, 64, 128, 0.0, 0.5, true, 0}};
 
 // The register-staged kernel has one stage of loads in flight: a stage costs
 // at least one load round trip (measured on small float32 products).
@@ -193,6 +194,7 @@ GemmPlan choose(const GemmDesc& d, bool assume_aligned, int64_t capacity, int fo
     // one for the forward layout only; 15 runs only when forced.
     if (t.cfg == 14 && d.layout != Layout::NN && forced != 14) continue;
     if (t.cfg == 15 && forced != 15) continue;
+    if (t.cfg == 16 && (d.layout == Layout::TN || forced != 16)) continue;
     if (forced >= 0 && t.cfg != forced) continue;
     for (int sp = 1; sp <= kMaxSplits; sp *= 2) {
       // a two-phase product's slices must not straddle its phase boundary
@@ -217,6 +219,17 @@ GemmPlan choose(const GemmDesc& d, bool assume_aligned, int64_t capacity, int fo
         best_t = e;
       }
     }
+  }
+  // Measured on 4096 x 1024 outputs (K 784 and 1024): where the 128 x 128
+  // direct-to-LDS tile gives at most one tile per CU, the 64 x 128 tile (two
+  // workgroups per CU, each running while the other waits on its loads) is
+  // faster, even where it costs the paired adjoint launch. Plain products only
+  // (no split, no second phase, no caller-summed slices).
+  if (best != nullptr && best->cfg == 12 && best_s == 1 && forced < 0 && can_async &&
+      d.layout != Layout::TN && d.A2 == nullptr && !d.split_epilogue && d.splits_hint == 0 &&
+      ceil_div(d.M, 128) * ceil_div(d.N, 128) <= kComputeUnits) {
+    for (const TileShape& t : kTiles)
+      if (t.cfg == 16) best = &t;
   }
   if (best == nullptr) {  // a forced configuration or split that cannot run is ignored
     if (forced >= 0 || fsplits > 0) return choose(d, assume_aligned, capacity, -1, -1);
