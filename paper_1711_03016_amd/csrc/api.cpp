@@ -115,6 +115,9 @@ struct WsLayout {
 
 GemmDesc gemm_tn(int dtype, int64_t M, int64_t N, int64_t K, const void* X, const void* dY,
                  int64_t ldy, float* dW, int64_t ldw, float* db, int64_t nvec);
+GemmDesc gemm_nn(int dtype, int out_dtype, int act, int64_t M, int64_t N, int64_t K, float alpha,
+                 const void* X, const void* W, int64_t ldw, const void* bias, void* H,
+                 int64_t ldh);
 
 // k-slices of the output layer's product in a gradient call (1: none). A
 // softmax head with few classes has few output tiles per batch; its
@@ -178,6 +181,12 @@ WsLayout ws_layout(const dlvm_model* m, int64_t B) {
   for (int l = 0; l < m->L; ++l) {
     const int64_t K = m->widths[l], N = m->widths[l + 1], Np = m->ldw[l];
     const GemmDesc d = gemm_tn(m->dtype, B, Np, K, nullptr, nullptr, Np, nullptr, Np, nullptr, N);
+    w.splitk_elems = std::max<int64_t>(w.splitk_elems, dlvm::split_ws_elems(d));
+  }
+  for (int l = 0; l + 1 < m->L; ++l) {  // the hidden layers' forward products (shapes only)
+    GemmDesc d = gemm_nn(m->dtype, m->dtype, m->acts[l], B, m->widths[l + 1], m->widths[l], 1.0f,
+                         nullptr, nullptr, m->ldw[l], nullptr, nullptr, m->widths[l + 1]);
+    d.split_epilogue = true;
     w.splitk_elems = std::max<int64_t>(w.splitk_elems, dlvm::split_ws_elems(d));
   }
   const int hs = head_splits(m, B);
@@ -427,14 +436,25 @@ class Launcher {
 // differentiated, section 3.1.4).
 // Forward product of layer l (0-based): H_{l+1} = act_l(H_l . W_l + b_l), from
 // where H_l lives (x for l = 0) to where H_{l+1} lives.
+// The forward product of hidden layer l; the planner may split it over k
+// (the bias and activation then follow the in-order sum of the slices).
+GemmDesc hidden_desc(const dlvm_model* m, const void* params, const void* in, int64_t batch,
+                     void* out, float* split_ws, int64_t split_elems, int l) {
+  const int dt = m->dtype;
+  GemmDesc d = gemm_nn(dt, dt, m->acts[l], batch, m->widths[l + 1], m->widths[l], 1.0f, in,
+                       param_ptr(m, params, m->offsets[2 * l]), m->ldw[l],
+                       param_ptr(m, params, m->offsets[2 * l + 1]), out, m->widths[l + 1]);
+  d.split_epilogue = true;
+  d.split_ws = split_ws;
+  d.split_ws_elems = split_elems;
+  return d;
+}
+
 dlvm_status plan_hidden_layer(const dlvm_model* m, const void* params, const void* x,
                               int64_t batch, void* ws, const WsLayout& w, int l, Launcher& run) {
-  const int dt = m->dtype;
   const void* in = l == 0 ? x : at<void>(ws, w.H[l]);
-  return run.gemm(gemm_nn(dt, dt, m->acts[l], batch, m->widths[l + 1], m->widths[l], 1.0f, in,
-                          param_ptr(m, params, m->offsets[2 * l]), m->ldw[l],
-                          param_ptr(m, params, m->offsets[2 * l + 1]), at<void>(ws, w.H[l + 1]),
-                          m->widths[l + 1]));
+  return run.gemm(hidden_desc(m, params, in, batch, at<void>(ws, w.H[l + 1]),
+                              at<float>(ws, w.splitk), w.splitk_elems, l));
 }
 
 // The hidden layers' forward (H_1 .. H_{L-1}, each written where it lives).

@@ -598,3 +598,29 @@ def test_forced_tile_configurations(dtype, cfg, batch, monkeypatch):
     rl, rg, rdx = oracle.mlp_gradient(_spec(wl), x, params, y, wrt_x=True)
     _, ref_out = oracle.mlp_forward(_spec(wl), x, params, y)
     _compare(wl, got, rl, rg, rdx, ref_out=ref_out)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("splits", [2, 4])
+def test_split_hidden_layer_products(dtype, splits, monkeypatch):
+    """The hidden layers' forward products split over k (forced through
+    DLVM_GEMM_SPLITS): the slices are summed in slice order and the bias and
+    activation applied after the sum; against the oracle, and two runs bitwise
+    equal."""
+    from dataclasses import replace
+    monkeypatch.setenv("DLVM_GEMM_SPLITS", str(splits))
+    base = workloads.WORKLOADS["c2" if dtype == "f32" else "c3"]
+    wl = replace(base, widths=(1024, 520, 264, 10), acts=("tanh", "relu", "none"), batch=200,
+                 wrt_x=True)
+    m = dl.Model(wl.widths, wl.acts, wl.dtype, wl.loss, True, wl.batch)
+    names = [p["name"] for p in m.plan(wl.batch)]
+    assert names[0].startswith("gemm_nn") and names[0].endswith(f"s{splits}")
+    assert names[1] == "split_epilogue"
+    x, params, y = workloads.make_inputs(wl, bias_scale=0.1)
+    got = _run(wl, x, params, y, wrt_x=True)
+    rl, rg, rdx = oracle.mlp_gradient(_spec(wl), x, params, y, wrt_x=True)
+    _, rout = oracle.mlp_forward(_spec(wl), x, params, y)
+    _compare(wl, got, rl, rg, rdx, ref_out=rout)
+    again = _run(wl, x, params, y, wrt_x=True, forward=False)
+    assert again["loss"] == got["loss"]
+    assert bool((again["dparams"] == got["dparams"]).all())
