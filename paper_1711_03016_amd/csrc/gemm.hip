@@ -223,10 +223,11 @@ GemmPlan choose(const GemmDesc& d, bool assume_aligned, int64_t capacity, int fo
   // Measured on 4096 x 1024 outputs (K 784 and 1024): where the 128 x 128
   // direct-to-LDS tile gives at most one tile per CU, the 64 x 128 tile (two
   // workgroups per CU, each running while the other waits on its loads) is
-  // faster, even where it costs the paired adjoint launch. Plain products only
-  // (no split, no second phase, no caller-summed slices).
+  // faster, even where it costs the paired adjoint launch. Only products
+  // the planner keeps whole of their own accord (no split asked for by the
+  // caller, no second phase).
   if (best != nullptr && best->cfg == 12 && best_s == 1 && forced < 0 && can_async &&
-      d.layout != Layout::TN && d.A2 == nullptr && !d.split_epilogue && d.splits_hint == 0 &&
+      d.layout != Layout::TN && d.A2 == nullptr && d.splits_hint == 0 &&
       ceil_div(d.M, 128) * ceil_div(d.N, 128) <= kComputeUnits) {
     for (const TileShape& t : kTiles)
       if (t.cfg == 16) best = &t;
