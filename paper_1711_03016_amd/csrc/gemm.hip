@@ -18,7 +18,7 @@ constexpr double kL2BytesPerClock = 64.0;
 // Tile configurations with the fraction of the matrix-core rate each sustains
 // when not starved, for float32 and for bf16 operands (measured on large
 // products). Configurations 0-5 are the register-staged kernel
-// (gemm_kernel.hpp), 10-13 the bf16 kernel with direct-to-LDS loads
+// (gemm_kernel.hpp), 10-13 and 16 the bf16 kernel with direct-to-LDS loads
 // (gemm_async.hpp), 14-15 the four-wave bf16 kernel (gemm_xl.hpp).
 struct TileShape {
   int cfg;
@@ -34,7 +34,7 @@ constexpr TileShape kTiles[] = {
     {10, 256, 256, 0.0, 0.9, true, 0},   {11, 256, 128, 0.0, 0.63, true, 0},
     {12, 128, 128, 0.0, 0.54, true, 0},  {13, 256, 256, 0.0, 0.88, true, 0},
     {14, 256, 256, 0.0, 0.89, true, 0},  {15, 256, 256, 0.0, 0.85, true, 0},
-    {16, 64, 128, 0.0, 0.5, true, 0}};
+    {16, 64, 128, 0.0, 0.5, true, 0},    {17, 128, 128, 0.0, 0.54, true, 0}};
 
 // The register-staged kernel has one stage of loads in flight: a stage costs
 // at least one load round trip (measured on small float32 products).
@@ -195,6 +195,7 @@ GemmPlan choose(const GemmDesc& d, bool assume_aligned, int64_t capacity, int fo
     if (t.cfg == 14 && d.layout != Layout::NN && forced != 14) continue;
     if (t.cfg == 15 && forced != 15) continue;
     if (t.cfg == 16 && (d.layout == Layout::TN || forced != 16)) continue;
+    if (t.cfg == 17 && forced != 17) continue;
     if (forced >= 0 && t.cfg != forced) continue;
     for (int sp = 1; sp <= kMaxSplits; sp *= 2) {
       // a two-phase product's slices must not straddle its phase boundary
@@ -231,6 +232,20 @@ GemmPlan choose(const GemmDesc& d, bool assume_aligned, int64_t capacity, int fo
       ceil_div(d.M, 128) * ceil_div(d.N, 128) <= kComputeUnits) {
     for (const TileShape& t : kTiles)
       if (t.cfg == 16) best = &t;
+  }
+  // The same for a product w.r.t. the weights split into k-slices that fill
+  // the CUs once: the 128 x 128 tile with a 2-deep ring (64 KiB, two
+  // workgroups per CU) and twice the slices.
+  if (best != nullptr && best->cfg == 12 && best_s > 1 && 2 * best_s <= kMaxSplits &&
+      forced < 0 && fsplits < 0 && can_async && d.layout == Layout::TN && d.A2 == nullptr &&
+      d.splits_hint == 0 &&
+      ceil_div(d.M, 128) * ceil_div(d.N, 128) * best_s <= kComputeUnits &&
+      slice_k(d.K, 2 * best_s) >= kMinChunk &&
+      ceil_div(d.K, slice_k(d.K, 2 * best_s)) == 2 * best_s &&
+      split_need(d, 2 * best_s) <= capacity) {
+    for (const TileShape& t : kTiles)
+      if (t.cfg == 17) best = &t;
+    best_s *= 2;
   }
   if (best == nullptr) {  // a forced configuration or split that cannot run is ignored
     if (forced >= 0 || fsplits > 0) return choose(d, assume_aligned, capacity, -1, -1);

@@ -506,6 +506,8 @@ __global__ __launch_bounds__(64 * WM * WN) void dlvm_gemm_async_pair_kernel(Para
 //   13: 256 x 256, BK 32, 2 x 4 waves (128 x 64 per wave),  4 stages (128 KiB LDS)
 //   16:  64 x 128, BK 64, 2 x 2 waves (32 x 64 per wave),   3 stages (72 KiB LDS: two
 //        workgroups per CU); k-contiguous A only (NN, NT)
+//   17: 128 x 128, BK 64, 2 x 2 waves (64 x 64 per wave),   2 stages (64 KiB LDS: two
+//        workgroups per CU)
 constexpr int kAsyncFirst = 10;
 
 template <typename TO, bool AK, bool BKM, int EPI, bool PH2 = false>
@@ -519,6 +521,9 @@ hipError_t launch_async(const Params& p, int cfg, unsigned grid, hipStream_t s) 
       break;
     case 12:
       launch_kernel((dlvm_gemm_async_kernel<TO, AK, BKM, 128, 128, 64, 2, 2, 4, EPI, PH2>), dim3(grid), dim3(256), s, p);
+      break;
+    case 17:
+      launch_kernel((dlvm_gemm_async_kernel<TO, AK, BKM, 128, 128, 64, 2, 2, 2, EPI, PH2>), dim3(grid), dim3(256), s, p);
       break;
     case 16:
       if constexpr (AK) {  // (an m-contiguous A needs 128-row tiles)

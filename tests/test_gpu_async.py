@@ -28,7 +28,7 @@ from helpers import TOL, device, quant, rel_l2, to_dev, to_np
 
 pytestmark = pytest.mark.gpu
 
-CFGS = [10, 11, 12, 13, 14, 15, 16]
+CFGS = [10, 11, 12, 13, 14, 15, 16, 17]
 EXACT = 1e-5
 # (M, N, K): single tile with K = 8, exact tiles, ragged edges with K % 64 != 0,
 # many k-tiles (deeper than every ring), and a wide ragged product.
