@@ -123,6 +123,11 @@ def lib() -> ctypes.CDLL:
         if not os.path.exists(LIB_PATH):
             raise RuntimeError(f"{LIB_PATH} is missing: build it with "
                                "`python -m paper_1711_03016_amd.build`")
+        # torch brings its own HIP runtime (libamdhip64 with the same soname).
+        # Loaded first, it is the one the library binds to; loaded after the
+        # library, it would be a second HIP/HSA runtime in the process, and
+        # the library's launches would then fail to find the device.
+        import torch  # noqa: F401
         h = ctypes.CDLL(LIB_PATH)
         for name, (res, args) in _SIGS.items():
             fn = getattr(h, name)

@@ -330,5 +330,33 @@ def test_small_network_plan(monkeypatch):
         .plan(256)[0]["name"].startswith("small")
     assert not dl.Model((64, 32, 10), ("sigmoid", "none"), "bf16", batch_max=16) \
         .plan(16)[0]["name"].startswith("small")
+    # at the limits: LDS (the batch), the layer count
+    assert dl.Model((6, 3), ("none",), batch_max=600).plan(600)[0]["name"] == "small_step_f32"
+    assert dl.Model((6, 3), ("none",), batch_max=1000).plan(1000)[0]["name"].startswith("gemm")
+    deep = (12,) * 8 + (10,)
+    assert dl.Model(deep, ("tanh",) * 7 + ("none",), batch_max=8).plan(8)[0]["name"] == "small_step_f32"
+    deeper = (12,) * 9 + (10,)
+    assert dl.Model(deeper, ("tanh",) * 8 + ("none",), batch_max=8).plan(8)[0]["name"].startswith("gemm")
     monkeypatch.setenv("DLVM_SMALL_STEP", "0")
     assert small.plan(16)[0]["name"].startswith("gemm_nn")
+
+
+def test_one_hip_runtime_whatever_the_import_order():
+    """The library loaded before the caller imports torch still binds to
+    torch's HIP runtime: one libamdhip64 mapped in the process (a second one
+    would be a second HIP/HSA runtime, whose launches cannot find the
+    device)."""
+    import subprocess
+    import sys
+    code = (
+        "import paper_1711_03016_amd as dl\n"
+        "dl.lib()\n"
+        "import torch\n"
+        "paths = {l.split()[-1] for l in open('/proc/self/maps') if 'libamdhip64' in l}\n"
+        "print(len(paths))\n"
+    )
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    out = subprocess.run([sys.executable, "-c", code], cwd=root, capture_output=True, text=True,
+                         timeout=300)
+    assert out.returncode == 0, out.stderr[-2000:]
+    assert out.stdout.strip().splitlines()[-1] == "1"

@@ -545,6 +545,9 @@ def torch_equal(a, b):
     ((37, 50, 23, 10), ("relu", "tanh", "none"), 7, True),      # ragged widths and batch
     ((96, 48, 48, 40, 30), ("tanh", "relu", "sigmoid", "none"), 9, False),
     ((20, 300), ("none",), 5, True),                             # one layer, wide head
+    ((6, 3), ("none",), 600, True),                              # a large batch (LDS nearly full)
+    ((8, 8, 4), ("relu", "none"), 400, False),
+    ((12,) * 8 + (10,), ("tanh",) * 7 + ("none",), 8, True),     # the most layers it takes
 ])
 def test_small_network_path(widths, acts, batch, wrt_x, monkeypatch):
     """The one-workgroup gradient of a small float32 network against the
