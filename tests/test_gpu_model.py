@@ -627,3 +627,32 @@ def test_split_hidden_layer_products(dtype, splits, monkeypatch):
     again = _run(wl, x, params, y, wrt_x=True, forward=False)
     assert again["loss"] == got["loss"]
     assert bool((again["dparams"] == got["dparams"]).all())
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_small_network_random_shapes(seed, monkeypatch):
+    """Seeded random small networks (1-4 layers, widths 1-80, batch 1-64,
+    random activations, with and without dx) through the one-workgroup
+    gradient, against the oracle and the multi-launch plan."""
+    from dataclasses import replace
+    rng = np.random.default_rng(900 + seed)
+    L = int(rng.integers(1, 5))
+    widths = tuple(int(v) for v in rng.integers(1, 81, size=L + 1))
+    widths = widths[:-1] + (max(widths[-1], 2),)          # at least two classes
+    acts = tuple(str(a) for a in rng.choice(["none", "relu", "tanh", "sigmoid"], size=L - 1)) + ("none",)
+    batch = int(rng.integers(1, 65))
+    wrt_x = bool(rng.integers(0, 2))
+    while dl.Model(widths, acts, "f32", "softmax_ce", wrt_x, batch).plan(batch)[0]["name"] \
+            != "small_step_f32":
+        assert batch > 1, widths
+        batch //= 2                                       # until it fits the workgroup's LDS
+    wl = replace(workloads.WORKLOADS["c1"], widths=widths, acts=acts, batch=batch, wrt_x=wrt_x)
+    x, params, y = workloads.make_inputs(wl, bias_scale=0.1)
+    got = _run(wl, x, params, y, wrt_x=wrt_x, forward=False)
+    rl, rg, rdx = oracle.mlp_gradient(_spec(wl), x, params, y, wrt_x=wrt_x)
+    _compare(wl, got, rl, rg, rdx if wrt_x else None)
+    monkeypatch.setenv("DLVM_SMALL_STEP", "0")
+    gen = _run(wl, x, params, y, wrt_x=wrt_x, forward=False)
+    assert abs(got["loss"] - gen["loss"]) <= 1e-5 * max(abs(gen["loss"]), 1e-30)
+    for (a, b), (c, d) in zip(got["grads"], gen["grads"]):
+        assert rel_l2(a, c) <= 1e-5 and rel_l2(b, d) <= 1e-5
