@@ -226,7 +226,7 @@ def measure(m, wl, step, eager_step, steps, warmup, with_sgd, flags_ws=None,
     plan = m.plan(B)
     if not with_sgd:
         plan = plan[:-1]
-    probe_steps = 3
+    probe_steps = 20  # (a few steps let one slow dispatch pick the wrong launch)
     m.probe_arm(-1, probe_steps * len(plan) + 8)
     for _ in range(probe_steps):
         eager_step()
