@@ -18,7 +18,7 @@ constexpr double kL2BytesPerClock = 64.0;
 // Tile configurations with the fraction of the matrix-core rate each sustains
 // when not starved, for float32 and for bf16 operands (measured on large
 // products). Configurations 0-5 are the register-staged kernel
-// (gemm_kernel.hpp), 10-13 and 16 the bf16 kernel with direct-to-LDS loads
+// (gemm_kernel.hpp), 10-13, 16 and 17 the bf16 kernel with direct-to-LDS loads
 // (gemm_async.hpp), 14-15 the four-wave bf16 kernel (gemm_xl.hpp).
 struct TileShape {
   int cfg;
