@@ -15,7 +15,12 @@ duration measured with HIP events on the launch stream during the timed steps.
 ``cpu_baseline`` times the float64 oracle on the host cores on a bounded sample
 of the same workload.
 
-Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c2]
+With no --workload the step is the deep bf16 network's training step (c5:
+4096 -> 8 x 4096 relu -> 1000, softmax cross-entropy, batch 16384, gradient and
+fused SGD), the largest configuration of the metric; the others are selected
+with --workload.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c5]
 """
 from __future__ import annotations
 
@@ -45,7 +50,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=None)
     ap.add_argument("--warmup", type=int, default=None)
-    ap.add_argument("--workload", default="c2",
+    ap.add_argument("--workload", default="c5",
                     choices=sorted(workloads.WORKLOADS) + sorted(workloads.RNN_WORKLOADS) +
                     sorted(workloads.CHAIN_WORKLOADS))
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
@@ -132,48 +137,113 @@ def default_steps(wl) -> tuple[int, int]:
     return 2000, 100
 
 
+def host_facts() -> dict:
+    """What the oracle baseline ran on: logical CPUs, the cores this process
+    may run on (affinity mask) and the CPU model."""
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"nproc": os.cpu_count(), "affinity_cores": len(os.sched_getaffinity(0)),
+            "cpu_model": model}
+
+
+def blas_threads() -> int:
+    try:
+        from threadpoolctl import threadpool_info
+        return max([d.get("num_threads", 1) for d in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover - threadpoolctl is optional
+        return os.cpu_count() or 1
+
+
+def single_thread(fn):
+    """Run fn() with the BLAS limited to one thread and the calling thread
+    pinned to one core of the affinity mask."""
+    from threadpoolctl import threadpool_limits
+    old = os.sched_getaffinity(0)
+    os.sched_setaffinity(0, {min(old)})
+    try:
+        with threadpool_limits(limits=1):
+            return fn()
+    finally:
+        os.sched_setaffinity(0, old)
+
+
 def cpu_baseline(wl, budget_s: float) -> dict | None:
-    """Time the oracle (as it stands) on the host on a bounded sample."""
+    """Time the oracle (as it stands) on the host on a bounded sample: with
+    the BLAS on all its threads, then on one thread pinned to one core.
+
+    A workload whose whole batch is cheap is timed at full size. Otherwise
+    the gradient is timed on r and 2r rows of the batch and its time fitted
+    as fixed + per_row * rows (the fixed part, e.g. rounding every parameter
+    to bf16, does not grow with the rows; every product does), evaluated at
+    the full batch (after one untimed call); the update is timed once as it
+    is (it does not depend on the rows)."""
     if budget_s <= 0:
         return None
     import oracle
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([d.get("num_threads", 1) for d in threadpool_info()] or [1])
-    except Exception:  # pragma: no cover - threadpoolctl is optional
-        threads = os.cpu_count() or 1
-    # sample: the whole batch when one oracle step is short, else a slice of rows
-    rows = wl.batch
-    while rows > 16 and wl.flops(rows) > 6e10:
-        rows //= 2
-    x, params, y = workloads.make_inputs(wl, batch=rows)
     spec = oracle.MlpSpec(wl.widths, wl.acts, wl.loss, wl.dtype)
-    n = 0
-    t_grad = t_sgd = 0.0
-    while True:
-        t0 = time.perf_counter()
-        loss, grads, _ = oracle.mlp_gradient(spec, x, params, y, wrt_x=wl.wrt_x)
-        t1 = time.perf_counter()
+
+    def update(params, grads):
+        for (W, b), (dW, db) in zip(params, grads):
+            oracle.sgd_f32(W, dW, wl.lr)
+            oracle.sgd_f32(b, db, wl.lr)
+
+    def run(cap_flops: float, budget: float):
+        if wl.flops(wl.batch) <= cap_flops:
+            x, params, y = workloads.make_inputs(wl)
+            n, el = 0, 0.0
+            while True:
+                t0 = time.perf_counter()
+                _, grads, _ = oracle.mlp_gradient(spec, x, params, y, wrt_x=wl.wrt_x)
+                if wl.sgd:
+                    update(params, grads)
+                el += time.perf_counter() - t0
+                n += 1
+                if el >= budget or el * (n + 1) / n > 2 * budget:
+                    break
+            return n / el, (f"{n} oracle steps (float64 gradient{' + SGD' if wl.sgd else ''}) "
+                            f"on the whole batch of {wl.batch} rows in {el:.1f} s")
+        r = wl.batch
+        while r > 1 and wl.flops(2 * r) > cap_flops:
+            r //= 2
+        x, params, y = workloads.make_inputs(wl, batch=2 * r)
+        # one untimed call first: the first touch of the oracle's large
+        # temporaries (every parameter in float64) costs several times a step
+        oracle.mlp_gradient(spec, x[:r], params, y[:r], wrt_x=wl.wrt_x)
+        t = []
+        for rows in (r, 2 * r):
+            t0 = time.perf_counter()
+            _, grads, _ = oracle.mlp_gradient(spec, x[:rows], params, y[:rows], wrt_x=wl.wrt_x)
+            t.append(time.perf_counter() - t0)
+        per_row = max((t[1] - t[0]) / r, 0.0)
+        fixed = max(t[0] - per_row * r, 0.0)
+        t_sgd = 0.0
         if wl.sgd:
-            for (W, b), (dW, db) in zip(params, grads):
-                oracle.sgd_f32(W, dW, wl.lr)
-                oracle.sgd_f32(b, db, wl.lr)
-        t2 = time.perf_counter()
-        t_grad += t1 - t0
-        t_sgd += t2 - t1
-        n += 1
-        el = t_grad + t_sgd
-        if el >= budget_s or el * (n + 1) / n > 2 * budget_s:
-            break
-    # the gradient's work is linear in the rows; the update's does not depend on them
-    per_step = (t_grad / n) * (wl.batch / rows) + t_sgd / n
-    sample = (f"{n} oracle steps (float64 gradient{' + SGD' if wl.sgd else ''}) on "
-              f"{rows} of {wl.batch} rows in {el:.1f} s")
-    if rows != wl.batch:
-        sample += (f"; gradient time scaled by {wl.batch}/{rows} rows (each of its terms is "
-                   "linear in the rows), update time taken as measured")
-    return {"value": 1.0 / per_step, "unit": "steps/s", "cores": int(threads),
-            "kind": "oracle", "sample": sample}
+            t0 = time.perf_counter()
+            update(params, grads)
+            t_sgd = time.perf_counter() - t0
+        per_step = fixed + per_row * wl.batch + t_sgd
+        sample = (f"float64 oracle gradient on {r} rows ({t[0]:.2f} s) and {2 * r} rows "
+                  f"({t[1]:.2f} s) of the {wl.batch}, fitted as {fixed:.2f} s + "
+                  f"{per_row * 1e3:.2f} ms per row and evaluated at {wl.batch} rows"
+                  + (f", plus one SGD update over all parameters ({t_sgd:.2f} s)" if wl.sgd else ""))
+        return 1.0 / per_step, sample
+
+    threads = blas_threads()
+    value, sample = run(1.1e11, budget_s / 2)
+    one_value, one_sample = single_thread(lambda: run(2.6e10, budget_s / 2))
+    return {"value": value, "unit": "steps/s", "cores": int(threads), "kind": "oracle",
+            "sample": sample,
+            "single_thread": {"value": one_value, "unit": "steps/s", "cores": 1,
+                              "sample": one_sample + "; BLAS limited to one thread, pinned "
+                                                     "to one core"},
+            "host": host_facts()}
 
 
 def vjp_bench(args, wl, m, P, xd, dP, dx, ws, stream, steps, warmup):
@@ -363,11 +433,7 @@ def rnn_cpu_baseline(wl, budget_s: float) -> dict | None:
     if budget_s <= 0:
         return None
     import oracle
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([d.get("num_threads", 1) for d in threadpool_info()] or [1])
-    except Exception:  # pragma: no cover - threadpoolctl is optional
-        threads = os.cpu_count() or 1
+    threads = blas_threads()
     rows = wl.batch
     while rows > 4 and wl.flops(rows) > 4e10:
         rows //= 2
@@ -397,7 +463,7 @@ def rnn_cpu_baseline(wl, budget_s: float) -> dict | None:
         sample += (f"; forward and gradient time scaled by {wl.batch}/{rows} rows (linear in "
                    "the rows), update time taken as measured")
     return {"value": 1.0 / per_step, "unit": "steps/s", "cores": int(threads),
-            "kind": "oracle", "sample": sample}
+            "kind": "oracle", "sample": sample, "host": host_facts()}
 
 
 def chain_main(args, wl) -> None:
@@ -471,11 +537,7 @@ def chain_cpu_baseline(wl, budget_s: float) -> dict | None:
     if budget_s <= 0:
         return None
     import oracle
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([d.get("num_threads", 1) for d in threadpool_info()] or [1])
-    except Exception:  # pragma: no cover - threadpoolctl is optional
-        threads = os.cpu_count() or 1
+    threads = blas_threads()
     mats = workloads.make_chain_inputs(wl.dims)
     rows = wl.dims[0]
     while rows > 16 and rows * sum(wl.dims[k + 1] * wl.dims[k + 2] for k in range(wl.n - 1)) > 2e9:
@@ -491,7 +553,7 @@ def chain_cpu_baseline(wl, budget_s: float) -> dict | None:
             break
     per = el / n * wl.dims[0] / rows
     return {"value": 1.0 / per, "unit": "steps/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{n} oracle chain products (float64, left to right) on {rows} of "
+            "host": host_facts(), "sample": f"{n} oracle chain products (float64, left to right) on {rows} of "
                       f"{wl.dims[0]} rows of A_0 in {el:.1f} s, scaled by {wl.dims[0]}/{rows}"}
 
 

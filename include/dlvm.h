@@ -120,6 +120,35 @@ dlvm_status dlvm_param_layout(const dlvm_model* m, int64_t* offsets, int64_t* ld
  * concurrently. */
 size_t dlvm_workspace_bytes(const dlvm_model* m, int64_t batch);
 
+/* Where a gradient call keeps the intermediate values of the adjoint code
+ * (section 3.1.3: the gradient function recomputes the forward keeping the
+ * layer outputs, then writes one adjoint per layer) inside a workspace for
+ * `batch` rows, so that a caller can read them after the call has completed
+ * (e.g. to check one layer at a time). Host only. On success *offset is the
+ * byte offset from the workspace base, *ld the row stride in elements and
+ * *dtype the element type (DLVM_F32 / DLVM_BF16) of a row-major
+ * [batch, ...] tensor:
+ *   DLVM_WS_HIDDEN,  layer l in [1, L-1]: H_l, the output of hidden layer l
+ *     (widths[l] columns, ld = widths[l], storage dtype), the input of layer
+ *     l + 1's products. With checkpoint_every k > 1, an H_l with l % k != 0
+ *     shares a slot with other layers and holds whatever was computed there last.
+ *   DLVM_WS_LOGITS (layer ignored): the output layer's product, float32
+ *     [batch, widths[L]] (the logits; z = x.W for CHAIN8). DLVM_ERR_UNSUPPORTED
+ *     when the plan never stores it: a softmax head whose product the loss
+ *     kernel receives as k-slices, or a chain run in the product's epilogue.
+ *   DLVM_WS_ADJOINT, layer l in [1, L]: dZ_l, the adjoint of layer l's output
+ *     before its activation (l = L: the adjoint of the logits, (softmax(z) -
+ *     onehot(y)) / batch for SOFTMAX_CE), ld = the row stride of W_l
+ *     (dlvm_param_layout; the padding columns hold zero), storage dtype
+ *     (float32 for CHAIN8).
+ * DLVM_ERR_INVALID_ARG for an unknown kind, a layer out of range or an
+ * invalid batch; DLVM_ERR_UNSUPPORTED for recurrent and matrix-chain handles
+ * and for a network whose gradient runs as one workgroup (see dlvm_gradient:
+ * that launch keeps every intermediate value in LDS). */
+enum { DLVM_WS_HIDDEN = 0, DLVM_WS_LOGITS = 1, DLVM_WS_ADJOINT = 2 };
+dlvm_status dlvm_workspace_tensor(const dlvm_model* m, int64_t batch, int32_t kind, int32_t layer,
+                                  size_t* offset, int64_t* ld, int32_t* dtype);
+
 /* The original function (Fig. 3's @foo): writes `out`, float32 [batch, widths[L]]:
  * the logits for SOFTMAX_CE, the chain value e for CHAIN8. Saves nothing (the
  * forward of a function that is not differentiated keeps no activations). */

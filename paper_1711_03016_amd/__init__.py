@@ -23,6 +23,7 @@ F32, BF16 = 0, 1
 ACTS = {"none": 0, "sigmoid": 1, "tanh": 2, "relu": 3}
 DTYPES = {"f32": F32, "bf16": BF16}
 LOSSES = {"softmax_ce": 0, "chain8": 1}
+WS_HIDDEN, WS_LOGITS, WS_ADJOINT = 0, 1, 2
 
 
 class DlvmError(RuntimeError):
@@ -78,6 +79,8 @@ _SIGS = {
     "dlvm_param_count": (_I64, [_P]),
     "dlvm_param_layout": (_I32, [_P, ctypes.POINTER(_I64), ctypes.POINTER(_I64)]),
     "dlvm_workspace_bytes": (ctypes.c_size_t, [_P, _I64]),
+    "dlvm_workspace_tensor": (_I32, [_P, _I64, _I32, _I32, ctypes.POINTER(ctypes.c_size_t),
+                                     ctypes.POINTER(_I64), ctypes.POINTER(_I32)]),
     "dlvm_forward": (_I32, [_P, _P, _P, _I64, _P, _P, ctypes.c_size_t, _P]),
     "dlvm_gradient": (_I32, [_P, _P, _P, _P, _I64, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "dlvm_sgd_step": (_I32, [_P, _P, _P, _P, _F, _P]),
@@ -239,6 +242,23 @@ class Model:
 
     def workspace_bytes(self, batch: int) -> int:
         return int(lib().dlvm_workspace_bytes(self._h, int(batch)))
+
+    def workspace_tensor_info(self, batch: int, kind: int, layer: int = 0) -> tuple[int, int, int]:
+        """(byte offset, row stride, dtype code) of a tensor a gradient call
+        keeps in its workspace (``dlvm_workspace_tensor``)."""
+        off, ld, dt = ctypes.c_size_t(), _I64(), _I32()
+        _check(lib().dlvm_workspace_tensor(self._h, int(batch), int(kind), int(layer),
+                                           ctypes.byref(off), ctypes.byref(ld), ctypes.byref(dt)))
+        return int(off.value), int(ld.value), int(dt.value)
+
+    def workspace_tensor(self, ws, batch: int, kind: int, layer: int = 0):
+        """A [batch, ld] view into the byte tensor `ws` of the saved layer
+        output (WS_HIDDEN), the logits (WS_LOGITS) or a layer's adjoint
+        (WS_ADJOINT) that the last gradient call on `ws` wrote."""
+        import torch
+        off, ld, dt = self.workspace_tensor_info(batch, kind, layer)
+        tdt, es = (torch.float32, 4) if dt == F32 else (torch.bfloat16, 2)
+        return ws[off:off + int(batch) * ld * es].view(tdt).view(int(batch), ld)
 
     def forward(self, params, x, batch, out, ws, stream=None) -> None:
         _check(lib().dlvm_forward(self._h, _ptr(params), _ptr(x), int(batch), _ptr(out),

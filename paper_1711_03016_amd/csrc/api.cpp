@@ -1113,6 +1113,49 @@ size_t dlvm_workspace_bytes(const dlvm_model* m, int64_t batch) {
   return ws_total(m, batch);
 }
 
+dlvm_status dlvm_workspace_tensor(const dlvm_model* m, int64_t batch, int32_t kind, int32_t layer,
+                                  size_t* offset, int64_t* ld, int32_t* dtype) {
+  if (m == nullptr || offset == nullptr || ld == nullptr || dtype == nullptr)
+    return fail(DLVM_ERR_INVALID_ARG, "null argument");
+  if (m->kind != 0) return fail(DLVM_ERR_UNSUPPORTED, "only dense networks keep these tensors");
+  const dlvm_status st = check_batch(m, batch);
+  if (st != DLVM_OK) return st;
+  const int L = m->L;
+  const bool chain = m->loss == DLVM_LOSS_CHAIN8;
+  dlvm::SmallNet sn{};
+  if (!chain && small_step_allowed() && m->dtype == DLVM_F32 &&
+      dlvm::small_net(L, m->widths.data(), m->acts.data(), m->offsets.data(), m->ldw.data(),
+                      batch, m->wrt_x != 0, sn))
+    return fail(DLVM_ERR_UNSUPPORTED,
+                "the one-workgroup gradient of this network keeps its tensors in LDS only");
+  const WsLayout w = ws_layout(m, batch);
+  switch (kind) {
+    case DLVM_WS_HIDDEN:
+      if (layer < 1 || layer >= L) return fail(DLVM_ERR_INVALID_ARG, "hidden layer outside [1, L-1]");
+      *offset = w.H[layer];
+      *ld = m->widths[layer];
+      *dtype = m->dtype;
+      return DLVM_OK;
+    case DLVM_WS_LOGITS:
+      if (chain ? m->chain_epi != 0 : head_splits(m, batch) > 1)
+        return fail(DLVM_ERR_UNSUPPORTED,
+                    "this plan never stores the output layer's product (its loss kernel sums "
+                    "the product's k-slices, or the chain runs in the product's epilogue)");
+      *offset = w.logits;
+      *ld = m->widths[L];
+      *dtype = DLVM_F32;
+      return DLVM_OK;
+    case DLVM_WS_ADJOINT:
+      if (layer < 1 || layer > L) return fail(DLVM_ERR_INVALID_ARG, "layer outside [1, L]");
+      *offset = w.dz[layer - 1];
+      *ld = m->ldw[layer - 1];
+      *dtype = chain ? DLVM_F32 : m->dtype;
+      return DLVM_OK;
+    default:
+      return fail(DLVM_ERR_INVALID_ARG, "unknown workspace tensor kind");
+  }
+}
+
 dlvm_status dlvm_forward(const dlvm_model* m, const void* params, const void* x, int64_t batch,
                          float* out, void* ws, size_t ws_bytes, void* stream) {
   if (m == nullptr || params == nullptr || x == nullptr || out == nullptr)

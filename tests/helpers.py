@@ -15,6 +15,48 @@ def rel_l2(got, ref) -> float:
     return float(num / den) if den > 0 else float(num)
 
 
+def rel_rows(got, ref, floor: float = 0.05) -> float:
+    """The largest relative error of one row: max_i ||g_i - o_i|| / ||o_i||.
+
+    A whole-tensor norm hides a single wrong row (one row of 4096 left at zero
+    moves the tensor's relative error by 1/64); this measure does not. A row
+    whose norm is below `floor` times the root-mean-square row norm is
+    measured against that floor instead, so rows that are nearly zero (a ReLU
+    output with few active units) are not judged on their rounding noise
+    alone. One-dimensional arrays are taken one element per row.
+    """
+    g = np.asarray(got, np.float64)
+    o = np.asarray(ref, np.float64)
+    assert g.shape == o.shape, (g.shape, o.shape)
+    if g.size == 0:
+        return 0.0
+    if g.ndim == 1:
+        g, o = g[:, None], o[:, None]
+    g = g.reshape(g.shape[0], -1)
+    o = o.reshape(o.shape[0], -1)
+    num = np.linalg.norm(g - o, axis=1)
+    den = np.linalg.norm(o, axis=1)
+    rms = float(np.sqrt(np.mean(den ** 2)))
+    if rms == 0.0:
+        return float(num.max())
+    return float((num / np.maximum(den, floor * rms)).max())
+
+
+def assert_close(got, ref, tol: float, what="", row_tol: float | None = None,
+                 floor: float | None = None) -> None:
+    """Whole-tensor relative L2 error within `tol` and every row's relative
+    error (rel_rows) within `row_tol` (default: `tol`). Vectors are checked
+    element by element against their root-mean-square (floor 1) unless a
+    floor is given."""
+    row_tol = tol if row_tol is None else row_tol
+    if floor is None:
+        floor = 1.0 if np.ndim(ref) == 1 else 0.05
+    e = rel_l2(got, ref)
+    r = rel_rows(got, ref, floor)
+    assert e <= tol, (what, "rel_l2", e, tol)
+    assert r <= row_tol, (what, "worst row", r, row_tol)
+
+
 def device():
     import torch
     assert torch.cuda.is_available(), "this test needs a GPU"

@@ -104,6 +104,55 @@ def test_layout_and_plan(name):
     assert len(tn) + len(pair) == wl.n_layers
 
 
+@pytest.mark.parametrize("name", sorted(workloads.WORKLOADS))
+def test_workspace_tensors(name):
+    """dlvm_workspace_tensor (host only): the saved layer outputs, logits and
+    adjoints lie inside the workspace, do not overlap, have the documented
+    strides and types, and invalid requests are refused."""
+    wl = workloads.WORKLOADS[name]
+    B = wl.batch
+    m = dl.Model(wl.widths, wl.acts, wl.dtype, wl.loss, wl.wrt_x, B)
+    if m.plan(B)[0]["name"] == "small_step_f32":
+        with pytest.raises(dl.DlvmError) as e:       # c1: everything stays in LDS
+            m.workspace_tensor_info(B, dl.WS_ADJOINT, 1)
+        assert e.value.status == dl.ERR_UNSUPPORTED
+        return
+    total = m.workspace_bytes(B)
+    _, lds = m.param_layout_lds()
+    L = wl.n_layers
+    chain = wl.loss == "chain8"
+    spans = []
+    for l in range(1, L):
+        off, ld, dt = m.workspace_tensor_info(B, dl.WS_HIDDEN, l)
+        assert ld == wl.widths[l] and dt == dl.DTYPES[wl.dtype]
+        spans.append((off, off + B * ld * (2 if dt == dl.BF16 else 4)))
+    for l in range(1, L + 1):
+        off, ld, dt = m.workspace_tensor_info(B, dl.WS_ADJOINT, l)
+        assert ld == lds[l - 1]
+        assert dt == (dl.F32 if chain else dl.DTYPES[wl.dtype])
+        spans.append((off, off + B * ld * (2 if dt == dl.BF16 else 4)))
+    split_head = any(e["name"] == "split_softmax_xent" for e in m.plan(B))
+    if split_head:
+        with pytest.raises(dl.DlvmError) as e:
+            m.workspace_tensor_info(B, dl.WS_LOGITS)
+        assert e.value.status == dl.ERR_UNSUPPORTED
+    else:
+        off, ld, dt = m.workspace_tensor_info(B, dl.WS_LOGITS)
+        assert ld == wl.widths[L] and dt == dl.F32
+        spans.append((off, off + B * ld * 4))
+    spans.sort()
+    assert all(a % 16 == 0 for a, _ in spans)
+    assert all(b <= c for (_, b), (c, _) in zip(spans, spans[1:]))   # disjoint
+    assert spans[-1][1] <= total
+    for kind, layer in ((dl.WS_HIDDEN, 0), (dl.WS_HIDDEN, L), (dl.WS_ADJOINT, 0),
+                        (dl.WS_ADJOINT, L + 1), (7, 1)):
+        with pytest.raises(dl.DlvmError) as e:
+            m.workspace_tensor_info(B, kind, layer)
+        assert e.value.status == dl.ERR_INVALID_ARG
+    with pytest.raises(dl.DlvmError):
+        m.workspace_tensor_info(B + 1, dl.WS_ADJOINT, 1)
+
+
 @pytest.mark.parametrize("ckpt,status", [(0, dl.OK), (1, dl.OK), (3, dl.OK), (4, dl.OK),
                                          (5, dl.ERR_INVALID_ARG), (-1, dl.ERR_INVALID_ARG)])
 def test_checkpoint_every_is_validated(ckpt, status):

@@ -24,12 +24,13 @@ import pytest
 import oracle
 import paper_1711_03016_amd as dl
 import workloads
-from helpers import TOL, device, quant, rel_l2, to_dev, to_np
+from helpers import TOL, assert_close, device, quant, rel_l2, to_dev, to_np
 
 pytestmark = pytest.mark.gpu
 
 CFGS = [10, 11, 12, 13, 14, 15, 16, 17]
 EXACT = 1e-5
+ROW_EXACT = 1e-4   # the same, for the worst single row (fewer terms average out)
 # (M, N, K): single tile with K = 8, exact tiles, ragged edges with K % 64 != 0,
 # many k-tiles (deeper than every ring), and a wide ragged product.
 SHAPES = [(8, 136, 8), (256, 256, 64), (520, 264, 200), (1000, 1000, 1000), (264, 520, 2056),
@@ -63,8 +64,10 @@ def test_async_forward(cfg, shape):
             torch.cuda.synchronize()
             ref = oracle.dense_forward(quant(X, "bf16"), quant(W, "bf16"), quant(b, "bf16"), act,
                                        0.75)
-            err = rel_l2(to_np(H), ref)
-            assert err <= (EXACT if out_dtype == "f32" else TOL["bf16"] / 2), (act, out_dtype, err)
+            if out_dtype == "f32":
+                assert_close(to_np(H), ref, EXACT, (act, out_dtype), row_tol=ROW_EXACT)
+            else:
+                assert_close(to_np(H), ref, TOL["bf16"] / 2, (act, out_dtype), row_tol=TOL["bf16"])
 
 
 @pytest.mark.parametrize("shape", SHAPES)
@@ -84,9 +87,11 @@ def test_async_backward_data(cfg, shape):
                                to_dev(Hprev, "bf16"), to_dev(R, "f32"), dX)
         torch.cuda.synchronize()
         ref = oracle.dense_vjp_input(quant(u, "f32"), quant(W, "bf16"), quant(dY, "bf16"), act) + R
-        err = rel_l2(to_np(dX), ref)
         # relu' taken from the bf16-rounded output is exact; sigmoid' is not.
-        assert err <= (EXACT if act != "sigmoid" else TOL["bf16"]), (act, err)
+        if act != "sigmoid":
+            assert_close(to_np(dX), ref, EXACT, act, row_tol=ROW_EXACT)
+        else:
+            assert_close(to_np(dX), ref, TOL["bf16"], act)
 
 
 @pytest.mark.parametrize("shape", SHAPES)
@@ -102,8 +107,8 @@ def test_async_backward_params(cfg, shape):
     dl.dense_backward_params("bf16", M, N, K, to_dev(X, "bf16"), to_dev(dY, "bf16"), dW, db)
     torch.cuda.synchronize()
     rdW, rdb = oracle.dense_vjp_params(quant(X, "bf16"), quant(dY, "bf16"))
-    assert rel_l2(to_np(dW), rdW) <= EXACT
-    assert rel_l2(to_np(db), rdb) <= EXACT
+    assert_close(to_np(dW), rdW, EXACT, "dW", row_tol=ROW_EXACT)
+    assert_close(to_np(db), rdb, EXACT, "db", row_tol=ROW_EXACT)
 
 
 def test_async_model_gradient(cfg):
@@ -128,6 +133,6 @@ def test_async_model_gradient(cfg):
     spec = oracle.MlpSpec(wl.widths, wl.acts, wl.loss, wl.dtype)
     rl, rg, _ = oracle.mlp_gradient(spec, x, params, y)
     assert abs(loss.item() - rl) <= TOL["bf16"] * abs(rl)
-    for (gw, gb), (rw, rb) in zip(m.unpack(dP), rg):
-        assert rel_l2(to_np(gw), rw) <= TOL["bf16"]
-        assert rel_l2(to_np(gb), rb) <= TOL["bf16"]
+    for l, ((gw, gb), (rw, rb)) in enumerate(zip(m.unpack(dP), rg)):
+        assert_close(to_np(gw), rw, TOL["bf16"], ("dW", l))
+        assert_close(to_np(gb), rb, TOL["bf16"], ("db", l))

@@ -13,7 +13,7 @@ import pytest
 import oracle
 import paper_1711_03016_amd as dl
 import workloads
-from helpers import TOL, device, rel_l2, to_dev, to_np, torch_dtype
+from helpers import TOL, assert_close, device, rel_l2, to_dev, to_np, torch_dtype
 
 pytestmark = pytest.mark.gpu
 
@@ -55,6 +55,10 @@ def _spec(wl):
 def _order_tolerances(wl, x, params, y, ref_grads):
     """Per-layer bounds for bf16 networks: max(2e-2, 2 x the oracle's own spread).
 
+    A secondary, end-to-end check: for the deep network these bounds are
+    wider than the stated 2e-2 (0.07-0.11 at batch 64). The stated bound is
+    applied product by product, row by row, in test_gpu_c5_layers.py.
+
     The spread is the distance between the oracle's float64-accumulate and
     float32-accumulate evaluations of the same bf16-storage network: the part
     of the gradient that the accumulation order does not determine (ReLU mask
@@ -71,19 +75,41 @@ def _order_tolerances(wl, x, params, y, ref_grads):
 
 
 def _compare(wl, got, ref_loss, ref_grads, ref_dx=None, ref_out=None, tol=None,
-             layer_tols=None):
+             layer_tols=None, rows=True):
+    """Loss, every dW and db, dx and the forward output against the oracle.
+
+    With `rows` every row of a matrix (every element of a vector, against
+    the vector's root-mean-square) is held to the same bound as the whole
+    tensor, so one wrong row fails. The end-to-end gradients of the deep bf16
+    network pass rows=False: their per-layer bounds are widened for the
+    accumulation-order ambiguity of the function itself, and its products are
+    checked row by row one at a time instead (test_gpu_c5_layers.py). For bf16
+    networks dx is checked as a whole tensor only: a row of dx whose path
+    crosses a bf16 rounding boundary differs between two valid evaluation
+    orders of the oracle itself by several percent (c3: 8e-2).
+    """
     tol = TOL[wl.dtype] if tol is None else tol
     assert got["status"] == dl.OK
     assert abs(got["loss"] - ref_loss) <= tol * abs(ref_loss), (got["loss"], ref_loss)
     for l, ((gw, gb), (rw, rb)) in enumerate(zip(got["grads"], ref_grads)):
         tw, tb = (tol, tol) if layer_tols is None else layer_tols[l]
-        ew, eb = rel_l2(gw, rw), rel_l2(gb, rb)
-        assert ew <= tw, (l, "dW", ew, tw)
-        assert eb <= tb, (l, "db", eb, tb)
+        if rows:
+            assert_close(gw, rw, tw, ("dW", l))
+            assert_close(gb, rb, tb, ("db", l))
+        else:
+            ew, eb = rel_l2(gw, rw), rel_l2(gb, rb)
+            assert ew <= tw, (l, "dW", ew, tw)
+            assert eb <= tb, (l, "db", eb, tb)
     if ref_dx is not None:
-        assert rel_l2(got["dx"], ref_dx) <= tol
+        if rows and wl.dtype == "f32":
+            assert_close(got["dx"], ref_dx, tol, "dx")
+        else:
+            assert rel_l2(got["dx"], ref_dx) <= tol
     if ref_out is not None:
-        assert rel_l2(got["forward"], ref_out) <= tol
+        if rows:
+            assert_close(got["forward"], ref_out, tol, "forward")
+        else:
+            assert rel_l2(got["forward"], ref_out) <= tol
 
 
 @pytest.mark.parametrize("name", ["c1", "c2", "c3"])
@@ -183,6 +209,34 @@ def test_label_out_of_range_is_reported(name, bad):
     assert good["status"] == dl.OK
 
 
+@pytest.mark.parametrize("name", ["c2", "c3"])
+def test_loss_adjoint_labels_are_exact(name):
+    """The adjoint of the logits that a full-batch gradient call stores in its
+    workspace, (softmax - onehot(y)) / B, read back through
+    dlvm_workspace_tensor. The heads of c2 (float32) and c3 (bf16) have ten
+    classes: their product is split over k and the loss kernel sums its
+    slices, so this checks that kernel's label handling bit for bit: every
+    row has exactly one negative entry, at its label, and the padding columns
+    (10 -> 16) are zero. The values match the oracle's adjoint of its own
+    logits."""
+    wl = workloads.WORKLOADS[name]
+    x, params, y = workloads.make_inputs(wl, bias_scale=0.1)
+    got = _run(wl, x, params, y, forward=False)
+    m, ws, B, C = got["model"], got["ws"], wl.batch, wl.widths[-1]
+    assert any(e["name"] == "split_softmax_xent" for e in m.plan(B))
+    with pytest.raises(dl.DlvmError):          # the split head never stores its logits
+        m.workspace_tensor(ws, B, dl.WS_LOGITS)
+    dz = to_np(m.workspace_tensor(ws, B, dl.WS_ADJOINT, m.n_layers))
+    assert dz.shape == (B, 16)
+    assert (dz[:, C:] == 0).all()
+    neg = dz[:, :C] < 0
+    assert (neg.sum(axis=1) == 1).all()
+    np.testing.assert_array_equal(np.argmax(neg, axis=1), y)
+    _, logits = oracle.mlp_forward(_spec(wl), x, params, y)
+    _, rdz = oracle.softmax_xent(logits, y)
+    assert_close(dz[:, :C], rdz, TOL[wl.dtype], "dZ_L")
+
+
 def test_non_default_stream():
     import torch
     wl = workloads.WORKLOADS["c2"]
@@ -232,7 +286,8 @@ def test_c5_reduced_batch():
     got = _run(wl, x, params, y)
     rl, rg, _ = oracle.mlp_gradient(_spec(wl), x, params, y)
     _, rout = oracle.mlp_forward(_spec(wl), x, params, y)
-    _compare(wl, got, rl, rg, None, rout, layer_tols=_order_tolerances(wl, x, params, y, rg))
+    _compare(wl, got, rl, rg, None, rout, layer_tols=_order_tolerances(wl, x, params, y, rg),
+             rows=False)
 
 
 def test_c5_full_batch_repeated_rows_and_sgd():
@@ -245,7 +300,7 @@ def test_c5_full_batch_repeated_rows_and_sgd():
     rl, rg, _ = oracle.mlp_gradient(_spec(wl), xb, params, yb)
     _, rout = oracle.mlp_forward(_spec(wl), xb, params, yb)
     _compare(wl, got, rl, rg, None, rout[idx],
-             layer_tols=_order_tolerances(wl, xb, params, yb, rg))
+             layer_tols=_order_tolerances(wl, xb, params, yb, rg), rows=False)
     # the fused update over the whole 138M-parameter buffer: master and bf16 shadow
     m, P = got["model"], got["P"]
     master = m.pack(params, device(), torch.float32)

@@ -8,7 +8,7 @@ import pytest
 
 import oracle
 import paper_1711_03016_amd as dl
-from helpers import TOL, device, quant, rel_l2, to_dev, to_np
+from helpers import TOL, assert_close, device, quant, rel_l2, to_dev, to_np
 
 pytestmark = pytest.mark.gpu
 
@@ -43,8 +43,7 @@ def test_dense_forward(dtype, out_dtype, shape):
                          to_dev(b, dtype), H)
         _sync()
         ref = oracle.dense_forward(quant(X, dtype), quant(W, dtype), quant(b, dtype), act, 0.75)
-        err = rel_l2(to_np(H), ref)
-        assert err <= TOL[dtype], (act, err)
+        assert_close(to_np(H), ref, TOL[dtype], act)
 
 
 @pytest.mark.parametrize("dtype,out_dtype", [("f32", "f32"), ("bf16", "bf16"), ("bf16", "f32")])
@@ -71,8 +70,7 @@ def test_dense_backward_data(dtype, out_dtype, shape):
             ref = oracle.dense_vjp_input(quant(u, "f32"), quant(W, dtype), quant(dY, dtype), act)
             if use_r:
                 ref = ref + (quant(R, out_dtype) if out_dtype == "bf16" else R)
-            err = rel_l2(to_np(dX), ref)
-            assert err <= TOL[dtype], (act, use_r, err)
+            assert_close(to_np(dX), ref, TOL[dtype], (act, use_r))
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
@@ -91,8 +89,8 @@ def test_dense_backward_params(dtype, shape):
     dl.dense_backward_params(dtype, M, N, K, to_dev(X, dtype), to_dev(dY, dtype), dW, db)
     _sync()
     rdW, rdb = oracle.dense_vjp_params(quant(X, dtype), quant(dY, dtype))
-    assert rel_l2(to_np(dW), rdW) <= TOL[dtype] / 10
-    assert rel_l2(to_np(db), rdb) <= TOL[dtype] / 10
+    assert_close(to_np(dW), rdW, TOL[dtype] / 10, "dW", row_tol=TOL[dtype])
+    assert_close(to_np(db), rdb, TOL[dtype] / 10, "db", row_tol=TOL[dtype])
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
@@ -113,7 +111,7 @@ def test_softmax_xent(dtype, rows, classes):
     rl, rdz = oracle.softmax_xent(z.astype(np.float64), y)
     assert abs(loss.item() - rl) <= 1e-5 * abs(rl)
     got = to_np(dz)
-    assert rel_l2(got, rdz) <= TOL[dtype]
+    assert_close(got, rdz, TOL[dtype], "dlogits")
     # labels are handled exactly: the one negative entry of each row is at its label
     neg = got < 0
     assert (neg.sum(axis=1) == 1).all()
@@ -159,8 +157,8 @@ def test_chain8(rows, cols):
     rl, rdz, _, rdx, _ = oracle.chain8(z.astype(np.float64), b.astype(np.float64),
                                        xs.astype(np.float64))
     assert abs(loss.item() - rl) <= 1e-5 * rl
-    assert rel_l2(to_np(zb), rdz) <= TOL["f32"]
-    assert rel_l2(to_np(xb), rdx) <= TOL["f32"]
+    assert_close(to_np(zb), rdz, TOL["f32"], "zbar")
+    assert_close(to_np(xb), rdx, TOL["f32"], "xbar")
 
 
 def test_chain8_full_size():
