@@ -421,6 +421,23 @@ dlvm_status dlvm_softmax_xent(int32_t dtype, int64_t rows, int64_t classes,
                               float scale, void* dlogits, float* loss, void* ws,
                               size_t ws_bytes, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * computation as dlvm_softmax_xent, with the loss partials and bad-label
+ * counts in a static device array of the library (2 MiB per GPU, held until
+ * the process ends) instead of a caller workspace. The first call on a device
+ * looks the array's address up (hipGetSymbolAddress); no call allocates or
+ * frees memory. rows in [1, 1048576] (DLVM_ERR_INVALID_ARG beyond, before
+ * anything is enqueued). `flags` (may be NULL) is an int32[2] device output:
+ * flags[0] = 1 if a label was outside [0, classes) (the loss is then NaN),
+ * flags[1] = 1 if the loss is not finite. loss and dlogits are bitwise those
+ * of dlvm_softmax_xent. Every call on a GPU uses that GPU's one array: calls
+ * that may run concurrently on one GPU (different streams or threads) race
+ * and must not overlap. */
+dlvm_status dlvm_softmax_xent_noalloc(int32_t dtype, int64_t rows, int64_t classes,
+                                      const float* logits, const int32_t* labels, float scale,
+                                      void* dlogits, float* loss, int32_t* flags, void* stream);
+
 /* The eight-operator element-wise chain, forward and adjoint fused in one
  * pass over float32 [rows, cols] tensors: a = tanh(z + b), s = sigmoid(0.5a + 1),
  * e = s * x_skip, loss = mean(e^2) (x^2 simplified to x*x, section 3.1.2);

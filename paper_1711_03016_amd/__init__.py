@@ -92,6 +92,7 @@ _SIGS = {
     "dlvm_dense_backward_params": (_I32, [_I32, _I64, _I64, _I64, _P, _P, _P, _P, _P]),
     "dlvm_softmax_xent_ws_bytes": (ctypes.c_size_t, [_I64]),
     "dlvm_softmax_xent": (_I32, [_I32, _I64, _I64, _P, _P, _F, _P, _P, _P, ctypes.c_size_t, _P]),
+    "dlvm_softmax_xent_noalloc": (_I32, [_I32, _I64, _I64, _P, _P, _F, _P, _P, _P, _P]),
     "dlvm_chain8_ws_bytes": (ctypes.c_size_t, [_I64, _I64]),
     "dlvm_chain8": (_I32, [_I64, _I64, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "dlvm_sgd": (_I32, [_I32, _I64, _P, _P, _P, _F, _P]),
@@ -419,6 +420,14 @@ def softmax_xent(dtype, rows, classes, logits, labels, scale, dlogits, loss, ws,
     _check(lib().dlvm_softmax_xent(DTYPES[dtype], rows, classes, _ptr(logits), _ptr(labels),
                                    float(scale), _ptr(dlogits), _ptr(loss), _ptr(ws),
                                    ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def softmax_xent_noalloc(dtype, rows, classes, logits, labels, scale, dlogits, loss, flags=None,
+                         stream=None):
+    """dlvm_softmax_xent without a workspace (the library's static scratch)."""
+    _check(lib().dlvm_softmax_xent_noalloc(DTYPES[dtype], rows, classes, _ptr(logits),
+                                           _ptr(labels), float(scale), _ptr(dlogits), _ptr(loss),
+                                           _ptr(flags), _stream(stream)))
 
 
 def chain8_ws_bytes(rows: int, cols: int) -> int:

@@ -15,6 +15,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -1773,6 +1774,72 @@ dlvm_status dlvm_softmax_xent(int32_t dtype, int64_t rows, int64_t classes, cons
   float* partials = at<float>(ws, align_up(16));
   int32_t* bad = at<int32_t>(ws, align_up(16) +
                                      align_up(static_cast<size_t>(dlvm::softmax_xent_partials(rows)) * 4));
+  int np = 0;
+  hipError_t e = dlvm::launch_softmax_xent(dtype, rows, classes, logits, labels, scale, dlogits,
+                                           classes, partials, bad, &np, s);
+  if (e != hipSuccess) return hip_fail(e, "softmax cross-entropy launch");
+  dlvm::ZeroGaps none{};
+  e = dlvm::launch_finalize(partials, bad, np, scale, loss, flags, nullptr, none, s);
+  if (e != hipSuccess) return hip_fail(e, "loss finalisation launch");
+  return DLVM_OK;
+}
+
+}  // extern "C"
+
+// Scratch of the allocation-free softmax cross-entropy: the per-block loss
+// partials and bad-label counts of at most kNoAllocMaxRows rows (2 MiB), in a
+// device array each GPU holds for the life of the process. In host code the
+// array's name is only a stand-in: its device address on the current device
+// comes from hipGetSymbolAddress, looked up once per device and kept.
+constexpr int64_t kNoAllocMaxRows = int64_t(1) << 20;
+constexpr int64_t kNoAllocPartials = (kNoAllocMaxRows + 3) / 4;  // >= softmax_xent_partials(max)
+static __device__ __align__(256) float scratch[2 * kNoAllocPartials];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+float* g_scratch[kMaxDevices] = {};
+
+dlvm_status scratch_on_current_device(float** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices) return fail(DLVM_ERR_UNSUPPORTED, "device index out of range");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch[dev] == nullptr) {
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || ptr == nullptr) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    g_scratch[dev] = static_cast<float*>(ptr);
+  }
+  *out = g_scratch[dev];
+  return DLVM_OK;
+}
+}  // namespace
+
+extern "C" {
+
+dlvm_status dlvm_softmax_xent_noalloc(int32_t dtype, int64_t rows, int64_t classes,
+                                      const float* logits, const int32_t* labels, float scale,
+                                      void* dlogits, float* loss, int32_t* flags, void* stream) {
+  if (!valid_dtype(dtype)) return fail(DLVM_ERR_INVALID_ARG, "bad dtype");
+  if (rows < 1 || classes < 1) return fail(DLVM_ERR_INVALID_ARG, "sizes must be positive");
+  if (rows > kNoAllocMaxRows)
+    return fail(DLVM_ERR_INVALID_ARG,
+                "rows exceed the 1048576 that the static scratch of dlvm_softmax_xent_noalloc holds");
+  if (logits == nullptr || labels == nullptr || dlogits == nullptr || loss == nullptr)
+    return fail(DLVM_ERR_INVALID_ARG, "null argument");
+  if (!aligned16(logits) || !aligned16(labels) || !aligned16(dlogits) || !aligned16(loss) ||
+      (flags != nullptr && !aligned16(flags)))
+    return fail(DLVM_ERR_MISALIGNED, "device pointers must be 16-byte aligned");
+  float* base = nullptr;
+  dlvm_status st = scratch_on_current_device(&base);
+  if (st != DLVM_OK) return st;
+  // every partial and count the finalisation reads is written by the loss
+  // launch just before it: nothing needs clearing between calls
+  float* partials = base;
+  int32_t* bad = reinterpret_cast<int32_t*>(base + kNoAllocPartials);
+  hipStream_t s = static_cast<hipStream_t>(stream);
   int np = 0;
   hipError_t e = dlvm::launch_softmax_xent(dtype, rows, classes, logits, labels, scale, dlogits,
                                            classes, partials, bad, &np, s);

@@ -246,6 +246,14 @@ def test_step_level_errors_are_host_side():
     assert L.dlvm_sgd(1, 16, A, None, A, 0.1, None) == dl.ERR_INVALID_ARG
     assert L.dlvm_softmax_xent_ws_bytes(0) == 0 and L.dlvm_softmax_xent_ws_bytes(5) > 0
     assert L.dlvm_chain8_ws_bytes(3, 0) == 0 and L.dlvm_chain8_ws_bytes(3, 5) > 0
+    # the allocation-free loss refuses rows beyond its static scratch, and bad
+    # arguments, before touching the device
+    nf = L.dlvm_softmax_xent_noalloc
+    assert nf(0, (1 << 20) + 1, 10, A, A, 1.0, A, A, None, None) == dl.ERR_INVALID_ARG
+    assert b"1048576" in L.dlvm_last_error()
+    assert nf(0, 4, 10, A, A, 1.0, A, None, None, None) == dl.ERR_INVALID_ARG
+    assert nf(2, 4, 10, A, A, 1.0, A, A, None, None) == dl.ERR_INVALID_ARG
+    assert nf(0, 4, 10, A, A, 1.0, A, A, A + 4, None) == dl.ERR_MISALIGNED
 
 
 def test_probe_arguments_are_validated():
