@@ -52,7 +52,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=None)
     ap.add_argument("--workload", default="c5",
                     choices=sorted(workloads.WORKLOADS) + sorted(workloads.RNN_WORKLOADS) +
-                    sorted(workloads.CHAIN_WORKLOADS))
+                    sorted(workloads.CHAIN_WORKLOADS) + ["ce5"])
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="budget of the oracle CPU baseline (0 disables it)")
     ap.add_argument("--entry", default="gradient", choices=["gradient", "vjp"],
@@ -557,6 +557,66 @@ def chain_cpu_baseline(wl, budget_s: float) -> dict | None:
                       f"{wl.dims[0]} rows of A_0 in {el:.1f} s, scaled by {wl.dims[0]}/{rows}"}
 
 
+def ce_main(args) -> None:
+    """The loss step of the deep bf16 network on its own: softmax
+    cross-entropy of 16384 x 1000 float32 logits with bf16 dlogits and the
+    loss (dlvm_softmax_xent: the loss kernel, then the one-block loss
+    finalisation). Its algorithmic bytes, 98,369,536 per call (logits read,
+    dlogits written, labels read), fit the 256 MB Infinity Cache, so the calls
+    rotate over 8 sets of logits and dlogits (786 MB together): each call
+    reads logits that the previous 7 calls have pushed out of the cache, and
+    the rate is that of HBM. The same calls on one resident set are timed
+    beside it."""
+    import torch
+
+    import paper_1711_03016_amd as dl
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    rows, C, R = 16384, 1000, 8
+    g = torch.Generator(device="cpu").manual_seed(5)
+    logits = [(torch.randn((rows, C), generator=g) * 3).to(dev) for _ in range(R)]
+    labels = torch.randint(0, C, (rows,), generator=g, dtype=torch.int32).to(dev)
+    dz = [torch.empty((rows, C), dtype=torch.bfloat16, device=dev) for _ in range(R)]
+    ws = torch.zeros(dl.softmax_xent_ws_bytes(rows), dtype=torch.uint8, device=dev)
+    loss = torch.empty(1, device=dev)
+    steps = args.steps if args.steps is not None else 200
+    warmup = args.warmup if args.warmup is not None else 16
+    nbytes = rows * C * (4 + 2) + rows * 4
+
+    def run(n, rotate):
+        for i in range(n):
+            k = i % R if rotate else 0
+            dl.softmax_xent("bf16", rows, C, logits[k], labels, 1.0 / rows, dz[k], loss, ws)
+
+    out = {}
+    for rotate in (True, False):
+        run(warmup, rotate)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        run(steps, rotate)
+        e1.record()
+        torch.cuda.synchronize()
+        out[rotate] = e0.elapsed_time(e1) / steps / 1e3
+    t = out[True]
+    achieved = nbytes / t / 1e9
+    print(json.dumps({
+        "metric": "fused softmax cross-entropy GB/s (logits from HBM)", "value": round(achieved, 1),
+        "unit": "GB/s", "n_gpus": 1, "steps": steps, "warmup": warmup,
+        "ms_per_step": round(t * 1e3, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": "ce5: softmax cross-entropy of 16384 x 1000 float32 logits, bf16 "
+                               "dlogits, 8 rotated buffers", "rows": rows, "classes": C},
+        "bytes_per_call": nbytes,
+        "resident_ms_per_call": round(out[False] * 1e3, 4),
+        "resident_gbs": round(nbytes / out[False] / 1e9, 1),
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
+                     "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None,
+                     "kernel": "softmax_xent call (loss kernel + one-block finalisation), "
+                               "rotated buffers"}}), flush=True)
+
+
 def main():
     args = parse()
     if args.copy_calibration:
@@ -566,6 +626,8 @@ def main():
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the workloads "
               "here are single-GPU and no multi-GPU path is built", file=sys.stderr)
         sys.exit(2)
+    if args.workload == "ce5":
+        return ce_main(args)
     if args.workload in workloads.RNN_WORKLOADS:
         return rnn_main(args, workloads.RNN_WORKLOADS[args.workload])
     if args.workload in workloads.CHAIN_WORKLOADS:
