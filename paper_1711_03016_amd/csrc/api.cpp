@@ -111,6 +111,8 @@ struct WsLayout {
                             // [B, ldw[l]] (storage dtype; float32 for the chain)
   size_t splitk = 0;        // float32 partials of a split adjoint product wrt the weights
   int64_t splitk_elems = 0;
+  std::vector<size_t> mask; // mask[l], l = 1 .. L-1: rectifier mask of H_l (0: none; see
+                            // relu_mask_planned), after every other region
   size_t total = 0;
 };
 
@@ -133,6 +135,9 @@ int head_splits(const dlvm_model* m, int64_t B) {
   while (s < 8 && K / (2 * s) >= 64 && tiles * 2 * s <= 256) s *= 2;
   return s;
 }
+
+bool relu_mask_planned(const dlvm_model* m, const void* params, const void* x, int64_t batch,
+                       void* ws, const WsLayout& w, int l);
 
 WsLayout ws_layout(const dlvm_model* m, int64_t B) {
   WsLayout w;
@@ -197,6 +202,14 @@ WsLayout ws_layout(const dlvm_model* m, int64_t B) {
   }
   w.splitk = off;
   off = align_up(off + static_cast<size_t>(w.splitk_elems) * 4);
+  // Rectifier masks, where the products' shapes allow them (the pointers of
+  // a call decide again, with the same rule, whether they are used).
+  w.mask.assign(m->L, 0);
+  for (int l = 1; l < m->L; ++l) {
+    if (!relu_mask_planned(m, nullptr, nullptr, B, nullptr, w, l)) continue;
+    w.mask[l] = off;
+    off = align_up(off + static_cast<size_t>(dlvm::mask_bytes(B, m->widths[l])));
+  }
   w.total = off;
   return w;
 }
@@ -289,7 +302,8 @@ LaunchInfo gemm_info(const GemmDesc& d) {
   const double es = double(elem_size(d.dtype)), eo = double(elem_size(d.out_dtype));
   double b = (M * K + K * N) * es + M * N * eo;
   if (d.bias) b += N * es;
-  if (d.layout == Layout::NT && d.act != DLVM_ACT_NONE) b += M * N * es;
+  if (d.layout == Layout::NT && d.act != DLVM_ACT_NONE) b += d.mask ? M * N / 8.0 : M * N * es;
+  if (d.layout == Layout::NN && d.mask) b += M * N / 8.0;  // the rectifier mask written
   if (d.residual) b += M * N * eo;
   if (d.colsum) b += N * 4.0;
   i.bytes = b;
@@ -451,11 +465,55 @@ GemmDesc hidden_desc(const dlvm_model* m, const void* params, const void* in, in
   return d;
 }
 
+// The product wrt the input of layer l >= 1 (dX = dZ_l . W_l^T times the
+// derivative of layer l - 1's activation, from H_l), into dz[l - 1].
+GemmDesc input_adjoint_desc(const dlvm_model* m, const void* params, int64_t batch, void* ws,
+                            const WsLayout& w, int l) {
+  const int64_t K = m->widths[l], N = m->widths[l + 1], Np = m->ldw[l];
+  GemmDesc d = gemm_nt(m->dtype, m->dtype, m->acts[l - 1], batch, Np, K, at<void>(ws, w.dz[l]), Np,
+                       param_ptr(m, params, m->offsets[2 * l]), Np, at<void>(ws, w.H[l]), nullptr,
+                       at<void>(ws, w.dz[l - 1]));
+  d.kvalid = N;
+  return d;
+}
+
+// Rectifier masks (section 3.1.3: the adjoint of the rectifier needs only the
+// sign of its saved output). Layer output H_l (1 <= l < L) of a bf16 network
+// whose layer l - 1 is rectified: when the forward product that writes H_l and
+// the product wrt the input of layer l, whose epilogue applies the
+// derivative, both pass dlvm::mask_ok as they will be launched, the forward
+// also writes the derivative's bits in accumulator order and the adjoint reads
+// them instead of H_l (one bit per element instead of two bytes). Both sides
+// ask this function with the same arguments, so they agree.
+// DLVM_RELU_MASK=0 turns the masks off (tests compare the two paths).
+bool relu_mask_planned(const dlvm_model* m, const void* params, const void* x, int64_t batch,
+                       void* ws, const WsLayout& w, int l) {
+  const char* env = std::getenv("DLVM_RELU_MASK");
+  if (env != nullptr && std::strcmp(env, "0") == 0) return false;
+  if (m->kind != 0 || m->loss == DLVM_LOSS_CHAIN8 || m->dtype != DLVM_BF16) return false;
+  if (l < 1 || l >= m->L || m->acts[l - 1] != DLVM_ACT_RELU) return false;
+  const void* in = l == 1 ? x : at<void>(ws, w.H[l - 1]);
+  const GemmDesc f = hidden_desc(m, params, in, batch, at<void>(ws, w.H[l]),
+                                 at<float>(ws, w.splitk), w.splitk_elems, l - 1);
+  const GemmDesc a = input_adjoint_desc(m, params, batch, ws, w, l);
+  return dlvm::mask_ok(f, dlvm::plan_gemm(f)) && dlvm::mask_ok(a, dlvm::plan_gemm(a));
+}
+
+// The rectifier mask of H_l a call uses, or null.
+uint32_t* relu_mask(const dlvm_model* m, const void* params, const void* x, int64_t batch,
+                    void* ws, const WsLayout& w, int l) {
+  if (l < 1 || l >= static_cast<int>(w.mask.size()) || w.mask[l] == 0) return nullptr;
+  if (!relu_mask_planned(m, params, x, batch, ws, w, l)) return nullptr;
+  return at<uint32_t>(ws, w.mask[l]);
+}
+
 dlvm_status plan_hidden_layer(const dlvm_model* m, const void* params, const void* x,
                               int64_t batch, void* ws, const WsLayout& w, int l, Launcher& run) {
   const void* in = l == 0 ? x : at<void>(ws, w.H[l]);
-  return run.gemm(hidden_desc(m, params, in, batch, at<void>(ws, w.H[l + 1]),
-                              at<float>(ws, w.splitk), w.splitk_elems, l));
+  GemmDesc d = hidden_desc(m, params, in, batch, at<void>(ws, w.H[l + 1]),
+                           at<float>(ws, w.splitk), w.splitk_elems, l);
+  d.mask = relu_mask(m, params, x, batch, ws, w, l + 1);
+  return run.gemm(d);
 }
 
 // The hidden layers' forward (H_1 .. H_{L-1}, each written where it lives).
@@ -508,9 +566,8 @@ dlvm_status plan_adjoint_layers(const dlvm_model* m, const void* params, const v
     // The product wrt the input (dead for the first layer unless x is
     // differentiated) reads the same adjoint: the two share one launch.
     if (l > 0) {
-      GemmDesc d = gemm_nt(dt, dt, m->acts[l - 1], batch, Np, K, dzl, Np, P(2 * l), Np,
-                           at<void>(ws, w.H[l]), nullptr, at<void>(ws, w.dz[l - 1]));
-      d.kvalid = N;
+      GemmDesc d = input_adjoint_desc(m, params, batch, ws, w, l);
+      d.mask = relu_mask(m, params, x, batch, ws, w, l);
       if ((st = run.gemm_pair(dw, d)) != DLVM_OK) return st;
     } else if (m->wrt_x) {
       GemmDesc d = gemm_nt(dt, DLVM_F32, DLVM_ACT_NONE, batch, Np, K, dzl, Np, P(0), Np, nullptr,

@@ -19,12 +19,14 @@ __device__ __forceinline__ float bf16_to_f32(bf16_t h) {
   return __uint_as_float(static_cast<uint32_t>(h) << 16);
 }
 
-// float32 -> bfloat16, round to nearest, ties to even; NaN stays a quiet NaN.
+// float32 -> bfloat16, round to nearest, ties to even, by gfx950's conversion
+// instruction (v_cvt_pk_bf16_f32; two values per instruction where the
+// compiler pairs them). Compared on the device over all 2^32 float32 bit
+// patterns with the integer rounding u + 0x7fff + ((u >> 16) & 1) >> 16: equal
+// for every non-NaN input (denormals, infinities and signed zeros included);
+// a NaN stays a NaN.
 __device__ __forceinline__ bf16_t f32_to_bf16(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<bf16_t>(0x7fc0u);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return static_cast<bf16_t>(u >> 16);
+  return __builtin_bit_cast(bf16_t, static_cast<__bf16>(f));
 }
 
 // Streaming 16-byte and 8-byte accesses that bypass cache retention

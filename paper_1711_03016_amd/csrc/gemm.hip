@@ -276,6 +276,14 @@ GemmPlan plan_gemm(const GemmDesc& d) {
                 forced_splits());
 }
 
+bool mask_ok(const GemmDesc& d, const GemmPlan& pl) {
+  if (d.dtype != BF16 || d.out_dtype != BF16 || d.act != ACT_RELU) return false;
+  if (pl.cfg != 10 || pl.splits != 1 || d.A2 != nullptr || d.chain_epilogue) return false;
+  return d.layout == Layout::NN || (d.layout == Layout::NT && d.residual == nullptr);
+}
+
+int64_t mask_bytes(int64_t M, int64_t N) { return ceil_div(M, 256) * ceil_div(N, 256) * 8192; }
+
 int64_t split_ws_elems(const GemmDesc& d) {
   if (d.layout != Layout::TN && !d.split_epilogue) return 0;
   const GemmPlan pl = choose(d, true, int64_t(1) << 40, forced_config(), forced_splits());
@@ -324,6 +332,7 @@ gemm::Params make_params(const GemmDesc& d, const GemmPlan& pl) {
   p.C2 = d.chain_epilogue ? d.C2 : nullptr;
   p.partials = d.chain_epilogue ? d.partials : nullptr;
   p.inv_n = d.inv_n;
+  p.mask = d.mask;
   if (pl.splits > 1) {
     p.C = d.split_ws;                  // partial products, then partial column sums
     p.c_split = d.M * d.ldc;
@@ -358,6 +367,7 @@ unsigned grid_of(const GemmPlan& pl) {
 hipError_t launch_gemm(const GemmDesc& d, const GemmPlan& pl, hipStream_t s) {
   bool va, vb;
   vector_ok(d, va, vb);
+  if (d.mask != nullptr && (!mask_ok(d, pl) || !aligned16(d.mask))) return hipErrorInvalidValue;
   const gemm::Params p = make_params(d, pl);
   const unsigned grid = grid_of(pl);
   const int out = pl.splits > 1 ? F32 : d.out_dtype;  // split slices: float32 partials
@@ -383,6 +393,8 @@ bool pairable(const GemmDesc& tn, const GemmPlan& ptn, const GemmDesc& nt, const
 
 hipError_t launch_gemm_pair(const GemmDesc& tn, const GemmPlan& ptn, const GemmDesc& nt,
                             const GemmPlan& pnt, hipStream_t s) {
+  if (tn.mask != nullptr) return hipErrorInvalidValue;
+  if (nt.mask != nullptr && (!mask_ok(nt, pnt) || !aligned16(nt.mask))) return hipErrorInvalidValue;
   const gemm::Params p1 = make_params(tn, ptn), p2 = make_params(nt, pnt);
   const unsigned n1 = grid_of(ptn);
   return gemm::launch_pair(p1, p2, static_cast<int>(n1), n1 + grid_of(pnt), tn.dtype,

@@ -30,6 +30,8 @@
 // * Tile order: tile_of (gemm_kernel.hpp), XCD-aware.
 #pragma once
 
+#include <type_traits>
+
 #include "common.hpp"
 #include "kernels.hpp"
 #include "gemm_kernel.hpp"
@@ -264,6 +266,67 @@ __device__ __forceinline__ void store8(float* p, const float (&v)[8]) {
   *reinterpret_cast<float4*>(p + 4) = make_float4(v[4], v[5], v[6], v[7]);
 }
 
+// Rectifier masks (Params::mask; the host sets one only with the rectifier,
+// which these two functions assume). The forward product of a rectified layer
+// stores its 32 x 32 blocks as store_block does and keeps, per element, the
+// bit (stored output > 0), which is the rectifier's derivative taken from the
+// saved output; the adjoint product of the next layer has the same tile and
+// wave decomposition of the same output shape, so lane t of its workgroup
+// holds the same elements and reads its 128 bits as one 16-byte word instead
+// of 256 bytes of saved activation through LDS.
+__device__ __forceinline__ uint32_t store_block_bits(const Params& p, const f32x16& acc,
+                                                     int64_t r0, int64_t c0, int lane) {
+  const int64_t col = c0 + (lane & 31);
+  const int64_t rb = r0 + 4 * (lane >> 5);
+  const bool full = r0 + 32 <= p.M && c0 + 32 <= p.N;
+  const int ld = static_cast<int>(p.ldc);
+  float bias_v = 0.0f;
+  if (p.bias != nullptr && col < p.nvec) bias_v = bf16_to_f32(static_cast<const bf16_t*>(p.bias)[col]);
+  bf16_t* __restrict__ C = static_cast<bf16_t*>(p.C) + rb * p.ldc + col;
+  uint32_t bits = 0;
+  auto one = [&](int r) {
+    const int ro = 8 * (r >> 2) + (r & 3);
+    const float z = p.alpha * acc[r] + bias_v;
+    const bf16_t o = f32_to_bf16(z > 0.0f ? z : 0.0f);  // apply_act(ACT_RELU, z)
+    C[ro * ld] = o;
+    bits |= (bf16_to_f32(o) > 0.0f ? 1u : 0u) << r;  // act_grad_from_output(ACT_RELU, o) > 0
+  };
+  if (full) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) one(r);
+  } else if (col < p.N) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r)
+      if (rb + 8 * (r >> 2) + (r & 3) < p.M) one(r);
+  }
+  return bits;
+}
+
+// The adjoint's store of one block with the rectifier's derivative from the
+// block's 16 mask bits: the same arithmetic as the saved-activation path
+// without a residual (product times derivative, plus a zero residual).
+template <typename TO>
+__device__ __forceinline__ void store_block_masked(const Params& p, const f32x16& acc, int64_t r0,
+                                                   int64_t c0, int lane, uint32_t bits) {
+  const int64_t col = c0 + (lane & 31);
+  const int64_t rb = r0 + 4 * (lane >> 5);
+  const bool full = r0 + 32 <= p.M && c0 + 32 <= p.N;
+  const int ld = static_cast<int>(p.ldc);
+  TO* __restrict__ C = static_cast<TO*>(p.C) + rb * p.ldc + col;
+  auto one = [&](int r) {
+    const float d = ((bits >> r) & 1u) ? 1.0f : 0.0f;
+    C[(8 * (r >> 2) + (r & 3)) * ld] = store_cast<TO>(acc[r] * d + 0.0f);
+  };
+  if (full) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) one(r);
+  } else if (col < p.N) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r)
+      if (rb + 8 * (r >> 2) + (r & 3) < p.M) one(r);
+  }
+}
+
 // Epilogue of one row of a wave's 32 x 32 accumulator blocks (32 x WTN
 // outputs starting at (r0, c0)) through the wave's own LDS region: the
 // accumulators are written to LDS in row-major order, then every lane takes
@@ -426,6 +489,20 @@ __device__ __forceinline__ void async_gemm_tile(Params& p, const int tile, char*
   for (int j = 0; j < TN; ++j) cs[j] = 0.0f;
   const bool do_colsum = (EPI == EPI_DW) && (p.colsum != nullptr) && (tm == 0) && (wm == 0);
 
+  // Rectifier mask (256 x 256 tiles on 2 x 4 waves, one phase, bf16 output):
+  // the adjoint's 16-byte word is loaded before the contraction so that its
+  // latency hides behind it.
+  constexpr bool MASKABLE = BM == 256 && BN == 256 && WM == 2 && WN == 4 && !PH2 &&
+                            (EPI == EPI_DACT || (EPI == EPI_STORE && std::is_same<TO, bf16_t>::value));
+  uint32_t* const mask_word =
+      MASKABLE && p.mask != nullptr
+          ? p.mask + (static_cast<int64_t>(tm) * p.tiles_n + tn) * (4 * THREADS) + 4 * tid
+          : nullptr;
+  uint4 mk = make_uint4(0u, 0u, 0u, 0u);
+  if constexpr (MASKABLE && EPI == EPI_DACT) {
+    if (mask_word != nullptr) mk = *reinterpret_cast<const uint4*>(mask_word);
+  }
+
   auto issue = [&](int kt) {
     char* st = smem + (kt % STAGES) * STAGE;
     const StageSrc<bf16_t, BKM> q = stage_src<bf16_t, BKM, PH2>(p, A, B, kt, nk1, BK);
@@ -457,7 +534,25 @@ __device__ __forceinline__ void async_gemm_tile(Params& p, const int tile, char*
                                                                acc, cs, do_colsum);
   }
 
-  if constexpr (EPI == EPI_DACT) {
+  if (MASKABLE && mask_word != nullptr) {
+    if constexpr (MASKABLE) {
+      static_assert(TM * TN == 8, "128 mask bits per lane");
+      uint32_t w[4] = {mk.x, mk.y, mk.z, mk.w};
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+          const int q = i * TN + j;
+          const int64_t r0 = m0 + wm * WTM + i * 32, c0 = n0 + wn * WTN + j * 32;
+          if constexpr (EPI == EPI_DACT)
+            store_block_masked<TO>(p, acc[i][j], r0, c0, lane, (w[q >> 1] >> (16 * (q & 1))) & 0xffffu);
+          else
+            w[q >> 1] |= store_block_bits(p, acc[i][j], r0, c0, lane) << (16 * (q & 1));
+        }
+      if constexpr (EPI == EPI_STORE)
+        *reinterpret_cast<uint4*>(mask_word) = make_uint4(w[0], w[1], w[2], w[3]);
+    }
+  } else if constexpr (EPI == EPI_DACT) {
     // The adjoint epilogue reads the saved activation (and a residual): it
     // goes through a per-wave LDS region once every wave is done with the
     // ring, so those reads and the stores move 8 consecutive columns at a time.

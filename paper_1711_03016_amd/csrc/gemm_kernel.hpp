@@ -91,6 +91,13 @@ struct Params {
   void* C2;
   float* partials;
   float inv_n;
+  // Rectifier masks in accumulator order (direct-to-LDS kernel, 256 x 256
+  // tiles on 2 x 4 waves, unsplit; null: none). Tile (tm, tn) owns 512 x 4
+  // words from (tm * tiles_n + tn) * 2048; lane t of the workgroup owns words
+  // 4t .. 4t + 3, whose bit 16 q + r is element r of the lane's accumulator
+  // block q = i * 2 + j. EPI_STORE with the rectifier writes bit = (stored
+  // output > 0); EPI_DACT reads it in place of the saved activation.
+  uint32_t* mask;
 };
 
 // Source of pipeline stage kt (KSTAGE k per stage) of a two-phase

@@ -78,6 +78,10 @@ struct GemmDesc {
   void* C2;
   float* partials;
   float inv_n;
+  // bf16 rectified layers on the 256 x 256 direct-to-LDS tile, unsplit
+  // (mask_ok): an NN product writes the rectifier bits of its output here, an
+  // NT product reads them in place of aux. Null: none.
+  uint32_t* mask;
 };
 
 // How one product is launched: tile configuration and grid.
@@ -95,6 +99,14 @@ int64_t split_ws_elems(const GemmDesc& d);
 
 // Choose the launch of a product.
 GemmPlan plan_gemm(const GemmDesc& d);
+
+// Whether a product so planned can write (NN) or read (NT) rectifier masks
+// (GemmDesc::mask): bf16 operands and output, the rectifier, the 256 x 256
+// direct-to-LDS tile (configuration 10), one k-slice, one phase, no residual.
+// Both products of a layer output must pass for the mask to be used.
+bool mask_ok(const GemmDesc& d, const GemmPlan& plan);
+// Bytes of the mask of an M x N output (8 KiB per 256 x 256 tile).
+int64_t mask_bytes(int64_t M, int64_t N);
 
 // Between begin and end (nestable; one library call), the tuning variables
 // DLVM_GEMM_CONFIG / DLVM_GEMM_SPLITS are read once instead of per product.
