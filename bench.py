@@ -179,11 +179,13 @@ def cpu_baseline(wl, budget_s: float) -> dict | None:
     the BLAS on all its threads, then on one thread pinned to one core.
 
     A workload whose whole batch is cheap is timed at full size. Otherwise
-    the gradient is timed on r and 2r rows of the batch and its time fitted
-    as fixed + per_row * rows (the fixed part, e.g. rounding every parameter
-    to bf16, does not grow with the rows; every product does), evaluated at
-    the full batch (after one untimed call); the update is timed once as it
-    is (it does not depend on the rows)."""
+    the gradient is timed on a rows and on b = 4a, 16a, ... rows of the batch
+    (after one untimed call), b growing until the rows' share of the time is
+    at least half the time on a rows or the budget is spent, and the time is
+    fitted through the two as fixed + per_row * rows (the fixed part, e.g.
+    rounding every parameter to bf16, does not grow with the rows; every
+    product does) and evaluated at the full batch; the update is timed once
+    as it is (it does not depend on the rows)."""
     if budget_s <= 0:
         return None
     import oracle
@@ -209,29 +211,46 @@ def cpu_baseline(wl, budget_s: float) -> dict | None:
                     break
             return n / el, (f"{n} oracle steps (float64 gradient{' + SGD' if wl.sgd else ''}) "
                             f"on the whole batch of {wl.batch} rows in {el:.1f} s")
-        r = wl.batch
-        while r > 1 and wl.flops(2 * r) > cap_flops:
-            r //= 2
-        x, params, y = workloads.make_inputs(wl, batch=2 * r)
+        a = wl.batch
+        while a > 1 and wl.flops(2 * a) > cap_flops:
+            a //= 2
+        x, params, y = workloads.make_inputs(wl, batch=wl.batch)
+
+        def timed(rows):
+            t0 = time.perf_counter()
+            _, g, _ = oracle.mlp_gradient(spec, x[:rows], params, y[:rows], wrt_x=wl.wrt_x)
+            return time.perf_counter() - t0, g
+
         # one untimed call first: the first touch of the oracle's large
         # temporaries (every parameter in float64) costs several times a step
-        oracle.mlp_gradient(spec, x[:r], params, y[:r], wrt_x=wl.wrt_x)
-        t = []
-        for rows in (r, 2 * r):
-            t0 = time.perf_counter()
-            _, grads, _ = oracle.mlp_gradient(spec, x[:rows], params, y[:rows], wrt_x=wl.wrt_x)
-            t.append(time.perf_counter() - t0)
-        per_row = max((t[1] - t[0]) / r, 0.0)
-        fixed = max(t[0] - per_row * r, 0.0)
+        t0 = time.perf_counter()
+        timed(a)
+        spent = time.perf_counter() - t0
+        ta, grads = timed(a)
+        spent += ta
+        b, tb = a, ta
+        while 4 * b <= wl.batch:
+            nb = 4 * b
+            per_row_est = max((tb - ta) / (b - a), 0.0) if b > a else 0.0
+            est = ta + (nb - a) * per_row_est
+            if b > a and spent + est > budget:
+                break
+            b = nb
+            tb, grads = timed(b)
+            spent += tb
+            if tb - ta >= 0.5 * ta:
+                break
+        per_row = max((tb - ta) / (b - a), 0.0) if b > a else 0.0
+        fixed = max(ta - per_row * a, 0.0)
         t_sgd = 0.0
         if wl.sgd:
             t0 = time.perf_counter()
             update(params, grads)
             t_sgd = time.perf_counter() - t0
         per_step = fixed + per_row * wl.batch + t_sgd
-        sample = (f"float64 oracle gradient on {r} rows ({t[0]:.2f} s) and {2 * r} rows "
-                  f"({t[1]:.2f} s) of the {wl.batch}, fitted as {fixed:.2f} s + "
-                  f"{per_row * 1e3:.2f} ms per row and evaluated at {wl.batch} rows"
+        sample = (f"float64 oracle gradient on {a} rows ({ta:.2f} s) and {b} rows "
+                  f"({tb:.2f} s) of the {wl.batch}, fitted as {fixed:.2f} s + "
+                  f"{per_row * 1e3:.3f} ms per row and evaluated at {wl.batch} rows"
                   + (f", plus one SGD update over all parameters ({t_sgd:.2f} s)" if wl.sgd else ""))
         return 1.0 / per_step, sample
 
