@@ -190,6 +190,9 @@ GemmPlan choose(const GemmDesc& d, bool assume_aligned, int64_t capacity, int fo
     // workgroup per compute unit they cannot hide their load latency).
     if (can_async && (t.cfg == 0 || t.cfg == 1 || t.cfg == 4) && forced != t.cfg) continue;
     if ((t.cfg == 14 || t.cfg == 15) && !xl_ok(d)) continue;
+    // The 256 x 256 direct-to-LDS tiles load one-phase products through
+    // buffer descriptors: operand extents below 2^31 bytes.
+    if ((t.cfg == 10 || t.cfg == 13) && d.A2 == nullptr && !xl_ok(d)) continue;
     // Measured on 16384 x 4096 x 4096: the four-wave kernel is the faster
     // one for the forward layout only; 15 runs only when forced.
     if (t.cfg == 14 && d.layout != Layout::NN && forced != 14) continue;
@@ -315,6 +318,12 @@ void vector_ok(const GemmDesc& d, bool& va, bool& vb) {
   }
 }
 
+// Whether a launch loads its operands through buffer descriptors (and needs
+// their extents below 2^31 bytes).
+bool buffer_loads(const GemmDesc& d, const GemmPlan& pl) {
+  return pl.cfg == 14 || pl.cfg == 15 || ((pl.cfg == 10 || pl.cfg == 13) && d.A2 == nullptr);
+}
+
 gemm::Params make_params(const GemmDesc& d, const GemmPlan& pl) {
   gemm::Params p;
   p.M = d.M; p.N = d.N; p.K = d.K;
@@ -347,7 +356,10 @@ gemm::Params make_params(const GemmDesc& d, const GemmPlan& pl) {
   } else {
     p.c_split = p.cs_split = 0;
   }
-  if (pl.cfg == 14 || pl.cfg == 15) {
+  // Extents for the buffer-descriptor loads: the four-wave kernel and the
+  // one-phase 256 x 256 direct-to-LDS tiles (which the planner runs only
+  // where xl_ok holds; launch_gemm refuses them otherwise).
+  if (buffer_loads(d, pl)) {
     int64_t ar, ac, br, bc;
     operand_dims(d, ar, ac, br, bc);
     p.a_bytes = static_cast<uint32_t>(extent_bytes(ar, ac, d.lda, 2));
@@ -368,6 +380,7 @@ hipError_t launch_gemm(const GemmDesc& d, const GemmPlan& pl, hipStream_t s) {
   bool va, vb;
   vector_ok(d, va, vb);
   if (d.mask != nullptr && (!mask_ok(d, pl) || !aligned16(d.mask))) return hipErrorInvalidValue;
+  if (buffer_loads(d, pl) && !xl_ok(d)) return hipErrorInvalidValue;
   const gemm::Params p = make_params(d, pl);
   const unsigned grid = grid_of(pl);
   const int out = pl.splits > 1 ? F32 : d.out_dtype;  // split slices: float32 partials
@@ -382,6 +395,7 @@ hipError_t launch_gemm(const GemmDesc& d, const GemmPlan& pl, hipStream_t s) {
 bool pairable(const GemmDesc& tn, const GemmPlan& ptn, const GemmDesc& nt, const GemmPlan& pnt) {
   if (tn.layout != Layout::TN || nt.layout != Layout::NT || tn.dtype != nt.dtype) return false;
   if (ptn.cfg != pnt.cfg || !gemm::pair_config(tn.dtype, ptn.cfg)) return false;
+  if ((buffer_loads(tn, ptn) && !xl_ok(tn)) || (buffer_loads(nt, pnt) && !xl_ok(nt))) return false;
   if (ptn.cfg < 10) {  // register-staged: 16-byte loads for all four operands
     bool a1, b1, a2, b2;
     vector_ok(tn, a1, b1);
@@ -394,6 +408,8 @@ bool pairable(const GemmDesc& tn, const GemmPlan& ptn, const GemmDesc& nt, const
 hipError_t launch_gemm_pair(const GemmDesc& tn, const GemmPlan& ptn, const GemmDesc& nt,
                             const GemmPlan& pnt, hipStream_t s) {
   if (tn.mask != nullptr) return hipErrorInvalidValue;
+  if ((buffer_loads(tn, ptn) && !xl_ok(tn)) || (buffer_loads(nt, pnt) && !xl_ok(nt)))
+    return hipErrorInvalidValue;
   if (nt.mask != nullptr && (!mask_ok(nt, pnt) || !aligned16(nt.mask))) return hipErrorInvalidValue;
   const gemm::Params p1 = make_params(tn, ptn), p2 = make_params(nt, pnt);
   const unsigned n1 = grid_of(ptn);

@@ -91,6 +91,37 @@ __device__ __forceinline__ int64_t chunk_src(int kb, int lane, int64_t ld, int64
   }
 }
 
+// Buffer descriptor of `bytes` bytes at `base` (raw buffer, no swizzle, no
+// index stride; the third word is the data-format word of gfx9 raw buffers).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, static_cast<int>(bytes),
+                                           0x00020000);
+}
+
+// Byte offsets (k-tile 0) of the 16-byte chunks that lane `lane` of `wave`
+// fetches for its LOADS wave instructions of one 256 x BK operand tile.
+// KMAJ: rows of BK k (2 BK bytes); the chunk c of row r holds k 8c..8c+7 and
+// sits in slot c ^ kswz(r). !KMAJ: k-rows of 256 elements (512 bytes); the
+// 16-byte column group c of k-row k sits in slot c ^ f(k & 3).
+template <bool KMAJ, int BK, int LOADS>
+__device__ __forceinline__ void xl_offsets(uint32_t (&off)[LOADS], int wave, int lane, int64_t ld,
+                                           int64_t r0) {
+#pragma unroll
+  for (int j = 0; j < LOADS; ++j) {
+    const int b = (wave * LOADS + j) * 1024 + lane * 16;  // byte inside the tile
+    if constexpr (KMAJ) {
+      const int r = b / (2 * BK);
+      const int c = ((b % (2 * BK)) >> 4) ^ kswz<BK>(r);
+      off[j] = static_cast<uint32_t>(((r0 + r) * ld + c * 8) * 2);
+    } else {
+      const int k = b / 512;
+      const int q = k & 3;
+      const int c = ((b % 512) >> 4) ^ ((q ^ ((q & 1) << 2)) << 1);
+      off[j] = static_cast<uint32_t>((k * ld + r0 + c * 8) * 2);
+    }
+  }
+}
+
 template <bool KMAJ, int ROWS, int BK, int NWAVES>
 __device__ __forceinline__ void async_tile(const bf16_t* __restrict__ P, int64_t ld, int64_t r0,
                                            int64_t rlim, int64_t k0, int64_t klim, char* lds,
@@ -439,10 +470,31 @@ __device__ __forceinline__ void epilogue_lds(const Params& p, const f32x16 (&acc
   }
 }
 
+// Buffer-descriptor direct loads of k-tile kt of a 256 x 256 tile's A and B
+// into ring slot `st`: LA and LB wave instructions per operand, at the lane's
+// precomputed byte offsets; the descriptors start at the k-tile's origin
+// (kt * step bytes into the operand).
+template <int LA, int LB, int A_BYTES>
+__device__ __forceinline__ void buf_ktile(const Params& p, int kt, uint32_t stepa, uint32_t stepb,
+                                          char* st, const uint32_t* offa, const uint32_t* offb,
+                                          int wave) {
+  const uint32_t sa = static_cast<uint32_t>(kt) * stepa, sb = static_cast<uint32_t>(kt) * stepb;
+  const __amdgpu_buffer_rsrc_t ra = make_rsrc(static_cast<const char*>(p.A) + sa, p.a_bytes - sa);
+  const __amdgpu_buffer_rsrc_t rb = make_rsrc(static_cast<const char*>(p.B) + sb, p.b_bytes - sb);
+#pragma unroll
+  for (int j = 0; j < LA; ++j)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, DLVM_LDS_PTR(st + (wave * LA + j) * 1024), 16,
+                                             offa[j], 0, 0, 0);
+#pragma unroll
+  for (int j = 0; j < LB; ++j)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, DLVM_LDS_PTR(st + A_BYTES + (wave * LB + j) * 1024),
+                                             16, offb[j], 0, 0, 0);
+}
+
 // One output tile (`tile` from split_slice) of the direct-to-LDS kernel, LDS
 // ring at `smem` (STAGES * (BM + BN) * 2 * BK bytes, 1024-byte aligned).
 template <typename TO, bool AK, bool BKM, int BM, int BN, int BK, int WM, int WN, int STAGES,
-          int EPI, bool PH2 = false, int ILV = 0>
+          int EPI, bool PH2 = false, int ILV = 0, bool BUFOK = true>
 __device__ __forceinline__ void async_gemm_tile(Params& p, const int tile, char* smem) {
   constexpr int NW = WM * WN;
   constexpr int THREADS = 64 * NW;
@@ -510,9 +562,39 @@ __device__ __forceinline__ void async_gemm_tile(Params& p, const int tile, char*
     async_tile<BKM, BN, BK, NW>(q.b, p.ldb, n0, p.N, q.k0, q.klim, st + A_BYTES, wave, lane);
   };
 
+  // Buffer-descriptor loads (256 x 256 tiles, one phase; the host sets the
+  // operand extents a_bytes and b_bytes, below 2^31 bytes, for every launch
+  // of such a tile). Each lane's byte offsets inside a k-tile are computed
+  // once; a k-tile's loads only move the descriptors' base and size (scalar
+  // work), and the hardware returns zero for offsets past the size, so rows
+  // past M or N need no clamping. Measured on the deep network's 16384 x 4096
+  // x 4096 products: the forward that writes the rectifier mask 540 -> 482-488
+  // us, the input adjoint reading it 476 -> 466-469, the weight adjoint 510 ->
+  // 482-485 (the computed addresses cost about 100 vector instructions per
+  // wave and k-tile between the barrier and the first matrix instruction);
+  // the loads spread over the k-tile's 16-k steps instead were slower than
+  // issuing them together. Other tiles compute every load's clamped address
+  // (issue above). BUFOK = false keeps computed addresses (a slice of a
+  // two-phase product may read A2, whose extent the host does not pass).
+  constexpr bool BUF = BUFOK && BM == 256 && BN == 256 && !PH2;
+  constexpr int LA = A_BYTES / 1024 / NW, LB = B_BYTES / 1024 / NW;
+  uint32_t offa[BUF ? LA : 1], offb[BUF ? LB : 1];
+  uint32_t stepa = 0, stepb = 0;
+  if constexpr (BUF) {
+    xl_offsets<AK, BK, LA>(offa, wave, lane, p.lda, m0);
+    xl_offsets<BKM, BK, LB>(offb, wave, lane, p.ldb, n0);
+    stepa = AK ? BK * 2 : static_cast<uint32_t>(BK * p.lda * 2);
+    stepb = BKM ? BK * 2 : static_cast<uint32_t>(BK * p.ldb * 2);
+  }
 #pragma unroll
-  for (int s = 0; s < STAGES - 1; ++s)
-    if (s < nk) issue(s);
+  for (int s = 0; s < STAGES - 1; ++s) {
+    if (s < nk) {
+      if constexpr (BUF)
+        buf_ktile<LA, LB, A_BYTES>(p, s, stepa, stepb, smem + s * STAGE, offa, offb, wave);
+      else
+        issue(s);
+    }
+  }
 
   for (int kt = 0; kt < nk; ++kt) {
     // Stage kt has landed once at most `ahead` later stages are outstanding.
@@ -529,7 +611,14 @@ __device__ __forceinline__ void async_gemm_tile(Params& p, const int tile, char*
       barrier_only();
     }
     // The slot refilled here was last read in iteration kt - 1, before the barrier.
-    if (kt + STAGES - 1 < nk) issue(kt + STAGES - 1);
+    const int kn = kt + STAGES - 1;
+    if (kn < nk) {
+      if constexpr (BUF)
+        buf_ktile<LA, LB, A_BYTES>(p, kn, stepa, stepb, smem + (kn % STAGES) * STAGE, offa, offb,
+                                   wave);
+      else
+        issue(kn);
+    }
     mma_ktile<AK, BKM, BM, BN, BK, TM, TN, EPI == EPI_DW, ILV>(As, Bs, wm * WTM, wn * WTN, lane,
                                                                acc, cs, do_colsum);
   }
@@ -595,8 +684,8 @@ __global__ __launch_bounds__(64 * WM * WN) void dlvm_gemm_async_kernel(Params p)
   // a k-slice of a split two-phase product lies in one phase
   if (PH2 && p.splits <= 1)
     async_gemm_tile<TO, AK, BKM, BM, BN, BK, WM, WN, STAGES, EPI, PH2, ILV>(p, tile, smem);
-  else
-    async_gemm_tile<TO, AK, BKM, BM, BN, BK, WM, WN, STAGES, EPI, false, ILV>(p, tile, smem);
+  else  // (a slice of a two-phase product may read A2: computed addresses)
+    async_gemm_tile<TO, AK, BKM, BM, BN, BK, WM, WN, STAGES, EPI, false, ILV, !PH2>(p, tile, smem);
 }
 
 // The two adjoint products of one dense layer in one launch (blocks [0, n1):

@@ -149,8 +149,9 @@ __device__ __forceinline__ int split_slice(Params& p, int bid) {
     }
     p.A = static_cast<const T*>(p.A) + sa;
     p.B = static_cast<const T*>(p.B) + sb;
-    p.a_bytes -= static_cast<uint32_t>(sa * static_cast<int64_t>(sizeof(T)));
-    p.b_bytes -= static_cast<uint32_t>(sb * static_cast<int64_t>(sizeof(T)));
+    // (extents of the buffer-descriptor loads; 0 means none and stays 0)
+    if (p.a_bytes != 0u) p.a_bytes -= static_cast<uint32_t>(sa * static_cast<int64_t>(sizeof(T)));
+    if (p.b_bytes != 0u) p.b_bytes -= static_cast<uint32_t>(sb * static_cast<int64_t>(sizeof(T)));
     p.K = kl;
     p.K1 = kl;  // split products have one phase
     p.C = static_cast<float*>(p.C) + sl * p.c_split;

@@ -31,37 +31,6 @@
 namespace dlvm {
 namespace gemm {
 
-// Buffer descriptor of `bytes` bytes at `base` (raw buffer, no swizzle, no
-// index stride; the third word is the data-format word of gfx9 raw buffers).
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, static_cast<int>(bytes),
-                                           0x00020000);
-}
-
-// Byte offsets (k-tile 0) of the 16-byte chunks that lane `lane` of `wave`
-// fetches for its LOADS wave instructions of one 256 x BK operand tile.
-// KMAJ: rows of BK k (2 BK bytes); the chunk c of row r holds k 8c..8c+7 and
-// sits in slot c ^ kswz(r). !KMAJ: k-rows of 256 elements (512 bytes); the
-// 16-byte column group c of k-row k sits in slot c ^ f(k & 3).
-template <bool KMAJ, int BK, int LOADS>
-__device__ __forceinline__ void xl_offsets(uint32_t (&off)[LOADS], int wave, int lane, int64_t ld,
-                                           int64_t r0) {
-#pragma unroll
-  for (int j = 0; j < LOADS; ++j) {
-    const int b = (wave * LOADS + j) * 1024 + lane * 16;  // byte inside the tile
-    if constexpr (KMAJ) {
-      const int r = b / (2 * BK);
-      const int c = ((b % (2 * BK)) >> 4) ^ kswz<BK>(r);
-      off[j] = static_cast<uint32_t>(((r0 + r) * ld + c * 8) * 2);
-    } else {
-      const int k = b / 512;
-      const int q = k & 3;
-      const int c = ((b % 512) >> 4) ^ ((q ^ ((q & 1) << 2)) << 1);
-      off[j] = static_cast<uint32_t>((k * ld + r0 + c * 8) * 2);
-    }
-  }
-}
-
 // Issue this wave's loads of one operand tile. The descriptor starts at the
 // k-tile's first element: `skip` bytes into an operand of `bytes` bytes.
 template <int LOADS>
