@@ -57,6 +57,33 @@ def test_no_masks_where_products_do_not_qualify(widths, acts, dtype, monkeypatch
     assert m.workspace_bytes(4096) == with_masks
 
 
+def test_operands_beyond_2gib_leave_the_256_tiles(monkeypatch):
+    """The 256 x 256 tiles load through buffer descriptors, whose extents are
+    32-bit: a product reading an operand of 2 GiB or more is planned on
+    another tile (here the 16384 x 4096 bf16 input grows to 2.46 GB at a batch
+    of 300000), and then its output gets no rectifier mask."""
+    widths, acts = (4096, 4096, 4096, 10), ("relu", "relu", "none")
+    m = dl.Model(widths, acts, "bf16", "softmax_ce", False, 300000)
+    plan = m.plan(300000)
+    for p in plan:
+        if p["name"].startswith(("gemm_nn", "gemm_nt", "gemm_tn", "gemm_pair")):
+            # bytes of the operands it reads through descriptors: A is M x K or K x M
+            big = p["M"] * p["K"] * 2 >= 2 ** 31 or p["N"] * p["K"] * 2 >= 2 ** 31
+            if big:
+                assert "c10" not in p["name"] and "c13" not in p["name"], p
+    assert plan[0]["name"].startswith("gemm_nn") and "c10" not in plan[0]["name"]
+    with_masks = m.workspace_bytes(300000)
+    monkeypatch.setenv("DLVM_RELU_MASK", "0")
+    assert m.workspace_bytes(300000) == with_masks
+    # below the limit the same network keeps the 256 x 256 tile and its masks
+    monkeypatch.delenv("DLVM_RELU_MASK")
+    m2 = dl.Model(widths, acts, "bf16", "softmax_ce", False, 200000)
+    assert m2.plan(200000)[0]["name"].endswith("c10")
+    masked = m2.workspace_bytes(200000)
+    monkeypatch.setenv("DLVM_RELU_MASK", "0")
+    assert masked - m2.workspace_bytes(200000) == 2 * _mask_bytes(200000, 4096)
+
+
 def _gradient(wl, x, params, y, ckpt=1, seed=None):
     import torch
     B = x.shape[0]
