@@ -2,8 +2,9 @@
 
 The planner picks these kernels only for large bf16 products; here each
 configuration (10: 256x256, 11: 256x128, 12: 128x128, 13: 256x256 with 32-deep
-k-tiles and a deeper ring, 14 and 15: 256x256 on four waves of 128x128 with
-buffer-descriptor loads, 64-deep k-tiles in 2 stages or 32-deep in 4) is
+k-tiles and a deeper ring, 14 and 15: 256x256 on four waves of 128x128,
+64-deep k-tiles in 2 stages or 32-deep in 4; the 256x256 tiles load through
+buffer descriptors, the others compute clamped addresses) is
 forced through
 DLVM_GEMM_CONFIG on shapes that span several tiles and stages with ragged M,
 N and K (K a multiple of 8 but not of 64, K smaller than one k-tile), for the
