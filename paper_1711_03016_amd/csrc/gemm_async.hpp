@@ -470,6 +470,62 @@ __device__ __forceinline__ void epilogue_lds(const Params& p, const f32x16 (&acc
   }
 }
 
+// Zero k >= kv of both operand tiles of a ring slot, then wait for every wave.
+template <bool AK, bool BKM, int BM, int BN, int BK, int THREADS, int A_BYTES>
+__device__ __forceinline__ void zero_tail_slot(char* slot, int kv, int tid) {
+  zero_k_tail<AK, BM, BK, THREADS>(slot, kv, tid);
+  zero_k_tail<BKM, BN, BK, THREADS>(slot + A_BYTES, kv, tid);
+  __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): the LDS writes are done
+  barrier_only();
+}
+
+// One 16-k step: the matrix instructions of the fragments in register set
+// CUR into acc, the reads of step s2 of the tile at (As2, Bs2) into the other
+// set interleaved with them when RD (ILV reads per matrix instruction), and
+// the column sums of the step's B fragments.
+template <bool AK, bool BKM, int BM, int BN, int BK, int TM, int TN, bool CS, int ILV, bool RD,
+          int CUR>
+__device__ __forceinline__ void mma_step(bf16x8 (&af)[2][TM], bf16x8 (&bfr)[2][TN],
+                                         const char* __restrict__ As2, const char* __restrict__ Bs2,
+                                         int s2, int arow, int brow, int lane,
+                                         f32x16 (&acc)[TM][TN], float (&cs)[TN], bool do_cs) {
+  if constexpr (RD) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i) af[CUR ^ 1][i] = frag<AK, BM, BK>(As2, arow + i * 32, s2, lane);
+#pragma unroll
+    for (int j = 0; j < TN; ++j) bfr[CUR ^ 1][j] = frag<BKM, BN, BK>(Bs2, brow + j * 32, s2, lane);
+  }
+  if constexpr (ILV == 0) __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[CUR][i], bfr[CUR][j], acc[i][j], 0, 0,
+                                                          0);
+  if constexpr (ILV > 0 && RD) {
+#pragma unroll
+    for (int q = 0; q < TM * TN; ++q) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, ILV & 7, 0);
+    }
+  }
+  __builtin_amdgcn_sched_barrier(0);
+  if constexpr (CS) {
+    if (do_cs) {
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const uint4 w = __builtin_bit_cast(uint4, bfr[CUR][j]);
+        const uint32_t q[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          cs[j] += __uint_as_float(q[e] << 16);
+          cs[j] += __uint_as_float(q[e] & 0xffff0000u);
+        }
+      }
+    }
+  }
+}
+
 // Buffer-descriptor direct loads of k-tile kt of a 256 x 256 tile's A and B
 // into ring slot `st`: LA and LB wave instructions per operand, at the lane's
 // precomputed byte offsets; the descriptors start at the k-tile's origin
@@ -494,7 +550,7 @@ __device__ __forceinline__ void buf_ktile(const Params& p, int kt, uint32_t step
 // One output tile (`tile` from split_slice) of the direct-to-LDS kernel, LDS
 // ring at `smem` (STAGES * (BM + BN) * 2 * BK bytes, 1024-byte aligned).
 template <typename TO, bool AK, bool BKM, int BM, int BN, int BK, int WM, int WN, int STAGES,
-          int EPI, bool PH2 = false, int ILV = 0, bool BUFOK = true>
+          int EPI, bool PH2 = false, int ILV = 0, bool BUFOK = true, bool EARLY = false>
 __device__ __forceinline__ void async_gemm_tile(Params& p, const int tile, char* smem) {
   constexpr int NW = WM * WN;
   constexpr int THREADS = 64 * NW;
@@ -596,6 +652,57 @@ __device__ __forceinline__ void async_gemm_tile(Params& p, const int tile, char*
     }
   }
 
+  if constexpr (EARLY) {
+    // The k-tile's barrier sits before its last 16-k step instead of at its
+    // start: the last step's matrix instructions run while the next k-tile's
+    // first fragments are read, and the previous step's instructions are
+    // still in the matrix pipeline during the wait. Bitwise the same sums.
+    static_assert(BUF && STAGES == 2, "early barrier: buffer loads, two stages");
+    constexpr int S = BK / 16;
+    static_assert(S == 2 || S == 4, "two or four 16-k steps");
+    if (nk > 1) buf_ktile<LA, LB, A_BYTES>(p, 1, stepa, stepb, smem + STAGE, offa, offb, wave);
+    if (nk > 1) wait_vm<LOADS>();
+    else wait_vm<0>();
+    barrier_only();
+    // (k past K in the last k-tile is zeroed once it has landed, everyone waiting)
+    if (nk == 1 && kv1 < BK) zero_tail_slot<AK, BKM, BM, BN, BK, THREADS, A_BYTES>(smem, kv1, tid);
+    bf16x8 af[2][TM], bfr[2][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i) af[0][i] = frag<AK, BM, BK>(smem, wm * WTM + i * 32, 0, lane);
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+      bfr[0][j] = frag<BKM, BN, BK>(smem + A_BYTES, wn * WTN + j * 32, 0, lane);
+    for (int kt = 0; kt < nk; ++kt) {
+      const char* As = smem + (kt % 2) * STAGE;
+      const char* Bs = As + A_BYTES;
+      mma_step<AK, BKM, BM, BN, BK, TM, TN, EPI == EPI_DW, ILV, true, 0>(
+          af, bfr, As, Bs, 1, wm * WTM, wn * WTN, lane, acc, cs, do_colsum);
+      if constexpr (S == 4) {
+        mma_step<AK, BKM, BM, BN, BK, TM, TN, EPI == EPI_DW, ILV, true, 1>(
+            af, bfr, As, Bs, 2, wm * WTM, wn * WTN, lane, acc, cs, do_colsum);
+        mma_step<AK, BKM, BM, BN, BK, TM, TN, EPI == EPI_DW, ILV, true, 0>(
+            af, bfr, As, Bs, 3, wm * WTM, wn * WTN, lane, acc, cs, do_colsum);
+      }
+      // Every read of this k-tile's slot is done (the last step's fragments
+      // are in registers) and the next k-tile has landed: then the slot is
+      // refilled with k-tile kt + 2 and the next k-tile's first fragments read.
+      __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
+      const bool more = kt + 1 < nk;
+      if (more) wait_vm<0>();
+      barrier_only();
+      if (kt + 2 < nk)
+        buf_ktile<LA, LB, A_BYTES>(p, kt + 2, stepa, stepb, smem + (kt % 2) * STAGE, offa, offb,
+                                   wave);
+      constexpr int last = (S - 1) & 1;
+      if (more && kt + 1 == nk - 1 && kv1 < BK)
+        zero_tail_slot<AK, BKM, BM, BN, BK, THREADS, A_BYTES>(smem + ((kt + 1) % 2) * STAGE, kv1,
+                                                             tid);
+      // (after the last k-tile these reads of the other slot are not used)
+      const char* An = smem + ((kt + 1) % 2) * STAGE;
+      mma_step<AK, BKM, BM, BN, BK, TM, TN, EPI == EPI_DW, ILV, true, last>(
+          af, bfr, An, An + A_BYTES, 0, wm * WTM, wn * WTN, lane, acc, cs, do_colsum);
+    }
+  } else
   for (int kt = 0; kt < nk; ++kt) {
     // Stage kt has landed once at most `ahead` later stages are outstanding.
     const int left = nk - 1 - kt;
@@ -674,18 +781,28 @@ __device__ __forceinline__ void async_gemm_tile(Params& p, const int tile, char*
 // (measured on the 256 x 256 tile with 64-deep k-tiles only).
 template <int BM, int BN, int BK>
 constexpr int async_ilv() { return (BM == 256 && BN == 256 && BK == 64) ? 4 : 0; }
+// The k-tile barrier before the last 16-k step (buffer-descriptor loads, two
+// stages), with two fragment reads per matrix instruction. Measured on the
+// deep network's products on one box, alternating builds: forward 3806-3811
+// against 3854-3865 us for its eight products and the output layer's, the
+// seven TN+NT pairs 6180-6194 against 6314-6325, the TN product 470 against
+// 480 (89.3-89.6 against 88.2-88.5 steps/s).
+template <int BM, int BN, int BK, int STAGES>
+constexpr bool async_early() { return BM == 256 && BN == 256 && BK == 64 && STAGES == 2; }
 
 template <typename TO, bool AK, bool BKM, int BM, int BN, int BK, int WM, int WN, int STAGES,
           int EPI, bool PH2>
 __global__ __launch_bounds__(64 * WM * WN) void dlvm_gemm_async_kernel(Params p) {
   __shared__ __attribute__((aligned(1024))) char smem[STAGES * (BM + BN) * 2 * BK];
   constexpr int ILV = async_ilv<BM, BN, BK>();
+  constexpr bool EARLY = !PH2 && async_early<BM, BN, BK, STAGES>();
   const int tile = split_slice<bf16_t, AK, BKM>(p, static_cast<int>(blockIdx.x));
   // a k-slice of a split two-phase product lies in one phase
   if (PH2 && p.splits <= 1)
     async_gemm_tile<TO, AK, BKM, BM, BN, BK, WM, WN, STAGES, EPI, PH2, ILV>(p, tile, smem);
   else  // (a slice of a two-phase product may read A2: computed addresses)
-    async_gemm_tile<TO, AK, BKM, BM, BN, BK, WM, WN, STAGES, EPI, false, ILV, !PH2>(p, tile, smem);
+    async_gemm_tile<TO, AK, BKM, BM, BN, BK, WM, WN, STAGES, EPI, false, EARLY ? 2 : ILV, !PH2,
+                    EARLY>(p, tile, smem);
 }
 
 // The two adjoint products of one dense layer in one launch (blocks [0, n1):
@@ -695,15 +812,16 @@ __global__ __launch_bounds__(64 * WM * WN) void dlvm_gemm_async_pair_kernel(Para
                                                                             int n1) {
   __shared__ __attribute__((aligned(1024))) char smem[STAGES * (BM + BN) * 2 * BK];
   const int b = static_cast<int>(blockIdx.x);
-  constexpr int ILV = async_ilv<BM, BN, BK>();
+  constexpr bool EARLY = async_early<BM, BN, BK, STAGES>();
+  constexpr int ILV = EARLY ? 2 : async_ilv<BM, BN, BK>();
   if (b < n1) {
     const int tile = split_slice<bf16_t, false, false>(p1, b);
-    async_gemm_tile<float, false, false, BM, BN, BK, WM, WN, STAGES, EPI_DW, false, ILV>(p1, tile,
-                                                                                      smem);
+    async_gemm_tile<float, false, false, BM, BN, BK, WM, WN, STAGES, EPI_DW, false, ILV, true,
+                    EARLY>(p1, tile, smem);
   } else {
     const int tile = split_slice<bf16_t, true, true>(p2, b - n1);
-    async_gemm_tile<TO2, true, true, BM, BN, BK, WM, WN, STAGES, EPI_DACT, false, ILV>(p2, tile,
-                                                                                     smem);
+    async_gemm_tile<TO2, true, true, BM, BN, BK, WM, WN, STAGES, EPI_DACT, false, ILV, true,
+                    EARLY>(p2, tile, smem);
   }
 }
 
