@@ -115,9 +115,14 @@ dlvm_status dlvm_param_layout(const dlvm_model* m, int64_t* offsets, int64_t* ld
  * (0 if the batch is invalid). Holds saved activations, adjoints, loss
  * partials, the float32 partial products of a split batch reduction (an
  * adjoint product wrt the weights whose output has too few tiles to occupy
- * the device is computed in k-slices and summed in slice order) and the device
- * error flags. One workspace must not be used by two calls that may run
- * concurrently. */
+ * the device is computed in k-slices and summed in slice order), the device
+ * error flags and, for a bf16 network whose rectified hidden outputs are
+ * produced and consumed by products on the 256 x 256 tile, one bit per
+ * element of each such output: the rectifier's derivative (output > 0), which
+ * the forward product writes and the adjoint product of the next layer reads
+ * instead of the saved output (section 3.1.3; the results are the same;
+ * the environment variable DLVM_RELU_MASK=0 turns the masks off). One
+ * workspace must not be used by two calls that may run concurrently. */
 size_t dlvm_workspace_bytes(const dlvm_model* m, int64_t batch);
 
 /* Where a gradient call keeps the intermediate values of the adjoint code
