@@ -60,6 +60,11 @@ bool phases_ok(const GemmDesc& d, int vw) {
   return d.A2 == nullptr || (aligned16(d.A2) && d.lda2 % vw == 0 && d.K1 % vw == 0);
 }
 
+// A contraction in two phases (a second source A2 for k in [K1, K)). Told by
+// the phase split as well as by A2, so a plan description, whose bases are
+// null, plans such a product as the call does.
+bool two_phase(const GemmDesc& d) { return d.A2 != nullptr || (d.K1 > 0 && d.K1 < d.K); }
+
 bool async_ok(const GemmDesc& d) {
   return d.dtype == BF16 && aligned16(d.A) && aligned16(d.B) && d.lda % 8 == 0 &&
          d.ldb % 8 == 0 && d.K % 8 == 0 && d.ldc % 8 == 0 && aligned16(d.C) &&
@@ -83,7 +88,7 @@ void operand_dims(const GemmDesc& d, int64_t& ar, int64_t& ac, int64_t& br, int6
 // offsets: every offset it forms (up to one tile past either extent) must stay
 // below 2^31.
 bool xl_ok(const GemmDesc& d) {
-  if (!async_ok(d) || d.A2 != nullptr) return false;
+  if (!async_ok(d) || two_phase(d)) return false;
   int64_t ar, ac, br, bc;
   operand_dims(d, ar, ac, br, bc);
   const int64_t lim = int64_t(1) << 31;
@@ -175,7 +180,7 @@ GemmPlan choose(const GemmDesc& d, bool assume_aligned, int64_t capacity, int fo
                 int fsplits) {
   const bool can_async = assume_aligned ? (d.dtype == BF16 && d.lda % 8 == 0 && d.ldb % 8 == 0 &&
                                            d.K % 8 == 0 && d.ldc % 8 == 0 &&
-                                           (d.A2 == nullptr || (d.lda2 % 8 == 0 && d.K1 % 8 == 0)))
+                                           (!two_phase(d) || (d.lda2 % 8 == 0 && d.K1 % 8 == 0)))
                                         : async_ok(d);
   const TileShape* best = nullptr;
   int best_s = 1;
@@ -190,9 +195,9 @@ GemmPlan choose(const GemmDesc& d, bool assume_aligned, int64_t capacity, int fo
     // workgroup per compute unit they cannot hide their load latency).
     if (can_async && (t.cfg == 0 || t.cfg == 1 || t.cfg == 4) && forced != t.cfg) continue;
     if ((t.cfg == 14 || t.cfg == 15) && !xl_ok(d)) continue;
-    // The 256 x 256 direct-to-LDS tiles load one-phase products through
-    // buffer descriptors: operand extents below 2^31 bytes.
-    if ((t.cfg == 10 || t.cfg == 13) && d.A2 == nullptr && !xl_ok(d)) continue;
+    // The direct-to-LDS tiles load one-phase products through buffer
+    // descriptors: operand extents below 2^31 bytes.
+    if (t.async && !two_phase(d) && !xl_ok(d)) continue;
     // Measured on 16384 x 4096 x 4096: the four-wave kernel is the faster
     // one for the forward layout only; 15 runs only when forced.
     if (t.cfg == 14 && d.layout != Layout::NN && forced != 14) continue;
@@ -202,7 +207,7 @@ GemmPlan choose(const GemmDesc& d, bool assume_aligned, int64_t capacity, int fo
     if (forced >= 0 && t.cfg != forced) continue;
     for (int sp = 1; sp <= kMaxSplits; sp *= 2) {
       // a two-phase product's slices must not straddle its phase boundary
-      if (sp > 1 && d.A2 != nullptr && d.K1 % slice_k(d.K, sp) != 0) continue;
+      if (sp > 1 && two_phase(d) && d.K1 % slice_k(d.K, sp) != 0) continue;
       const bool forcing = fsplits > 0 && d.split_epilogue;  // (overrides the caller's split)
       if (!forcing && d.splits_hint > 0 && split_need(d, d.splits_hint) <= capacity) {
         // the caller's split (a multiple of 64 k per slice, whole slices)
@@ -231,7 +236,7 @@ GemmPlan choose(const GemmDesc& d, bool assume_aligned, int64_t capacity, int fo
   // the planner keeps whole of their own accord (no split asked for by the
   // caller, no second phase).
   if (best != nullptr && best->cfg == 12 && best_s == 1 && forced < 0 && can_async &&
-      d.layout != Layout::TN && d.A2 == nullptr && d.splits_hint == 0 &&
+      d.layout != Layout::TN && !two_phase(d) && d.splits_hint == 0 &&
       ceil_div(d.M, 128) * ceil_div(d.N, 128) <= kComputeUnits) {
     for (const TileShape& t : kTiles)
       if (t.cfg == 16) best = &t;
@@ -240,7 +245,7 @@ GemmPlan choose(const GemmDesc& d, bool assume_aligned, int64_t capacity, int fo
   // the CUs once: the 128 x 128 tile with a 2-deep ring (64 KiB, two
   // workgroups per CU) and twice the slices.
   if (best != nullptr && best->cfg == 12 && best_s > 1 && 2 * best_s <= kMaxSplits &&
-      forced < 0 && fsplits < 0 && can_async && d.layout == Layout::TN && d.A2 == nullptr &&
+      forced < 0 && fsplits < 0 && can_async && d.layout == Layout::TN && !two_phase(d) &&
       d.splits_hint == 0 &&
       ceil_div(d.M, 128) * ceil_div(d.N, 128) * best_s <= kComputeUnits &&
       slice_k(d.K, 2 * best_s) >= kMinChunk &&
@@ -281,7 +286,7 @@ GemmPlan plan_gemm(const GemmDesc& d) {
 
 bool mask_ok(const GemmDesc& d, const GemmPlan& pl) {
   if (d.dtype != BF16 || d.out_dtype != BF16 || d.act != ACT_RELU) return false;
-  if (pl.cfg != 10 || pl.splits != 1 || d.A2 != nullptr || d.chain_epilogue) return false;
+  if (pl.cfg != 10 || pl.splits != 1 || two_phase(d) || d.chain_epilogue) return false;
   return d.layout == Layout::NN || (d.layout == Layout::NT && d.residual == nullptr);
 }
 
@@ -319,9 +324,13 @@ void vector_ok(const GemmDesc& d, bool& va, bool& vb) {
 }
 
 // Whether a launch loads its operands through buffer descriptors (and needs
-// their extents below 2^31 bytes).
+// their extents below 2^31 bytes): the bf16 direct-to-LDS and four-wave
+// kernels, for one-phase products.
 bool buffer_loads(const GemmDesc& d, const GemmPlan& pl) {
-  return pl.cfg == 14 || pl.cfg == 15 || ((pl.cfg == 10 || pl.cfg == 13) && d.A2 == nullptr);
+  if (two_phase(d)) return false;
+  for (const TileShape& t : kTiles)
+    if (t.cfg == pl.cfg) return t.async;
+  return false;
 }
 
 gemm::Params make_params(const GemmDesc& d, const GemmPlan& pl) {
@@ -356,9 +365,8 @@ gemm::Params make_params(const GemmDesc& d, const GemmPlan& pl) {
   } else {
     p.c_split = p.cs_split = 0;
   }
-  // Extents for the buffer-descriptor loads: the four-wave kernel and the
-  // one-phase 256 x 256 direct-to-LDS tiles (which the planner runs only
-  // where xl_ok holds; launch_gemm refuses them otherwise).
+  // Extents for the buffer-descriptor loads (the planner runs these kernels
+  // only where xl_ok holds; launch_gemm refuses them otherwise).
   if (buffer_loads(d, pl)) {
     int64_t ar, ac, br, bc;
     operand_dims(d, ar, ac, br, bc);

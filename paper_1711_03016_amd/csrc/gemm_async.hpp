@@ -99,13 +99,15 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, ui
 }
 
 // Byte offsets (k-tile 0) of the 16-byte chunks that lane `lane` of `wave`
-// fetches for its LOADS wave instructions of one 256 x BK operand tile.
-// KMAJ: rows of BK k (2 BK bytes); the chunk c of row r holds k 8c..8c+7 and
-// sits in slot c ^ kswz(r). !KMAJ: k-rows of 256 elements (512 bytes); the
-// 16-byte column group c of k-row k sits in slot c ^ f(k & 3).
-template <bool KMAJ, int BK, int LOADS>
-__device__ __forceinline__ void xl_offsets(uint32_t (&off)[LOADS], int wave, int lane, int64_t ld,
-                                           int64_t r0) {
+// fetches for its LOADS wave instructions of one ROWS x BK operand tile (the
+// same chunks as chunk_src, without clamping). KMAJ: rows of BK k (2 BK
+// bytes); the chunk c of row r holds k 8c..8c+7 and sits in slot c ^ kswz(r).
+// !KMAJ: k-rows of ROWS elements (2 ROWS bytes); the 16-byte column group c of
+// k-row k sits in slot c ^ f(k & 3).
+template <bool KMAJ, int ROWS, int BK, int LOADS>
+__device__ __forceinline__ void tile_offsets(uint32_t (&off)[LOADS], int wave, int lane, int64_t ld,
+                                             int64_t r0) {
+  constexpr int RB = ROWS * 2;
 #pragma unroll
   for (int j = 0; j < LOADS; ++j) {
     const int b = (wave * LOADS + j) * 1024 + lane * 16;  // byte inside the tile
@@ -114,12 +116,17 @@ __device__ __forceinline__ void xl_offsets(uint32_t (&off)[LOADS], int wave, int
       const int c = ((b % (2 * BK)) >> 4) ^ kswz<BK>(r);
       off[j] = static_cast<uint32_t>(((r0 + r) * ld + c * 8) * 2);
     } else {
-      const int k = b / 512;
+      const int k = b / RB;
       const int q = k & 3;
-      const int c = ((b % 512) >> 4) ^ ((q ^ ((q & 1) << 2)) << 1);
+      const int c = ((b % RB) >> 4) ^ ((q ^ ((q & 1) << 2)) << 1);
       off[j] = static_cast<uint32_t>((k * ld + r0 + c * 8) * 2);
     }
   }
+}
+template <bool KMAJ, int BK, int LOADS>
+__device__ __forceinline__ void xl_offsets(uint32_t (&off)[LOADS], int wave, int lane, int64_t ld,
+                                           int64_t r0) {
+  tile_offsets<KMAJ, 256, BK, LOADS>(off, wave, lane, ld, r0);
 }
 
 template <bool KMAJ, int ROWS, int BK, int NWAVES>
@@ -618,27 +625,27 @@ __device__ __forceinline__ void async_gemm_tile(Params& p, const int tile, char*
     async_tile<BKM, BN, BK, NW>(q.b, p.ldb, n0, p.N, q.k0, q.klim, st + A_BYTES, wave, lane);
   };
 
-  // Buffer-descriptor loads (256 x 256 tiles, one phase; the host sets the
-  // operand extents a_bytes and b_bytes, below 2^31 bytes, for every launch
-  // of such a tile). Each lane's byte offsets inside a k-tile are computed
-  // once; a k-tile's loads only move the descriptors' base and size (scalar
-  // work), and the hardware returns zero for offsets past the size, so rows
-  // past M or N need no clamping. Measured on the deep network's 16384 x 4096
-  // x 4096 products: the forward that writes the rectifier mask 540 -> 482-488
-  // us, the input adjoint reading it 476 -> 466-469, the weight adjoint 510 ->
-  // 482-485 (the computed addresses cost about 100 vector instructions per
-  // wave and k-tile between the barrier and the first matrix instruction);
-  // the loads spread over the k-tile's 16-k steps instead were slower than
-  // issuing them together. Other tiles compute every load's clamped address
-  // (issue above). BUFOK = false keeps computed addresses (a slice of a
-  // two-phase product may read A2, whose extent the host does not pass).
-  constexpr bool BUF = BUFOK && BM == 256 && BN == 256 && !PH2;
+  // Buffer-descriptor loads (one-phase products; the host sets the operand
+  // extents a_bytes and b_bytes, below 2^31 bytes, for every such launch).
+  // Each lane's byte offsets inside a k-tile are computed once; a k-tile's
+  // loads only move the descriptors' base and size (scalar work), and the
+  // hardware returns zero for offsets past the size, so rows past M or N need
+  // no clamping. Measured on the deep network's 16384 x 4096 x 4096 products
+  // (256 x 256 tile): the forward that writes the rectifier mask 540 ->
+  // 482-488 us, the input adjoint reading it 476 -> 466-469, the weight
+  // adjoint 510 -> 482-485 (the computed addresses cost about 100 vector
+  // instructions per wave and k-tile between the barrier and the first matrix
+  // instruction); the loads spread over the k-tile's 16-k steps instead were
+  // slower than issuing them together. Two-phase products compute every
+  // load's clamped address (issue above), and so does BUFOK = false (a slice
+  // of a two-phase product may read A2, whose extent the host does not pass).
+  constexpr bool BUF = BUFOK && !PH2;
   constexpr int LA = A_BYTES / 1024 / NW, LB = B_BYTES / 1024 / NW;
   uint32_t offa[BUF ? LA : 1], offb[BUF ? LB : 1];
   uint32_t stepa = 0, stepb = 0;
   if constexpr (BUF) {
-    xl_offsets<AK, BK, LA>(offa, wave, lane, p.lda, m0);
-    xl_offsets<BKM, BK, LB>(offb, wave, lane, p.ldb, n0);
+    tile_offsets<AK, BM, BK, LA>(offa, wave, lane, p.lda, m0);
+    tile_offsets<BKM, BN, BK, LB>(offb, wave, lane, p.ldb, n0);
     stepa = AK ? BK * 2 : static_cast<uint32_t>(BK * p.lda * 2);
     stepb = BKM ? BK * 2 : static_cast<uint32_t>(BK * p.ldb * 2);
   }

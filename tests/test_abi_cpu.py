@@ -285,6 +285,9 @@ def test_rnn_handle_plan_and_errors():
     nn = [p for p in plan if p["name"].startswith("gemm_nn")]
     assert len(nn) == wl.steps
     assert all(p["K"] == wl.in_width + wl.hidden and p["M"] == wl.batch for p in nn)
+    # every cell is a two-phase product, the first too (its h0 block has a
+    # null address in the description, whose bases are null): one tile for all
+    assert len({p["name"] for p in nn}) == 1
     assert plan[-1]["name"].startswith("sgd")
     assert sum(p["flops"] for p in plan) == wl.flops()
     ws = m.workspace_bytes(wl.batch)
