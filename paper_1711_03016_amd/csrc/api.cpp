@@ -829,14 +829,15 @@ GemmDesc rnn_du(const dlvm_model* m, int64_t B, const void* hs, const void* dz, 
 
 // k-slices for one of the recurrent step's products (a cell product or a
 // recurrent adjoint). One step's product has few output tiles (B x H over
-// 128 x 128 tiles: 64 for r1's 1024 x 1024) and the steps run one after the
-// other, so the contraction is split until there are as many tile-slices as
-// compute units, at most 4 ways, each slice at least 256 deep and, for a
-// two-phase product, within one phase. (Measured on 1024 x 1024 products,
-// K = 2048 / 1024: 4 slices fastest of 1, 2, 4, 8 for the cell products; 2 and
-// 4 alike for the recurrent adjoints.)
+// the 64 x 128 tiles of the k-group kernel: 128 for a 1024 x 1024 output) and
+// the steps run one after the other, so the contraction is split until there
+// are as many tile-slices as compute units, at most 4 ways, each slice at
+// least 256 deep and, for a two-phase product, within one phase. (Measured on
+// 1024 x 1024 products, K = 2048 / 1024, batch 1024 and T = 32: two slices on
+// that tile 673 steps/s against 607 for four on the 128 x 128 tile, one slice
+// 597.)
 int rnn_split_hint(int64_t M, int64_t N, int64_t K, int64_t K1) {
-  const int64_t tiles = (M + 127) / 128 * ((N + 127) / 128);
+  const int64_t tiles = (M + 63) / 64 * ((N + 127) / 128);
   int s = 1;
   while (s < 4 && tiles * s < 256) {
     const int64_t kc = ((K + 2 * s - 1) / (2 * s) + 63) / 64 * 64;  // k per slice at 2s slices

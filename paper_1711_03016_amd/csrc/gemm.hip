@@ -19,7 +19,8 @@ constexpr double kL2BytesPerClock = 64.0;
 // when not starved, for float32 and for bf16 operands (measured on large
 // products). Configurations 0-5 are the register-staged kernel
 // (gemm_kernel.hpp), 10-13, 16 and 17 the bf16 kernel with direct-to-LDS loads
-// (gemm_async.hpp), 14-15 the four-wave bf16 kernel (gemm_xl.hpp).
+// (gemm_async.hpp; 18 with two k-groups of waves), 14-15 the four-wave bf16
+// kernel (gemm_xl.hpp).
 struct TileShape {
   int cfg;
   int bm, bn;
@@ -34,7 +35,8 @@ constexpr TileShape kTiles[] = {
     {10, 256, 256, 0.0, 0.9, true, 0},   {11, 256, 128, 0.0, 0.63, true, 0},
     {12, 128, 128, 0.0, 0.54, true, 0},  {13, 256, 256, 0.0, 0.88, true, 0},
     {14, 256, 256, 0.0, 0.89, true, 0},  {15, 256, 256, 0.0, 0.85, true, 0},
-    {16, 64, 128, 0.0, 0.5, true, 0},    {17, 128, 128, 0.0, 0.54, true, 0}};
+    {16, 64, 128, 0.0, 0.5, true, 0},    {17, 128, 128, 0.0, 0.54, true, 0},
+    {18, 64, 128, 0.0, 0.55, true, 0}};
 
 // The register-staged kernel has one stage of loads in flight: a stage costs
 // at least one load round trip (measured on small float32 products).
@@ -204,6 +206,16 @@ GemmPlan choose(const GemmDesc& d, bool assume_aligned, int64_t capacity, int fo
     if (t.cfg == 15 && forced != 15) continue;
     if (t.cfg == 16 && (d.layout == Layout::TN || forced != 16)) continue;
     if (t.cfg == 17 && forced != 17) continue;
+    // The k-group tile: products whose caller asks for k-slices (the steps
+    // of a recurrence, whose few output tiles are split over k to fill the
+    // CUs). Measured on the 1024 x 1024 x 2048 cell and 1024 x 1024 x 1024
+    // recurrent products, two slices on this tile against four on the
+    // 128 x 128 tile: 17.3 against 16.9 us and 11.6 against 15.7 us. On the
+    // 4096 x 1024 products of a whole batch it gains nothing over 16 in the
+    // step, and a 64-deep contraction is slower.
+    if (t.cfg == 18 && (d.layout == Layout::TN ||
+                        (forced != 18 && !(d.split_epilogue && d.splits_hint > 0))))
+      continue;
     if (forced >= 0 && t.cfg != forced) continue;
     for (int sp = 1; sp <= kMaxSplits; sp *= 2) {
       // a two-phase product's slices must not straddle its phase boundary

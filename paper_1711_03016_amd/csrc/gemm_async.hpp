@@ -275,6 +275,72 @@ __device__ __forceinline__ void mma_ktile(const char* __restrict__ As, const cha
   }
 }
 
+// NS consecutive 16-k steps of a k-tile from step s0 (a tile whose waves form
+// k-groups gives each group its own steps of every k-tile), the next step's
+// fragments read while the matrix cores work on the current ones.
+template <bool AK, bool BKM, int BM, int BN, int BK, int TM, int TN, int NS>
+__device__ __forceinline__ void mma_ksteps(const char* __restrict__ As, const char* __restrict__ Bs,
+                                           int s0, int arow, int brow, int lane,
+                                           f32x16 (&acc)[TM][TN]) {
+  bf16x8 af[2][TM], bfr[2][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i) af[0][i] = frag<AK, BM, BK>(As, arow + i * 32, s0, lane);
+#pragma unroll
+  for (int j = 0; j < TN; ++j) bfr[0][j] = frag<BKM, BN, BK>(Bs, brow + j * 32, s0, lane);
+#pragma unroll
+  for (int s = 0; s < NS; ++s) {
+    const int cur = s & 1, nxt = cur ^ 1;
+    if (s + 1 < NS) {
+#pragma unroll
+      for (int i = 0; i < TM; ++i) af[nxt][i] = frag<AK, BM, BK>(As, arow + i * 32, s0 + s + 1, lane);
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+        bfr[nxt][j] = frag<BKM, BN, BK>(Bs, brow + j * 32, s0 + s + 1, lane);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cur][i], bfr[cur][j], acc[i][j], 0, 0, 0);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
+// Partial sums of block rows [I0, I0 + TH) of a wave's accumulators to LDS
+// (xchg_put), or added from LDS (xchg_add): TH x TN blocks as 4 float4 per
+// lane each, lane-interleaved (lane l's float4 q at xb[(slot + q) * 64 + l]).
+template <int I0, int TH, int TM, int TN>
+__device__ __forceinline__ void xchg_put(float4* xb, const f32x16 (&acc)[TM][TN], int slot,
+                                         int lane) {
+#pragma unroll
+  for (int i = 0; i < TH; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const f32x16& a = acc[I0 + i][j];
+        xb[(slot + (i * TN + j) * 4 + r) * 64 + lane] =
+            make_float4(a[4 * r], a[4 * r + 1], a[4 * r + 2], a[4 * r + 3]);
+      }
+}
+template <int I0, int TH, int TM, int TN>
+__device__ __forceinline__ void xchg_add(const float4* xb, f32x16 (&acc)[TM][TN], int slot,
+                                         int lane) {
+#pragma unroll
+  for (int i = 0; i < TH; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float4 v = xb[(slot + (i * TN + j) * 4 + r) * 64 + lane];
+        acc[I0 + i][j][4 * r] += v.x;
+        acc[I0 + i][j][4 * r + 1] += v.y;
+        acc[I0 + i][j][4 * r + 2] += v.z;
+        acc[I0 + i][j][4 * r + 3] += v.w;
+      }
+}
+
 // Vector access to 8 consecutive elements (16 bytes of bf16, 32 of float32).
 __device__ __forceinline__ void load8(const bf16_t* p, float (&v)[8]) {
   const uint4 w = *reinterpret_cast<const uint4*>(p);
@@ -467,13 +533,14 @@ __device__ __forceinline__ void epilogue_row(const Params& p, const f32x16 (&acc
   __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
 
-// All TM rows of blocks, each with a statically indexed accumulator row.
-template <typename TO, int EPI, int TM, int TN, int I = 0>
+// Rows of blocks [I, IEND) (all TM by default), each with a statically
+// indexed accumulator row; r0 is the row of block row 0.
+template <typename TO, int EPI, int TM, int TN, int I = 0, int IEND = TM>
 __device__ __forceinline__ void epilogue_lds(const Params& p, const f32x16 (&acc)[TM][TN],
                                              float* region, int64_t r0, int64_t c0, int lane) {
-  if constexpr (I < TM) {
+  if constexpr (I < IEND) {
     epilogue_row<TO, EPI, TN>(p, acc[I], region, r0 + 32 * I, c0, lane);
-    epilogue_lds<TO, EPI, TM, TN, I + 1>(p, acc, region, r0, c0, lane);
+    epilogue_lds<TO, EPI, TM, TN, I + 1, IEND>(p, acc, region, r0, c0, lane);
   }
 }
 
@@ -556,10 +623,15 @@ __device__ __forceinline__ void buf_ktile(const Params& p, int kt, uint32_t step
 
 // One output tile (`tile` from split_slice) of the direct-to-LDS kernel, LDS
 // ring at `smem` (STAGES * (BM + BN) * 2 * BK bytes, 1024-byte aligned).
+// WK = 2: the waves form two k-groups of WM x WN waves over the same output
+// blocks, each taking half of every k-tile's 16-k steps (twice the waves per
+// SIMD with the LDS reads of WM x WN waves per k-tile); their partial sums are
+// added through LDS at the end and each group stores half of the block rows.
 template <typename TO, bool AK, bool BKM, int BM, int BN, int BK, int WM, int WN, int STAGES,
-          int EPI, bool PH2 = false, int ILV = 0, bool BUFOK = true, bool EARLY = false>
+          int EPI, bool PH2 = false, int ILV = 0, bool BUFOK = true, bool EARLY = false,
+          int WK = 1>
 __device__ __forceinline__ void async_gemm_tile(Params& p, const int tile, char* smem) {
-  constexpr int NW = WM * WN;
+  constexpr int NW = WM * WN * WK;
   constexpr int THREADS = 64 * NW;
   constexpr int WTM = BM / WM, WTN = BN / WN;
   constexpr int TM = WTM / 32, TN = WTN / 32;
@@ -570,11 +642,14 @@ __device__ __forceinline__ void async_gemm_tile(Params& p, const int tile, char*
   static_assert(STAGES >= 2 && STAGES - 2 <= 3 && 3 * LOADS < 64, "pipeline depth");
   static_assert(AK || BM >= 128, "m-contiguous tile needs 256-byte k-rows");
   static_assert(BKM || BN >= 128, "n-contiguous tile needs 256-byte k-rows");
+  static_assert(WK == 1 || (WK == 2 && !EARLY && EPI != EPI_DW && TM % 2 == 0 && BK == 64),
+                "k-groups: two, without the early barrier or column sums");
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  const int wm = wave / WN, wn = wave % WN;
+  const int wk = wave / (WM * WN);  // k-group
+  const int wm = (wave % (WM * WN)) / WN, wn = wave % WN;
   int tm, tn;
   tile_of(tile, p.tiles_m, p.tiles_n, tm, tn);
   const int64_t m0 = static_cast<int64_t>(tm) * BM;
@@ -607,7 +682,7 @@ __device__ __forceinline__ void async_gemm_tile(Params& p, const int tile, char*
   // Rectifier mask (256 x 256 tiles on 2 x 4 waves, one phase, bf16 output):
   // the adjoint's 16-byte word is loaded before the contraction so that its
   // latency hides behind it.
-  constexpr bool MASKABLE = BM == 256 && BN == 256 && WM == 2 && WN == 4 && !PH2 &&
+  constexpr bool MASKABLE = BM == 256 && BN == 256 && WM == 2 && WN == 4 && WK == 1 && !PH2 &&
                             (EPI == EPI_DACT || (EPI == EPI_STORE && std::is_same<TO, bf16_t>::value));
   uint32_t* const mask_word =
       MASKABLE && p.mask != nullptr
@@ -733,8 +808,58 @@ __device__ __forceinline__ void async_gemm_tile(Params& p, const int tile, char*
       else
         issue(kn);
     }
-    mma_ktile<AK, BKM, BM, BN, BK, TM, TN, EPI == EPI_DW, ILV>(As, Bs, wm * WTM, wn * WTN, lane,
-                                                               acc, cs, do_colsum);
+    if constexpr (WK == 1)
+      mma_ktile<AK, BKM, BM, BN, BK, TM, TN, EPI == EPI_DW, ILV>(As, Bs, wm * WTM, wn * WTN, lane,
+                                                                 acc, cs, do_colsum);
+    else
+      mma_ksteps<AK, BKM, BM, BN, BK, TM, TN, BK / 32>(As, Bs, wk * (BK / 32), wm * WTM, wn * WTN,
+                                                       lane, acc);
+  }
+
+  if constexpr (WK == 2) {
+    // Group 0 finishes block rows [0, TM/2) of the wave's blocks, group 1 the
+    // rest: each first hands the other group its partials of the other half
+    // (through LDS, once every wave is done with the ring) and adds the
+    // other's partials of its own half (a two-term sum: the same whichever
+    // group adds).
+    constexpr int TH = TM / 2;
+    constexpr int XW = TH * TN * 4;  // float4 per lane handed over
+    static_assert(NW * XW * 64 * 16 <= STAGES * STAGE, "exchange fits the ring");
+    float4* xb = reinterpret_cast<float4*>(smem);
+    const int partner = wave ^ (WM * WN);
+    barrier_only();
+    if (wk == 0)
+      xchg_put<TH, TH, TM, TN>(xb, acc, wave * XW, lane);
+    else
+      xchg_put<0, TH, TM, TN>(xb, acc, wave * XW, lane);
+    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): the writes are done
+    barrier_only();
+    if (wk == 0)
+      xchg_add<0, TH, TM, TN>(xb, acc, partner * XW, lane);
+    else
+      xchg_add<TH, TH, TM, TN>(xb, acc, partner * XW, lane);
+    const int64_t rw = m0 + wm * WTM, cw = n0 + wn * WTN;
+    if constexpr (EPI == EPI_DACT) {
+      static_assert(NW * 32 * (WTN + 4) * 4 <= STAGES * STAGE, "epilogue staging fits the ring");
+      __builtin_amdgcn_s_waitcnt(0xc07f);  // the exchange reads are done
+      barrier_only();
+      float* region = reinterpret_cast<float*>(smem) + wave * 32 * (WTN + 4);
+      if (wk == 0)
+        epilogue_lds<TO, EPI, TM, TN, 0, TH>(p, acc, region, rw, cw, lane);
+      else
+        epilogue_lds<TO, EPI, TM, TN, TH, TM>(p, acc, region, rw, cw, lane);
+    } else {
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int i = 0; i < TH; ++i) {
+          if (wk == 0)
+            store_block<bf16_t, TO, EPI>(p, acc[i][j], rw + i * 32, cw + j * 32, lane);
+          else
+            store_block<bf16_t, TO, EPI>(p, acc[TH + i][j], rw + (TH + i) * 32, cw + j * 32, lane);
+        }
+    }
+    return;
   }
 
   if (MASKABLE && mask_word != nullptr) {
@@ -759,7 +884,8 @@ __device__ __forceinline__ void async_gemm_tile(Params& p, const int tile, char*
     // The adjoint epilogue reads the saved activation (and a residual): it
     // goes through a per-wave LDS region once every wave is done with the
     // ring, so those reads and the stores move 8 consecutive columns at a time.
-    static_assert(NW * 32 * (WTN + 4) * 4 <= STAGES * STAGE, "epilogue staging fits the ring");
+    static_assert(WK > 1 || NW * 32 * (WTN + 4) * 4 <= STAGES * STAGE,
+                  "epilogue staging fits the ring");
     barrier_only();
     epilogue_lds<TO, EPI, TM, TN>(p, acc, reinterpret_cast<float*>(smem) + wave * 32 * (WTN + 4),
                                   m0 + wm * WTM, n0 + wn * WTN, lane);
@@ -812,6 +938,21 @@ __global__ __launch_bounds__(64 * WM * WN) void dlvm_gemm_async_kernel(Params p)
                     EARLY>(p, tile, smem);
 }
 
+// The same with two k-groups of WM x WN waves (WK = 2), sized for two
+// workgroups per compute unit (at most 256 registers per lane).
+template <typename TO, bool AK, bool BKM, int BM, int BN, int BK, int WM, int WN, int STAGES,
+          int EPI, bool PH2>
+__global__ __launch_bounds__(128 * WM * WN, 2) void dlvm_gemm_async_kgroup_kernel(Params p) {
+  __shared__ __attribute__((aligned(1024))) char smem[STAGES * (BM + BN) * 2 * BK];
+  const int tile = split_slice<bf16_t, AK, BKM>(p, static_cast<int>(blockIdx.x));
+  if (PH2 && p.splits <= 1)
+    async_gemm_tile<TO, AK, BKM, BM, BN, BK, WM, WN, STAGES, EPI, PH2, 0, true, false, 2>(p, tile,
+                                                                                          smem);
+  else
+    async_gemm_tile<TO, AK, BKM, BM, BN, BK, WM, WN, STAGES, EPI, false, 0, !PH2, false, 2>(
+        p, tile, smem);
+}
+
 // The two adjoint products of one dense layer in one launch (blocks [0, n1):
 // TN wrt the weights, the rest: NT wrt the input), as dlvm_gemm_pair_kernel.
 template <typename TO2, int BM, int BN, int BK, int WM, int WN, int STAGES>
@@ -841,6 +982,8 @@ __global__ __launch_bounds__(64 * WM * WN) void dlvm_gemm_async_pair_kernel(Para
 //        workgroups per CU); k-contiguous A only (NN, NT)
 //   17: 128 x 128, BK 64, 2 x 2 waves (64 x 64 per wave),   2 stages (64 KiB LDS: two
 //        workgroups per CU)
+//   18:  64 x 128, BK 64, 1 x 2 waves (64 x 64 per wave) in two k-groups, 3 stages (72
+//        KiB LDS: two workgroups per CU); k-contiguous A, no column sums (NN, NT)
 constexpr int kAsyncFirst = 10;
 
 template <typename TO, bool AK, bool BKM, int EPI, bool PH2 = false>
@@ -858,6 +1001,13 @@ hipError_t launch_async(const Params& p, int cfg, unsigned grid, hipStream_t s) 
     case 17:
       launch_kernel((dlvm_gemm_async_kernel<TO, AK, BKM, 128, 128, 64, 2, 2, 2, EPI, PH2>), dim3(grid), dim3(256), s, p);
       break;
+    case 18:
+      if constexpr (AK && EPI != EPI_DW) {
+        launch_kernel((dlvm_gemm_async_kgroup_kernel<TO, AK, BKM, 64, 128, 64, 1, 2, 3, EPI, PH2>), dim3(grid), dim3(256), s, p);
+        break;
+      } else {
+        return hipErrorInvalidValue;
+      }
     case 16:
       if constexpr (AK) {  // (an m-contiguous A needs 128-row tiles)
         launch_kernel((dlvm_gemm_async_kernel<TO, AK, BKM, 64, 128, 64, 2, 2, 3, EPI, PH2>), dim3(grid), dim3(256), s, p);
