@@ -36,7 +36,7 @@ constexpr TileShape kTiles[] = {
     {12, 128, 128, 0.0, 0.54, true, 0},  {13, 256, 256, 0.0, 0.88, true, 0},
     {14, 256, 256, 0.0, 0.89, true, 0},  {15, 256, 256, 0.0, 0.85, true, 0},
     {16, 64, 128, 0.0, 0.5, true, 0},    {17, 128, 128, 0.0, 0.54, true, 0},
-    {18, 64, 128, 0.0, 0.55, true, 0}};
+    {18, 64, 128, 0.0, 0.55, true, 0},   {19, 128, 128, 0.0, 0.56, true, 0}};
 
 // The register-staged kernel has one stage of loads in flight: a stage costs
 // at least one load round trip (measured on small float32 products).
@@ -213,6 +213,7 @@ GemmPlan choose(const GemmDesc& d, bool assume_aligned, int64_t capacity, int fo
     // 128 x 128 tile: 17.3 against 16.9 us and 11.6 against 15.7 us. On the
     // 4096 x 1024 products of a whole batch it gains nothing over 16 in the
     // step, and a 64-deep contraction is slower.
+    if (t.cfg == 19 && forced != 19) continue;
     if (t.cfg == 18 && (d.layout == Layout::TN ||
                         (forced != 18 && !(d.split_epilogue && d.splits_hint > 0))))
       continue;
@@ -253,19 +254,13 @@ GemmPlan choose(const GemmDesc& d, bool assume_aligned, int64_t capacity, int fo
     for (const TileShape& t : kTiles)
       if (t.cfg == 16) best = &t;
   }
-  // The same for a product w.r.t. the weights split into k-slices that fill
-  // the CUs once: the 128 x 128 tile with a 2-deep ring (64 KiB, two
-  // workgroups per CU) and twice the slices.
-  if (best != nullptr && best->cfg == 12 && best_s > 1 && 2 * best_s <= kMaxSplits &&
-      forced < 0 && fsplits < 0 && can_async && d.layout == Layout::TN && !two_phase(d) &&
-      d.splits_hint == 0 &&
-      ceil_div(d.M, 128) * ceil_div(d.N, 128) * best_s <= kComputeUnits &&
-      slice_k(d.K, 2 * best_s) >= kMinChunk &&
-      ceil_div(d.K, slice_k(d.K, 2 * best_s)) == 2 * best_s &&
-      split_need(d, 2 * best_s) <= capacity) {
+  // A product w.r.t. the weights split into k-slices that fill the CUs once:
+  // the 128 x 128 tile of two k-groups of waves, same slices.
+  if (best != nullptr && best->cfg == 12 && best_s > 1 && forced < 0 && fsplits < 0 &&
+      can_async && d.layout == Layout::TN && !two_phase(d) && d.splits_hint == 0 &&
+      ceil_div(d.M, 128) * ceil_div(d.N, 128) * best_s <= kComputeUnits) {
     for (const TileShape& t : kTiles)
-      if (t.cfg == 17) best = &t;
-    best_s *= 2;
+      if (t.cfg == 19) best = &t;
   }
   if (best == nullptr) {  // a forced configuration or split that cannot run is ignored
     if (forced >= 0 || fsplits > 0) return choose(d, assume_aligned, capacity, -1, -1);

@@ -277,11 +277,12 @@ __device__ __forceinline__ void mma_ktile(const char* __restrict__ As, const cha
 
 // NS consecutive 16-k steps of a k-tile from step s0 (a tile whose waves form
 // k-groups gives each group its own steps of every k-tile), the next step's
-// fragments read while the matrix cores work on the current ones.
-template <bool AK, bool BKM, int BM, int BN, int BK, int TM, int TN, int NS>
+// fragments read while the matrix cores work on the current ones; with CS and
+// do_cs, the column sums of the B fragments as in mma_ktile.
+template <bool AK, bool BKM, int BM, int BN, int BK, int TM, int TN, int NS, bool CS>
 __device__ __forceinline__ void mma_ksteps(const char* __restrict__ As, const char* __restrict__ Bs,
                                            int s0, int arow, int brow, int lane,
-                                           f32x16 (&acc)[TM][TN]) {
+                                           f32x16 (&acc)[TM][TN], float (&cs)[TN], bool do_cs) {
   bf16x8 af[2][TM], bfr[2][TN];
 #pragma unroll
   for (int i = 0; i < TM; ++i) af[0][i] = frag<AK, BM, BK>(As, arow + i * 32, s0, lane);
@@ -304,6 +305,20 @@ __device__ __forceinline__ void mma_ksteps(const char* __restrict__ As, const ch
       for (int j = 0; j < TN; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cur][i], bfr[cur][j], acc[i][j], 0, 0, 0);
     __builtin_amdgcn_sched_barrier(0);
+    if constexpr (CS) {
+      if (do_cs) {
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          const uint4 w = __builtin_bit_cast(uint4, bfr[cur][j]);
+          const uint32_t q[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            cs[j] += __uint_as_float(q[e] << 16);
+            cs[j] += __uint_as_float(q[e] & 0xffff0000u);
+          }
+        }
+      }
+    }
   }
 }
 
@@ -642,8 +657,8 @@ __device__ __forceinline__ void async_gemm_tile(Params& p, const int tile, char*
   static_assert(STAGES >= 2 && STAGES - 2 <= 3 && 3 * LOADS < 64, "pipeline depth");
   static_assert(AK || BM >= 128, "m-contiguous tile needs 256-byte k-rows");
   static_assert(BKM || BN >= 128, "n-contiguous tile needs 256-byte k-rows");
-  static_assert(WK == 1 || (WK == 2 && !EARLY && EPI != EPI_DW && TM % 2 == 0 && BK == 64),
-                "k-groups: two, without the early barrier or column sums");
+  static_assert(WK == 1 || (WK == 2 && !EARLY && TM % 2 == 0 && BK == 64),
+                "k-groups: two, without the early barrier");
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -812,8 +827,8 @@ __device__ __forceinline__ void async_gemm_tile(Params& p, const int tile, char*
       mma_ktile<AK, BKM, BM, BN, BK, TM, TN, EPI == EPI_DW, ILV>(As, Bs, wm * WTM, wn * WTN, lane,
                                                                  acc, cs, do_colsum);
     else
-      mma_ksteps<AK, BKM, BM, BN, BK, TM, TN, BK / 32>(As, Bs, wk * (BK / 32), wm * WTM, wn * WTN,
-                                                       lane, acc);
+      mma_ksteps<AK, BKM, BM, BN, BK, TM, TN, BK / 32, EPI == EPI_DW>(
+          As, Bs, wk * (BK / 32), wm * WTM, wn * WTN, lane, acc, cs, do_colsum);
   }
 
   if constexpr (WK == 2) {
@@ -824,20 +839,42 @@ __device__ __forceinline__ void async_gemm_tile(Params& p, const int tile, char*
     // group adds).
     constexpr int TH = TM / 2;
     constexpr int XW = TH * TN * 4;  // float4 per lane handed over
-    static_assert(NW * XW * 64 * 16 <= STAGES * STAGE, "exchange fits the ring");
+    // (then the column sums of group 1, TN floats per lane of each wave)
+    constexpr int XCS = NW * XW * 64 * 16;
+    static_assert(XCS + (EPI == EPI_DW ? WM * WN * TN * 64 * 4 : 0) <= STAGES * STAGE,
+                  "exchange fits the ring");
     float4* xb = reinterpret_cast<float4*>(smem);
+    float* xc = reinterpret_cast<float*>(smem + XCS);
     const int partner = wave ^ (WM * WN);
     barrier_only();
     if (wk == 0)
       xchg_put<TH, TH, TM, TN>(xb, acc, wave * XW, lane);
     else
       xchg_put<0, TH, TM, TN>(xb, acc, wave * XW, lane);
+    if constexpr (EPI == EPI_DW) {
+      if (do_colsum && wk == 1) {
+#pragma unroll
+        for (int j = 0; j < TN; ++j) xc[((wave - WM * WN) * TN + j) * 64 + lane] = cs[j];
+      }
+    }
     __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): the writes are done
     barrier_only();
     if (wk == 0)
       xchg_add<0, TH, TM, TN>(xb, acc, partner * XW, lane);
     else
       xchg_add<TH, TH, TM, TN>(xb, acc, partner * XW, lane);
+    if constexpr (EPI == EPI_DW) {
+      // group 0 completes the column sums: its partial plus group 1's
+      if (do_colsum && wk == 0) {
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          const float t0 = cs[j] + xc[(wave * TN + j) * 64 + lane];
+          const float t = t0 + __shfl_xor(t0, 32);
+          const int64_t col = n0 + wn * WTN + j * 32 + lane;
+          if (lane < 32 && col < p.nvec) p.colsum[col] = t;
+        }
+      }
+    }
     const int64_t rw = m0 + wm * WTM, cw = n0 + wn * WTN;
     if constexpr (EPI == EPI_DACT) {
       static_assert(NW * 32 * (WTN + 4) * 4 <= STAGES * STAGE, "epilogue staging fits the ring");
@@ -983,7 +1020,9 @@ __global__ __launch_bounds__(64 * WM * WN) void dlvm_gemm_async_pair_kernel(Para
 //   17: 128 x 128, BK 64, 2 x 2 waves (64 x 64 per wave),   2 stages (64 KiB LDS: two
 //        workgroups per CU)
 //   18:  64 x 128, BK 64, 1 x 2 waves (64 x 64 per wave) in two k-groups, 3 stages (72
-//        KiB LDS: two workgroups per CU); k-contiguous A, no column sums (NN, NT)
+//        KiB LDS: two workgroups per CU); k-contiguous A only (NN, NT)
+//   19: 128 x 128, BK 64, 2 x 2 waves (64 x 64 per wave) in two k-groups, 3 stages (96
+//        KiB LDS)
 constexpr int kAsyncFirst = 10;
 
 template <typename TO, bool AK, bool BKM, int EPI, bool PH2 = false>
@@ -1001,8 +1040,11 @@ hipError_t launch_async(const Params& p, int cfg, unsigned grid, hipStream_t s) 
     case 17:
       launch_kernel((dlvm_gemm_async_kernel<TO, AK, BKM, 128, 128, 64, 2, 2, 2, EPI, PH2>), dim3(grid), dim3(256), s, p);
       break;
+    case 19:
+      launch_kernel((dlvm_gemm_async_kgroup_kernel<TO, AK, BKM, 128, 128, 64, 2, 2, 3, EPI, PH2>), dim3(grid), dim3(512), s, p);
+      break;
     case 18:
-      if constexpr (AK && EPI != EPI_DW) {
+      if constexpr (AK) {
         launch_kernel((dlvm_gemm_async_kgroup_kernel<TO, AK, BKM, 64, 128, 64, 1, 2, 3, EPI, PH2>), dim3(grid), dim3(256), s, p);
         break;
       } else {

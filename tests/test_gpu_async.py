@@ -29,7 +29,7 @@ from helpers import TOL, assert_close, device, quant, rel_l2, to_dev, to_np
 
 pytestmark = pytest.mark.gpu
 
-CFGS = [10, 11, 12, 13, 14, 15, 16, 17, 18]
+CFGS = [10, 11, 12, 13, 14, 15, 16, 17, 18, 19]
 EXACT = 1e-5
 ROW_EXACT = 1e-4   # the same, for the worst single row (fewer terms average out)
 # (M, N, K): single tile with K = 8, exact tiles, ragged edges with K % 64 != 0,

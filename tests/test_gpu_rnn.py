@@ -52,7 +52,7 @@ def test_cell_forward(dtype, act, M, Kx, H):
 
 
 @pytest.mark.parametrize("dtype,cfg", [("f32", c) for c in (0, 1, 3, 4, 5)] +
-                         [("bf16", c) for c in (0, 1, 3, 4, 10, 11, 12, 13, 14, 16, 17, 18)])
+                         [("bf16", c) for c in (0, 1, 3, 4, 10, 11, 12, 13, 14, 16, 17, 18, 19)])
 def test_cell_forward_every_configuration(dtype, cfg, monkeypatch):
     """Each tile configuration forced on a two-phase product whose phases both
     end inside a k-tile and whose rows and columns are ragged (a configuration
