@@ -104,6 +104,30 @@ def test_layout_and_plan(name):
     assert len(tn) + len(pair) == wl.n_layers
 
 
+def test_k_group_tiles_where_the_planner_takes_them():
+    """The k-group tiles (configurations 18 and 19) run the products they were
+    measured on: the recurrent step's cell products and adjoints in two
+    k-slices on 18, the batch-4096 network's large weight adjoints in four
+    k-slices on 19; the forward and input-adjoint products of a whole batch
+    keep configuration 16, and the deep network keeps its 256 x 256 tiles."""
+    wl = workloads.RNN_WORKLOADS["r1"]
+    rnn = dl.Rnn(wl.steps, wl.in_width, wl.hidden, wl.act, wl.dtype, wl.wrt_x, wl.wrt_h0, wl.batch)
+    names = [p["name"] for p in rnn.plan(wl.batch)]
+    assert names.count("gemm_nn_bf16_64x128c18s2") == wl.steps
+    assert names.count("gemm_nt_bf16_64x128c18s2") == wl.steps - 1
+    assert names.count("split_epilogue") == 2 * wl.steps - 1
+    wl = workloads.WORKLOADS["c3"]
+    plan = dl.Model(wl.widths, wl.acts, wl.dtype, wl.loss, wl.wrt_x, wl.batch).plan(wl.batch)
+    big_tn = [p["name"] for p in plan if p["name"].startswith("gemm_tn") and p["N"] == 1024]
+    assert big_tn == ["gemm_tn_bf16_128x128c19s4"] * 2, big_tn
+    wide = [p["name"] for p in plan
+            if p["name"].startswith(("gemm_nn", "gemm_nt")) and p["M"] == 4096 and p["N"] == 1024]
+    assert wide and all(n.endswith("c16") for n in wide), wide
+    wl = workloads.WORKLOADS["c5"]
+    plan = dl.Model(wl.widths, wl.acts, wl.dtype, wl.loss, wl.wrt_x, wl.batch).plan(wl.batch)
+    assert all("c10" in p["name"] for p in plan if p["name"].startswith("gemm")), plan
+
+
 @pytest.mark.parametrize("name", sorted(workloads.WORKLOADS))
 def test_workspace_tensors(name):
     """dlvm_workspace_tensor (host only): the saved layer outputs, logits and
