@@ -741,7 +741,6 @@ dlvm_status plan_vjp(const dlvm_model* m, const void* params, const void* x, con
   const WsLayout w = ws_layout(m, batch);
   const int L = m->L;
   const int dt = m->dtype;
-  auto P = [&](int idx) { return param_ptr(m, params, m->offsets[idx]); };
   dlvm_status st = DLVM_OK;
   if ((st = plan_hidden_forward(m, params, x, batch, ws, w, run)) != DLVM_OK) return st;
   const int64_t C = m->widths[L], ldc = m->ldw[L - 1];
