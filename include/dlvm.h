@@ -117,7 +117,8 @@ dlvm_status dlvm_param_layout(const dlvm_model* m, int64_t* offsets, int64_t* ld
  * adjoint product wrt the weights whose output has too few tiles to occupy
  * the device is computed in k-slices and summed in slice order), the device
  * error flags and, for a bf16 network whose rectified hidden outputs are
- * produced and consumed by products on the 256 x 256 tile, one bit per
+ * produced and consumed by products on the same 256 x 256 or 64 x 128 tile
+ * configuration, one bit per
  * element of each such output: the rectifier's derivative (output > 0), which
  * the forward product writes and the adjoint product of the next layer reads
  * instead of the saved output (section 3.1.3; the results are the same;

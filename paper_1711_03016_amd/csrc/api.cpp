@@ -496,7 +496,9 @@ bool relu_mask_planned(const dlvm_model* m, const void* params, const void* x, i
   const GemmDesc f = hidden_desc(m, params, in, batch, at<void>(ws, w.H[l]),
                                  at<float>(ws, w.splitk), w.splitk_elems, l - 1);
   const GemmDesc a = input_adjoint_desc(m, params, batch, ws, w, l);
-  return dlvm::mask_ok(f, dlvm::plan_gemm(f)) && dlvm::mask_ok(a, dlvm::plan_gemm(a));
+  const dlvm::GemmPlan pf = dlvm::plan_gemm(f), pa = dlvm::plan_gemm(a);
+  // (the mask is in the accumulator order of one tile configuration)
+  return pf.cfg == pa.cfg && dlvm::mask_ok(f, pf) && dlvm::mask_ok(a, pa);
 }
 
 // The rectifier mask of H_l a call uses, or null.

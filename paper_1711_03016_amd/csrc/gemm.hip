@@ -1,5 +1,6 @@
 // Host side of the dense-layer products: choice of the tile configuration for
 // a given problem, and the launch.
+#include <algorithm>
 #include <cstdlib>
 
 #include "gemm_kernel.hpp"
@@ -293,11 +294,15 @@ GemmPlan plan_gemm(const GemmDesc& d) {
 
 bool mask_ok(const GemmDesc& d, const GemmPlan& pl) {
   if (d.dtype != BF16 || d.out_dtype != BF16 || d.act != ACT_RELU) return false;
-  if (pl.cfg != 10 || pl.splits != 1 || two_phase(d) || d.chain_epilogue) return false;
+  if ((pl.cfg != 10 && pl.cfg != 16) || pl.splits != 1 || two_phase(d) || d.chain_epilogue)
+    return false;
   return d.layout == Layout::NN || (d.layout == Layout::NT && d.residual == nullptr);
 }
 
-int64_t mask_bytes(int64_t M, int64_t N) { return ceil_div(M, 256) * ceil_div(N, 256) * 8192; }
+int64_t mask_bytes(int64_t M, int64_t N) {
+  // one bit per element of whole tiles: 256 x 256 (config 10) or 64 x 128 (16)
+  return std::max(ceil_div(M, 256) * ceil_div(N, 256) * 8192, ceil_div(M, 64) * ceil_div(N, 128) * 1024);
+}
 
 int64_t split_ws_elems(const GemmDesc& d) {
   if (d.layout != Layout::TN && !d.split_epilogue) return 0;

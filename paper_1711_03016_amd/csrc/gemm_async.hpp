@@ -694,18 +694,30 @@ __device__ __forceinline__ void async_gemm_tile(Params& p, const int tile, char*
   for (int j = 0; j < TN; ++j) cs[j] = 0.0f;
   const bool do_colsum = (EPI == EPI_DW) && (p.colsum != nullptr) && (tm == 0) && (wm == 0);
 
-  // Rectifier mask (256 x 256 tiles on 2 x 4 waves, one phase, bf16 output):
-  // the adjoint's 16-byte word is loaded before the contraction so that its
-  // latency hides behind it.
-  constexpr bool MASKABLE = BM == 256 && BN == 256 && WM == 2 && WN == 4 && WK == 1 && !PH2 &&
+  // Rectifier mask (256 x 256 tiles on 2 x 4 waves and 64 x 128 tiles on
+  // 2 x 2 waves, one phase, bf16 output): MW words per lane, 16 bits per
+  // 32 x 32 block; the adjoint's words are loaded before the contraction so
+  // that their latency hides behind it.
+  constexpr int MW = TM * TN / 2;
+  constexpr bool MASKABLE = ((BM == 256 && BN == 256 && WM == 2 && WN == 4) ||
+                             (BM == 64 && BN == 128 && WM == 2 && WN == 2)) &&
+                            WK == 1 && !PH2 &&
                             (EPI == EPI_DACT || (EPI == EPI_STORE && std::is_same<TO, bf16_t>::value));
   uint32_t* const mask_word =
       MASKABLE && p.mask != nullptr
-          ? p.mask + (static_cast<int64_t>(tm) * p.tiles_n + tn) * (4 * THREADS) + 4 * tid
+          ? p.mask + (static_cast<int64_t>(tm) * p.tiles_n + tn) * (MW * THREADS) + MW * tid
           : nullptr;
-  uint4 mk = make_uint4(0u, 0u, 0u, 0u);
+  uint32_t mk[MW > 0 ? MW : 1] = {};
   if constexpr (MASKABLE && EPI == EPI_DACT) {
-    if (mask_word != nullptr) mk = *reinterpret_cast<const uint4*>(mask_word);
+    static_assert(MW == 1 || MW == 4, "one or four mask words per lane");
+    if (mask_word != nullptr) {
+      if constexpr (MW == 4) {
+        const uint4 v = *reinterpret_cast<const uint4*>(mask_word);
+        mk[0] = v.x; mk[1] = v.y; mk[2] = v.z; mk[3] = v.w;
+      } else {
+        mk[0] = *mask_word;
+      }
+    }
   }
 
   auto issue = [&](int kt) {
@@ -901,8 +913,10 @@ __device__ __forceinline__ void async_gemm_tile(Params& p, const int tile, char*
 
   if (MASKABLE && mask_word != nullptr) {
     if constexpr (MASKABLE) {
-      static_assert(TM * TN == 8, "128 mask bits per lane");
-      uint32_t w[4] = {mk.x, mk.y, mk.z, mk.w};
+      static_assert(MW == 1 || MW == 4, "one or four mask words per lane");
+      uint32_t w[MW];
+#pragma unroll
+      for (int q = 0; q < MW; ++q) w[q] = mk[q];
 #pragma unroll
       for (int j = 0; j < TN; ++j)
 #pragma unroll
@@ -914,8 +928,12 @@ __device__ __forceinline__ void async_gemm_tile(Params& p, const int tile, char*
           else
             w[q >> 1] |= store_block_bits(p, acc[i][j], r0, c0, lane) << (16 * (q & 1));
         }
-      if constexpr (EPI == EPI_STORE)
-        *reinterpret_cast<uint4*>(mask_word) = make_uint4(w[0], w[1], w[2], w[3]);
+      if constexpr (EPI == EPI_STORE) {
+        if constexpr (MW == 4)
+          *reinterpret_cast<uint4*>(mask_word) = make_uint4(w[0], w[1], w[2], w[3]);
+        else
+          *mask_word = w[0];
+      }
     }
   } else if constexpr (EPI == EPI_DACT) {
     // The adjoint epilogue reads the saved activation (and a residual): it

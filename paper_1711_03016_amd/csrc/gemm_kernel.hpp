@@ -92,11 +92,13 @@ struct Params {
   float* partials;
   float inv_n;
   // Rectifier masks in accumulator order (direct-to-LDS kernel, 256 x 256
-  // tiles on 2 x 4 waves, unsplit; null: none). Tile (tm, tn) owns 512 x 4
-  // words from (tm * tiles_n + tn) * 2048; lane t of the workgroup owns words
-  // 4t .. 4t + 3, whose bit 16 q + r is element r of the lane's accumulator
-  // block q = i * 2 + j. EPI_STORE with the rectifier writes bit = (stored
-  // output > 0); EPI_DACT reads it in place of the saved activation.
+  // tiles on 2 x 4 waves or 64 x 128 tiles on 2 x 2 waves, unsplit; null:
+  // none). With W = TM * TN / 2 words per lane (4 and 1) and T threads, tile
+  // (tm, tn) owns T x W words from (tm * tiles_n + tn) * T * W; lane t of the
+  // workgroup owns words W t .. W t + W - 1, whose bit 16 q + r (in word q / 2
+  // for q odd, shifted) is element r of the lane's accumulator block
+  // q = i * TN + j. EPI_STORE with the rectifier writes bit = (stored output
+  // > 0); EPI_DACT reads it in place of the saved activation.
   uint32_t* mask;
 };
 

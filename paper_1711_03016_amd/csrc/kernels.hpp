@@ -78,9 +78,9 @@ struct GemmDesc {
   void* C2;
   float* partials;
   float inv_n;
-  // bf16 rectified layers on the 256 x 256 direct-to-LDS tile, unsplit
-  // (mask_ok): an NN product writes the rectifier bits of its output here, an
-  // NT product reads them in place of aux. Null: none.
+  // bf16 rectified layers on the 256 x 256 or 64 x 128 direct-to-LDS tile,
+  // unsplit (mask_ok): an NN product writes the rectifier bits of its output
+  // here, an NT product reads them in place of aux. Null: none.
   uint32_t* mask;
 };
 
@@ -101,11 +101,14 @@ int64_t split_ws_elems(const GemmDesc& d);
 GemmPlan plan_gemm(const GemmDesc& d);
 
 // Whether a product so planned can write (NN) or read (NT) rectifier masks
-// (GemmDesc::mask): bf16 operands and output, the rectifier, the 256 x 256
-// direct-to-LDS tile (configuration 10), one k-slice, one phase, no residual.
-// Both products of a layer output must pass for the mask to be used.
+// (GemmDesc::mask): bf16 operands and output, the rectifier, the 256 x 256 or
+// 64 x 128 direct-to-LDS tile (configurations 10 and 16: the mask is in the
+// tile's accumulator order), one k-slice, one phase, no residual. Both
+// products of a layer output must pass, on the same configuration, for the
+// mask to be used.
 bool mask_ok(const GemmDesc& d, const GemmPlan& plan);
-// Bytes of the mask of an M x N output (8 KiB per 256 x 256 tile).
+// Bytes of the mask of an M x N output (one bit per element of whole tiles of
+// either configuration: 8 KiB per 256 x 256 tile, 1 KiB per 64 x 128).
 int64_t mask_bytes(int64_t M, int64_t N);
 
 // Between begin and end (nestable; one library call), the tuning variables

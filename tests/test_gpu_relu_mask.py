@@ -5,7 +5,8 @@ the rectifier's adjoint needs only the sign of its saved output).
 
 The masked path must give bitwise the results of the saved-output path
 (DLVM_RELU_MASK=0), on ragged shapes, through the gradient, the seedable
-gradient and the checkpointed plan, and agree with the oracle.
+gradient and the checkpointed plan, and agree with the oracle, on both tile
+configurations that write masks (10: 256 x 256, 16: 64 x 128).
 """
 from dataclasses import replace
 
@@ -26,7 +27,7 @@ def _wl(widths, batch):
 
 
 def _mask_bytes(M, N):
-    return -(-M // 256) * -(-N // 256) * 8192
+    return max(-(-M // 256) * -(-N // 256) * 8192, -(-M // 64) * -(-N // 128) * 1024)
 
 
 @pytest.mark.parametrize("masks", ["on", "off"])
@@ -48,7 +49,7 @@ def test_workspace_reserves_masks_for_the_deep_network(masks, monkeypatch):
 @pytest.mark.parametrize("widths,acts,dtype", [
     ((784, 512, 512, 10), ("relu", "relu", "none"), "f32"),         # float32 network
     ((4096, 4096, 4096, 10), ("tanh", "sigmoid", "none"), "bf16"),  # not rectified
-    ((784, 1024, 1024, 10), ("relu", "relu", "none"), "bf16"),      # products on smaller tiles
+    ((784, 2048, 2048, 10), ("relu", "relu", "none"), "bf16"),      # products on 256 x 128 tiles
 ])
 def test_no_masks_where_products_do_not_qualify(widths, acts, dtype, monkeypatch):
     m = dl.Model(widths, acts, dtype, "softmax_ce", False, 4096)
@@ -106,15 +107,16 @@ def _gradient(wl, x, params, y, ckpt=1, seed=None):
 
 
 @pytest.mark.gpu
+@pytest.mark.parametrize("cfg", ["10", "16"])
 @pytest.mark.parametrize("widths,batch", [
     ((264, 520, 296, 10), 1000),     # ragged rows and columns, several tiles
     ((264, 520, 296, 10), 7),        # one partial tile row
     ((520, 256, 512, 264, 40), 512), # whole tiles, three rectified outputs
 ])
 @pytest.mark.parametrize("entry", ["gradient", "vjp"])
-def test_masked_path_is_bitwise_the_saved_output_path(widths, batch, entry, monkeypatch):
+def test_masked_path_is_bitwise_the_saved_output_path(widths, batch, entry, cfg, monkeypatch):
     import torch
-    monkeypatch.setenv("DLVM_GEMM_CONFIG", "10")   # the 256 x 256 tile on every product
+    monkeypatch.setenv("DLVM_GEMM_CONFIG", cfg)    # the tile on every product that can run it
     wl = _wl(widths, batch)
     x, params, y = workloads.make_inputs(wl, bias_scale=0.1)
     seed = None
@@ -130,11 +132,12 @@ def test_masked_path_is_bitwise_the_saved_output_path(widths, batch, entry, monk
 
 
 @pytest.mark.gpu
-def test_masked_path_with_checkpointing(monkeypatch):
+@pytest.mark.parametrize("cfg", ["10", "16"])
+def test_masked_path_with_checkpointing(cfg, monkeypatch):
     """Recomputed segments rewrite their masks: every segment length gives
     bitwise the keep-everything result."""
     import torch
-    monkeypatch.setenv("DLVM_GEMM_CONFIG", "10")
+    monkeypatch.setenv("DLVM_GEMM_CONFIG", cfg)
     wl = _wl((264,) + (296,) * 6 + (10,), 600)
     x, params, y = workloads.make_inputs(wl, bias_scale=0.1)
     _, *ref = _gradient(wl, x, params, y)
@@ -145,8 +148,9 @@ def test_masked_path_with_checkpointing(monkeypatch):
 
 
 @pytest.mark.gpu
-def test_masked_path_against_oracle(monkeypatch):
-    monkeypatch.setenv("DLVM_GEMM_CONFIG", "10")
+@pytest.mark.parametrize("cfg", ["10", "16"])
+def test_masked_path_against_oracle(cfg, monkeypatch):
+    monkeypatch.setenv("DLVM_GEMM_CONFIG", cfg)
     wl = _wl((264, 520, 296, 10), 1000)
     x, params, y = workloads.make_inputs(wl, bias_scale=0.1)
     m, loss, dP, dx, _ = _gradient(wl, x, params, y)
