@@ -99,6 +99,17 @@ bool xl_ok(const GemmDesc& d) {
          ac <= d.lda && bc <= d.ldb;
 }
 
+// The same for the k-slices of a two-phase (forward) product, each of which
+// reads one phase: A's M x K1 block (stride lda), A2's M x (K - K1) block
+// (stride lda2) and B.
+bool xl_phases_ok(const GemmDesc& d) {
+  if (!async_ok(d) || !two_phase(d) || d.layout != Layout::NN) return false;
+  const int64_t lim = int64_t(1) << 31;
+  return (d.M + 256) * d.lda * 2 + 512 < lim && (d.M + 256) * d.lda2 * 2 + 512 < lim &&
+         (d.K + 256) * d.ldb * 2 + 512 < lim && d.K1 <= d.lda && d.K - d.K1 <= d.lda2 &&
+         d.N <= d.ldb;
+}
+
 // k per slice when K is split `splits` ways (a multiple of 64, so every
 // slice but the last is whole k-tiles for every kernel).
 int64_t slice_k(int64_t K, int splits) { return ceil_div(ceil_div(K, splits), 64) * 64; }
@@ -220,8 +231,10 @@ GemmPlan choose(const GemmDesc& d, bool assume_aligned, int64_t capacity, int fo
       continue;
     if (forced >= 0 && t.cfg != forced) continue;
     for (int sp = 1; sp <= kMaxSplits; sp *= 2) {
-      // a two-phase product's slices must not straddle its phase boundary
+      // a two-phase product's slices must not straddle its phase boundary,
+      // and on the direct-to-LDS tiles they load through descriptors
       if (sp > 1 && two_phase(d) && d.K1 % slice_k(d.K, sp) != 0) continue;
+      if (sp > 1 && two_phase(d) && t.async && !assume_aligned && !xl_phases_ok(d)) continue;
       const bool forcing = fsplits > 0 && d.split_epilogue;  // (overrides the caller's split)
       if (!forcing && d.splits_hint > 0 && split_need(d, d.splits_hint) <= capacity) {
         // the caller's split (a multiple of 64 k per slice, whole slices)
@@ -339,7 +352,7 @@ void vector_ok(const GemmDesc& d, bool& va, bool& vb) {
 // their extents below 2^31 bytes): the bf16 direct-to-LDS and four-wave
 // kernels, for one-phase products.
 bool buffer_loads(const GemmDesc& d, const GemmPlan& pl) {
-  if (two_phase(d)) return false;
+  if (two_phase(d) && pl.splits <= 1) return false;  // (unsplit: computed addresses)
   for (const TileShape& t : kTiles)
     if (t.cfg == pl.cfg) return t.async;
   return false;
@@ -379,7 +392,12 @@ gemm::Params make_params(const GemmDesc& d, const GemmPlan& pl) {
   }
   // Extents for the buffer-descriptor loads (the planner runs these kernels
   // only where xl_ok holds; launch_gemm refuses them otherwise).
-  if (buffer_loads(d, pl)) {
+  p.a2_bytes = 0;
+  if (buffer_loads(d, pl) && two_phase(d)) {  // k-slices of a two-phase forward product
+    p.a_bytes = static_cast<uint32_t>(extent_bytes(d.M, d.K1, d.lda, 2));
+    p.a2_bytes = static_cast<uint32_t>(extent_bytes(d.M, d.K - d.K1, d.lda2, 2));
+    p.b_bytes = static_cast<uint32_t>(extent_bytes(d.K, d.N, d.ldb, 2));
+  } else if (buffer_loads(d, pl)) {
     int64_t ar, ac, br, bc;
     operand_dims(d, ar, ac, br, bc);
     p.a_bytes = static_cast<uint32_t>(extent_bytes(ar, ac, d.lda, 2));
@@ -400,7 +418,8 @@ hipError_t launch_gemm(const GemmDesc& d, const GemmPlan& pl, hipStream_t s) {
   bool va, vb;
   vector_ok(d, va, vb);
   if (d.mask != nullptr && (!mask_ok(d, pl) || !aligned16(d.mask))) return hipErrorInvalidValue;
-  if (buffer_loads(d, pl) && !xl_ok(d)) return hipErrorInvalidValue;
+  if (buffer_loads(d, pl) && !(two_phase(d) ? xl_phases_ok(d) : xl_ok(d)))
+    return hipErrorInvalidValue;
   const gemm::Params p = make_params(d, pl);
   const unsigned grid = grid_of(pl);
   const int out = pl.splits > 1 ? F32 : d.out_dtype;  // split slices: float32 partials

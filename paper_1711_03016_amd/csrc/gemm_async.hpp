@@ -738,9 +738,10 @@ __device__ __forceinline__ void async_gemm_tile(Params& p, const int tile, char*
   // adjoint 510 -> 482-485 (the computed addresses cost about 100 vector
   // instructions per wave and k-tile between the barrier and the first matrix
   // instruction); the loads spread over the k-tile's 16-k steps instead were
-  // slower than issuing them together. Two-phase products compute every
-  // load's clamped address (issue above), and so does BUFOK = false (a slice
-  // of a two-phase product may read A2, whose extent the host does not pass).
+  // slower than issuing them together. An unsplit two-phase product computes
+  // every load's clamped address (issue above), and so does BUFOK = false; a
+  // k-slice of a two-phase product lies in one phase and loads through a
+  // descriptor of that phase's operand (the host passes both extents).
   constexpr bool BUF = BUFOK && !PH2;
   constexpr int LA = A_BYTES / 1024 / NW, LB = B_BYTES / 1024 / NW;
   uint32_t offa[BUF ? LA : 1], offb[BUF ? LB : 1];
@@ -985,11 +986,12 @@ __global__ __launch_bounds__(64 * WM * WN) void dlvm_gemm_async_kernel(Params p)
   constexpr int ILV = async_ilv<BM, BN, BK>();
   constexpr bool EARLY = !PH2 && async_early<BM, BN, BK, STAGES>();
   const int tile = split_slice<bf16_t, AK, BKM>(p, static_cast<int>(blockIdx.x));
-  // a k-slice of a split two-phase product lies in one phase
+  // a k-slice of a split two-phase product lies in one phase (A or A2, whose
+  // extents the host passes as well: buffer-descriptor loads)
   if (PH2 && p.splits <= 1)
     async_gemm_tile<TO, AK, BKM, BM, BN, BK, WM, WN, STAGES, EPI, PH2, ILV>(p, tile, smem);
-  else  // (a slice of a two-phase product may read A2: computed addresses)
-    async_gemm_tile<TO, AK, BKM, BM, BN, BK, WM, WN, STAGES, EPI, false, EARLY ? 2 : ILV, !PH2,
+  else
+    async_gemm_tile<TO, AK, BKM, BM, BN, BK, WM, WN, STAGES, EPI, false, EARLY ? 2 : ILV, true,
                     EARLY>(p, tile, smem);
 }
 
@@ -1004,7 +1006,7 @@ __global__ __launch_bounds__(128 * WM * WN, 2) void dlvm_gemm_async_kgroup_kerne
     async_gemm_tile<TO, AK, BKM, BM, BN, BK, WM, WN, STAGES, EPI, PH2, 0, true, false, 2>(p, tile,
                                                                                           smem);
   else
-    async_gemm_tile<TO, AK, BKM, BM, BN, BK, WM, WN, STAGES, EPI, false, 0, !PH2, false, 2>(
+    async_gemm_tile<TO, AK, BKM, BM, BN, BK, WM, WN, STAGES, EPI, false, 0, true, false, 2>(
         p, tile, smem);
 }
 

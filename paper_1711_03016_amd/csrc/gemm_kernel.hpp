@@ -72,6 +72,7 @@ struct Params {
   int tiles_m, tiles_n;
   int64_t nvec;  // entries of bias / colsum (columns n >= nvec have none)
   uint32_t a_bytes, b_bytes;  // extents of A and B in bytes (buffer-descriptor kernels)
+  uint32_t a2_bytes;          // extent of A2 (k-slices of a two-phase product), or 0
   // Split reduction (adjoint wrt the weights): workgroup b handles tile
   // b % (tiles_m * tiles_n) over k-slice b / (tiles_m * tiles_n) of k_chunk
   // k, and writes its float32 partial product (and partial column sums) at
@@ -148,6 +149,7 @@ __device__ __forceinline__ int split_slice(Params& p, int bid) {
       p.A = p.A2;
       p.lda = p.lda2;
       sa = AK ? k0 - p.K1 : (k0 - p.K1) * p.lda2;
+      if (p.a_bytes != 0u) p.a_bytes = p.a2_bytes;
     }
     p.A = static_cast<const T*>(p.A) + sa;
     p.B = static_cast<const T*>(p.B) + sb;
