@@ -197,14 +197,16 @@ def test_rnn_backward_is_deterministic():
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("splits", [2, 4])
-def test_split_cell_and_recurrent_products(dtype, splits, monkeypatch):
+@pytest.mark.parametrize("H", [512, 480])
+def test_split_cell_and_recurrent_products(dtype, splits, H, monkeypatch):
     """The cell products and recurrent adjoints computed in k-slices (forced),
     summed in slice order with the epilogue (bias + activation, residual +
-    act') applied after the sum; the cell's slices fall on its phase boundary.
-    Two runs are bitwise equal."""
+    act') applied after the sum; the cell's slices fall on its phase boundary
+    (with H = 480 the second phase ends inside a k-tile, and rows and columns
+    are ragged). Two runs are bitwise equal."""
     monkeypatch.setenv("DLVM_GEMM_SPLITS", str(splits))
-    wl, inputs = _case(4, 512, 512, 100, dtype, "tanh", seed=21)
-    m = dl.Rnn(4, 512, 512, "tanh", dtype, True, True, 100)
+    wl, inputs = _case(4, 512, H, 100, dtype, "tanh", seed=21)
+    m = dl.Rnn(4, 512, H, "tanh", dtype, True, True, 100)
     names = [p["name"] for p in m.plan(100)]
     assert any(n.startswith("gemm_nn") and n.endswith(f"s{splits}") for n in names)
     assert names.count("split_epilogue") >= 4
