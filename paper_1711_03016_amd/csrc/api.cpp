@@ -728,9 +728,10 @@ dlvm_status plan_gradient(const dlvm_model* m, const void* params, const void* x
                  "softmax cross-entropy launch");
   }
   if (st != DLVM_OK) return st;
-  if ((st = plan_adjoint_layers(m, params, x, batch, dparams, dx, ws, w, run)) != DLVM_OK)
-    return st;
-  return finalize();
+  // The loss and its flags right away, while the loss kernel's partials are
+  // still in the caches (nothing in the adjoint sweep reads or writes them).
+  if ((st = finalize()) != DLVM_OK) return st;
+  return plan_adjoint_layers(m, params, x, batch, dparams, dx, ws, w, run);
 }
 
 // The launches of one seedable gradient call (Fig. 3's seedable

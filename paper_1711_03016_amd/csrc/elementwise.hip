@@ -808,9 +808,10 @@ hipError_t launch_finalize(const float* partials, const int32_t* bad, int n, flo
 
 hipError_t launch_sgd(int dtype, int64_t n, void* params, float* master, const float* grads,
                       float lr, hipStream_t s) {
-  // one block per kSgdChunk float4 chunks, up to 16 blocks per compute unit
+  // one block per kSgdChunk float4 chunks, up to 32 blocks per compute unit
+  // (measured on 138M bf16 parameters: 8192 blocks 326 us, 4096 blocks 334)
   int64_t nb64 = ((n / 4) + kSgdChunk - 1) / kSgdChunk;
-  nb64 = nb64 < 1 ? 1 : (nb64 > 4096 ? 4096 : nb64);
+  nb64 = nb64 < 1 ? 1 : (nb64 > 8192 ? 8192 : nb64);
   const unsigned nb = static_cast<unsigned>(nb64);
   if (dtype == F32)
     launch_kernel(dlvm_sgd_f32_kernel, dim3(nb), dim3(kBlock), s, n,
